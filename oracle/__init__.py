@@ -1,0 +1,166 @@
+"""fp64 CPU oracle for paged grouped-query decode attention.
+
+TEST INFRASTRUCTURE ONLY.  Only the test-suite, the smoke check and the
+benchmark's CPU-baseline leg may import this package.  It shares no code with
+the GPU library and imports nothing from it.
+
+The arithmetic lives in ``decode_attn_oracle.c`` (plain C, fp64); this module
+only compiles it with gcc and marshals numpy arrays through ctypes.  The
+operation is the scaled dot-product attention of one decode step over a paged
+KV cache (the paper's rollout phase, Sec. 2.1; its paged KV cache, Sec. 1):
+``out[b,h] = softmax(scale * q[b,h] . K_b^T) V_b`` with ``K_b``/``V_b`` the
+first ``seq_lens[b]`` cached tokens of sequence ``b``, gathered through the
+block table, and KV head ``h // (Hq // Hkv)``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "decode_attn_oracle.c")
+LIB_PATH = os.path.join(_HERE, "libdecode_attn_oracle.so")
+
+KV_BF16 = 0
+KV_FP8_E4M3 = 1
+
+OK = 0
+ERR_ARG = 1
+ERR_PRECONDITION = 2
+ERR_NOMEM = 3
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (-O2, OpenMP, no FMA contraction)."""
+    if not force and os.path.exists(LIB_PATH):
+        return LIB_PATH
+    tmp = LIB_PATH + ".tmp%d" % os.getpid()
+    cmd = ["gcc", "-O2", "-std=c11", "-Wall", "-Wextra", "-fopenmp",
+           "-ffp-contract=off", "-fPIC", "-shared", _SRC, "-o", tmp, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, LIB_PATH)
+    return LIB_PATH
+
+
+class _Problem(ctypes.Structure):
+    _fields_ = [
+        ("batch", ctypes.c_int32),
+        ("num_q_heads", ctypes.c_int32),
+        ("num_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("page_size", ctypes.c_int32),
+        ("kv_dtype", ctypes.c_int32),
+        ("max_pages", ctypes.c_int32),
+        ("num_pages", ctypes.c_int64),
+        ("scale", ctypes.c_double),
+        ("q", ctypes.c_void_p),
+        ("k_pool", ctypes.c_void_p),
+        ("v_pool", ctypes.c_void_p),
+        ("k_scale", ctypes.c_void_p),
+        ("v_scale", ctypes.c_void_p),
+        ("block_table", ctypes.c_void_p),
+        ("seq_lens", ctypes.c_void_p),
+    ]
+
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        # RL_ORACLE_LIB points the tests at a deliberately mutated build of the
+        # oracle, to show that the pins catch plausible mistakes.
+        path = os.environ.get("RL_ORACLE_LIB") or LIB_PATH
+        if path == LIB_PATH and not os.path.exists(LIB_PATH):
+            build()
+        lib = ctypes.CDLL(path)
+        lib.rl_oracle_decode_attn.argtypes = [
+            ctypes.POINTER(_Problem), ctypes.c_void_p, ctypes.c_int64,
+            ctypes.c_void_p]
+        lib.rl_oracle_decode_attn.restype = ctypes.c_int
+        lib.rl_oracle_e4m3_to_double.argtypes = [ctypes.c_uint8]
+        lib.rl_oracle_e4m3_to_double.restype = ctypes.c_double
+        lib.rl_oracle_bf16_to_double.argtypes = [ctypes.c_uint16]
+        lib.rl_oracle_bf16_to_double.restype = ctypes.c_double
+        lib.rl_oracle_max_threads.argtypes = []
+        lib.rl_oracle_max_threads.restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def _c(a, dtype):
+    a = np.ascontiguousarray(a)
+    if a.dtype != dtype:
+        raise TypeError("expected %s, got %s" % (np.dtype(dtype), a.dtype))
+    return a
+
+
+def decode_attention(q_bits, k_pool, v_pool, block_table, seq_lens, *,
+                     num_kv_heads, scale, kv_dtype=KV_BF16, k_scale=None,
+                     v_scale=None, rows=None):
+    """Attention rows in fp64.
+
+    q_bits      uint16 [B, Hq, D] bf16 bit patterns
+    k_pool/v_pool uint16 (bf16 bits) or uint8 (e4m3 codes) [P, Hkv, page, D]
+    block_table int32 [B, max_pages];  seq_lens int32 [B]
+    rows        None (all (b, h), returns [B, Hq, D]) or int array [n, 2] of
+                (b, h) pairs (returns [n, D]).
+    """
+    lib = _load()
+    q_bits = _c(q_bits, np.uint16)
+    pool_dtype = np.uint16 if kv_dtype == KV_BF16 else np.uint8
+    k_pool = _c(k_pool, pool_dtype)
+    v_pool = _c(v_pool, pool_dtype)
+    block_table = _c(block_table, np.int32)
+    seq_lens = _c(seq_lens, np.int32)
+    B, Hq, D = q_bits.shape
+    P, Hkv, page, D2 = k_pool.shape
+    if D2 != D or v_pool.shape != k_pool.shape or Hkv != num_kv_heads:
+        raise ValueError("pool shape does not match q / num_kv_heads")
+    if block_table.ndim != 2 or block_table.shape[0] != B or seq_lens.shape != (B,):
+        raise ValueError("block_table / seq_lens shape")
+    if kv_dtype == KV_FP8_E4M3:
+        k_scale = _c(k_scale, np.float32)
+        v_scale = _c(v_scale, np.float32)
+        if k_scale.shape != (P, Hkv) or v_scale.shape != (P, Hkv):
+            raise ValueError("scale shape")
+    prob = _Problem(
+        batch=B, num_q_heads=Hq, num_kv_heads=Hkv, head_dim=D, page_size=page,
+        kv_dtype=kv_dtype, max_pages=block_table.shape[1], num_pages=P,
+        scale=float(scale), q=q_bits.ctypes.data, k_pool=k_pool.ctypes.data,
+        v_pool=v_pool.ctypes.data,
+        k_scale=k_scale.ctypes.data if kv_dtype == KV_FP8_E4M3 else None,
+        v_scale=v_scale.ctypes.data if kv_dtype == KV_FP8_E4M3 else None,
+        block_table=block_table.ctypes.data, seq_lens=seq_lens.ctypes.data)
+    if rows is None:
+        out = np.empty((B, Hq, D), dtype=np.float64)
+        rc = lib.rl_oracle_decode_attn(ctypes.byref(prob), None, 0,
+                                       out.ctypes.data)
+    else:
+        rows = _c(np.asarray(rows, dtype=np.int32).reshape(-1, 2), np.int32)
+        out = np.empty((rows.shape[0], D), dtype=np.float64)
+        rc = lib.rl_oracle_decode_attn(ctypes.byref(prob), rows.ctypes.data,
+                                       rows.shape[0], out.ctypes.data)
+    if rc != OK:
+        raise OracleError("oracle failed with code %d" % rc)
+    return out
+
+
+def e4m3_to_double(code: int) -> float:
+    return _load().rl_oracle_e4m3_to_double(int(code))
+
+
+def bf16_to_double(bits: int) -> float:
+    return _load().rl_oracle_bf16_to_double(int(bits))
+
+
+def max_threads() -> int:
+    return _load().rl_oracle_max_threads()

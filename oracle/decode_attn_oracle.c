@@ -1,0 +1,222 @@
+/*
+ * decode_attn_oracle.c -- fp64 CPU oracle for one decode step of paged
+ * grouped-query attention.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file exists so that tests, the smoke check
+ * and the CPU-baseline leg of the benchmark can check the GPU library.  No
+ * product code may include, link or call it, and it includes and links
+ * nothing from the GPU library: the two share no source, header, table or
+ * helper.
+ *
+ * What is computed.  The paper (arXiv 2512.22492, Sec. 1 and Sec. 2.1) places
+ * rollout generation in an inference engine with a paged KV cache
+ * (PagedAttention, cited in Sec. 1 and Sec. 9); it prints no attention
+ * formula.  The operation is the textbook scaled dot-product attention of one
+ * new query token per sequence against that sequence's cached keys/values,
+ * with grouped KV heads:
+ *
+ *     out[b,h,:] = sum_t softmax_t( scale * <q[b,h,:], K[b,kvh,t,:]> ) V[b,kvh,t,:]
+ *     kvh = floor(h / G),  G = Hq / Hkv,  t = 0 .. seq_lens[b]-1
+ *
+ * where the cached token t of sequence b lives in physical page
+ * block_table[b][t / page_size], slot t % page_size, and a pool is laid out
+ * [num_pages][Hkv][page_size][D].  For fp8 pools every (page, kv head) slab
+ * carries one fp32 scale, and a stored code c stands for e4m3(c) * scale.
+ *
+ * The oracle favours being checkable by eye over speed: every score is formed
+ * in fp64 from the exactly decoded inputs, summed over d in increasing order,
+ * then the maximum is subtracted, exponentiated, normalised and the weighted
+ * sum of values formed, again in fp64.  Nothing is blocked or fused.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include "decode_attn_oracle.h"
+
+/* bf16 is the upper half of an IEEE binary32; widening is exact. */
+static double oracle_bf16_to_double(uint16_t bits)
+{
+    uint32_t u = (uint32_t)bits << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+}
+
+/*
+ * OCP 8-bit floating point, E4M3 ("FN": finite, no infinities): sign bit,
+ * 4 exponent bits with bias 7, 3 mantissa bits.  Exponent field 0 holds the
+ * subnormals m/8 * 2^-6; the single code S.1111.111 is NaN; every other code
+ * with exponent field 15 is a normal number (so the largest is 448).
+ */
+double rl_oracle_e4m3_to_double(uint8_t code)
+{
+    const int sign = (code >> 7) & 1;
+    const int e = (code >> 3) & 0xF;
+    const int m = code & 0x7;
+    double mag;
+    if (e == 0xF && m == 0x7)
+        return NAN;
+    if (e == 0)
+        mag = ldexp((double)m / 8.0, -6);
+    else
+        mag = ldexp(1.0 + (double)m / 8.0, e - 7);
+    return sign ? -mag : mag;
+}
+
+double rl_oracle_bf16_to_double(uint16_t bits)
+{
+    return oracle_bf16_to_double(bits);
+}
+
+/* Decoded element d of token slot `slot` in slab (page, kvh) of a pool. */
+static double pool_element(const rl_oracle_problem* p, const void* pool,
+                           const float* slab_scale, int64_t page, int kvh,
+                           int slot, int d)
+{
+    const int64_t idx =
+        (((int64_t)page * p->num_kv_heads + kvh) * p->page_size + slot) *
+            (int64_t)p->head_dim + d;
+    if (p->kv_dtype == RL_ORACLE_KV_BF16)
+        return oracle_bf16_to_double(((const uint16_t*)pool)[idx]);
+    return rl_oracle_e4m3_to_double(((const uint8_t*)pool)[idx]) *
+           (double)slab_scale[(int64_t)page * p->num_kv_heads + kvh];
+}
+
+/* Checks the preconditions of one (b, h) row; nonzero when they hold. */
+static int row_is_valid(const rl_oracle_problem* p, int b, int h)
+{
+    if (b < 0 || b >= p->batch || h < 0 || h >= p->num_q_heads)
+        return 0;
+    const int L = p->seq_lens[b];
+    if (L <= 0)
+        return 1;
+    if ((int64_t)L > (int64_t)p->max_pages * p->page_size)
+        return 0;
+    const int used_pages = (L + p->page_size - 1) / p->page_size;
+    for (int j = 0; j < used_pages; ++j) {
+        const int32_t page = p->block_table[(int64_t)b * p->max_pages + j];
+        if (page < 0 || (int64_t)page >= p->num_pages)
+            return 0;
+    }
+    return 1;
+}
+
+/*
+ * One output row out[b,h,:], written to dst[0..D-1].  `scores` is caller
+ * scratch of at least seq_lens[b] doubles.
+ */
+static void attend_one_row(const rl_oracle_problem* p, int b, int h,
+                           double* scores, double* dst)
+{
+    const int D = p->head_dim;
+    const int G = p->num_q_heads / p->num_kv_heads;
+    const int kvh = h / G;
+    const int L = p->seq_lens[b];
+    const int32_t* pages = p->block_table + (int64_t)b * p->max_pages;
+    const uint16_t* qrow =
+        (const uint16_t*)p->q + ((int64_t)b * p->num_q_heads + h) * D;
+
+    if (L <= 0) {
+        for (int d = 0; d < D; ++d)
+            dst[d] = 0.0;
+        return;
+    }
+
+    /* Scores s_t = scale * sum_d q[d] * k_t[d]. */
+    for (int t = 0; t < L; ++t) {
+        const int64_t page = pages[t / p->page_size];
+        const int slot = t % p->page_size;
+        double dot = 0.0;
+        for (int d = 0; d < D; ++d)
+            dot += oracle_bf16_to_double(qrow[d]) *
+                   pool_element(p, p->k_pool, p->k_scale, page, kvh, slot, d);
+        scores[t] = p->scale * dot;
+    }
+
+    /* Softmax weights w_t = exp(s_t - max_s) / sum_u exp(s_u - max_s). */
+    double smax = scores[0];
+    for (int t = 1; t < L; ++t)
+        if (scores[t] > smax)
+            smax = scores[t];
+    double z = 0.0;
+    for (int t = 0; t < L; ++t) {
+        scores[t] = exp(scores[t] - smax);
+        z += scores[t];
+    }
+
+    /* out[d] = sum_t w_t * v_t[d]. */
+    for (int d = 0; d < D; ++d)
+        dst[d] = 0.0;
+    for (int t = 0; t < L; ++t) {
+        const int64_t page = pages[t / p->page_size];
+        const int slot = t % p->page_size;
+        const double w = scores[t] / z;
+        for (int d = 0; d < D; ++d)
+            dst[d] += w * pool_element(p, p->v_pool, p->v_scale, page, kvh,
+                                       slot, d);
+    }
+}
+
+int rl_oracle_decode_attn(const rl_oracle_problem* p, const int32_t* rows,
+                          int64_t num_rows, double* out)
+{
+    if (p == NULL || out == NULL || p->q == NULL || p->k_pool == NULL ||
+        p->v_pool == NULL || p->block_table == NULL || p->seq_lens == NULL)
+        return RL_ORACLE_ERR_ARG;
+    if (p->batch < 0 || p->num_q_heads <= 0 || p->num_kv_heads <= 0 ||
+        p->num_q_heads % p->num_kv_heads != 0 || p->head_dim <= 0 ||
+        p->page_size <= 0 || p->max_pages < 0 || p->num_pages < 0)
+        return RL_ORACLE_ERR_ARG;
+    if (p->kv_dtype != RL_ORACLE_KV_BF16 && p->kv_dtype != RL_ORACLE_KV_FP8_E4M3)
+        return RL_ORACLE_ERR_ARG;
+    if (p->kv_dtype == RL_ORACLE_KV_FP8_E4M3 &&
+        (p->k_scale == NULL || p->v_scale == NULL))
+        return RL_ORACLE_ERR_ARG;
+
+    /* rows == NULL means every (b, h) in order b-major. */
+    const int64_t n =
+        rows ? num_rows : (int64_t)p->batch * (int64_t)p->num_q_heads;
+    int max_len = 1;
+    for (int b = 0; b < p->batch; ++b)
+        if (p->seq_lens[b] > max_len)
+            max_len = p->seq_lens[b];
+
+    for (int64_t r = 0; r < n; ++r) {
+        const int b = rows ? rows[2 * r] : (int)(r / p->num_q_heads);
+        const int h = rows ? rows[2 * r + 1] : (int)(r % p->num_q_heads);
+        if (!row_is_valid(p, b, h))
+            return RL_ORACLE_ERR_PRECONDITION;
+    }
+
+    int failed = 0;
+#pragma omp parallel
+    {
+        double* scores = (double*)malloc(sizeof(double) * (size_t)max_len);
+        if (scores == NULL) {
+#pragma omp atomic write
+            failed = 1;
+        }
+#pragma omp for schedule(dynamic, 1)
+        for (int64_t r = 0; r < n; ++r) {
+            if (scores == NULL)
+                continue;
+            const int b = rows ? rows[2 * r] : (int)(r / p->num_q_heads);
+            const int h = rows ? rows[2 * r + 1] : (int)(r % p->num_q_heads);
+            attend_one_row(p, b, h, scores, out + r * p->head_dim);
+        }
+        free(scores);
+    }
+    return failed ? RL_ORACLE_ERR_NOMEM : RL_ORACLE_OK;
+}
+
+int rl_oracle_max_threads(void)
+{
+#ifdef _OPENMP
+    extern int omp_get_max_threads(void);
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}

@@ -1,0 +1,73 @@
+/*
+ * decode_attn_oracle.h -- C interface of the fp64 CPU oracle.
+ *
+ * TEST INFRASTRUCTURE ONLY: used by tests, the smoke check and the benchmark's
+ * CPU-baseline leg.  Independent of the GPU library (no shared code).
+ *
+ * Every pointer is a host pointer owned by the caller.  The oracle never
+ * writes its inputs.  Layouts (row-major, innermost last):
+ *   q            [batch][num_q_heads][head_dim]            bf16 bit patterns
+ *   k_pool/v_pool [num_pages][num_kv_heads][page_size][head_dim]
+ *                 bf16 bit patterns, or OCP e4m3 codes for the fp8 variant
+ *   k_scale/v_scale [num_pages][num_kv_heads] fp32 (fp8 only, else unused)
+ *   block_table  [batch][max_pages] int32 physical page indices
+ *   seq_lens     [batch] int32 cached tokens per sequence (<= 0: empty)
+ *   out          [num_rows][head_dim] fp64, one row per requested (b, h)
+ */
+#ifndef RL_DECODE_ATTN_ORACLE_H
+#define RL_DECODE_ATTN_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+    RL_ORACLE_OK = 0,
+    RL_ORACLE_ERR_ARG = 1,          /* malformed problem description          */
+    RL_ORACLE_ERR_PRECONDITION = 2, /* page index or length out of range      */
+    RL_ORACLE_ERR_NOMEM = 3
+};
+
+enum { RL_ORACLE_KV_BF16 = 0, RL_ORACLE_KV_FP8_E4M3 = 1 };
+
+typedef struct {
+    int32_t batch, num_q_heads, num_kv_heads, head_dim, page_size;
+    int32_t kv_dtype;   /* RL_ORACLE_KV_*                                  */
+    int32_t max_pages;  /* columns of block_table                          */
+    int64_t num_pages;  /* pages in each pool                              */
+    double scale;       /* softmax scale applied to q.k                    */
+    const void* q;
+    const void* k_pool;
+    const void* v_pool;
+    const float* k_scale;
+    const float* v_scale;
+    const int32_t* block_table;
+    const int32_t* seq_lens;
+} rl_oracle_problem;
+
+/*
+ * out[r][:] = attention row (b, h) = (rows[2r], rows[2r+1]) for r < num_rows;
+ * rows == NULL computes every (b, h), b-major.  Rows whose sequence is empty
+ * are zero.  Fails with RL_ORACLE_ERR_PRECONDITION, writing nothing, when a
+ * requested row reads a block-table entry outside [0, num_pages) or has a
+ * length beyond max_pages * page_size.
+ */
+int rl_oracle_decode_attn(const rl_oracle_problem* p, const int32_t* rows,
+                          int64_t num_rows, double* out);
+
+/* Exact value of one OCP E4M3FN code (NaN for S.1111.111). */
+double rl_oracle_e4m3_to_double(uint8_t code);
+
+/* Exact value of one bf16 bit pattern. */
+double rl_oracle_bf16_to_double(uint16_t bits);
+
+/* OpenMP threads the oracle will use (1 without OpenMP). */
+int rl_oracle_max_threads(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif
