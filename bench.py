@@ -1,0 +1,211 @@
+#!/usr/bin/env python3
+"""Decode-attention benchmark: one layer, one decode step, one GPU.
+
+A step is one rl_decode_attn_run() (split-K kernel + merge kernel) over one
+batch.  Inputs are seeded synthetic tensors resident in HBM before timing
+starts.  Prints one JSON line:
+  value      = KV bytes read per step / step time  (GB/s, the metric's unit)
+  roofline   = the split-K kernel's achieved bytes/s against 8 TB/s, timed
+               live with HIP events recorded around each of its launches
+  cpu_baseline = the fp64 oracle timed on the host on a sample of the step
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def parse_args():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="qwen3_8b_step",
+                    help="workload name (see paper_2512_22492_amd.workloads.CONFIGS)")
+    ap.add_argument("--replicas", type=int, default=2,
+                    help="copies of the KV pools visited round-robin, so that no step "
+                         "reads data a previous step left in the caches")
+    ap.add_argument("--scores", choices=["mfma", "valu"], default="mfma",
+                    help="score path of the split-K kernel")
+    ap.add_argument("--split-tokens", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-kernel-events", action="store_true",
+                    help="do not record events around the split kernel (profiling runs)")
+    return ap.parse_args()
+
+
+def algorithmic_bytes(p):
+    """Bytes the split-K kernel must move: K and V of every cached token (plus
+    fp8 slab scales), the queries, the used block-table entries, seq_lens."""
+    import numpy as np
+    L = np.clip(p.lengths(), 0, None)
+    pages = (L + p.page_size - 1) // p.page_size
+    kv = p.kv_bytes()
+    q = p.batch * p.num_q_heads * p.head_dim * 2
+    return kv + q + int(pages.sum()) * 4 + p.batch * 4, kv
+
+
+def load_traffic(config, kernel_source_sha):
+    try:
+        with open(TRAFFIC_FILE) as f:
+            data = json.load(f)
+    except (OSError, ValueError):
+        return None
+    entry = data.get(config)
+    if not entry or entry.get("kernel_source_sha256") != kernel_source_sha:
+        return None
+    return entry.get("bytes_per_launch")
+
+
+def kernel_source_sha():
+    import hashlib
+    path = os.path.join(ROOT, "paper_2512_22492_amd", "csrc", "rl_decode_attn.hip")
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def cpu_baseline(p, rows_per_call=None):
+    """Times the oracle on the host.  The sample is the whole step (every
+    (sequence, head) row) when that is bounded, else the first sequences."""
+    import numpy as np
+    import oracle
+    kv_code = oracle.KV_BF16 if p.kv_dtype == "bf16" else oracle.KV_FP8_E4M3
+    h = p.host_arrays()
+    L = np.clip(p.lengths(), 0, None)
+    # bound the sample to ~5e10 fp64 multiply-adds (a few seconds on 16 cores)
+    per_seq = L * p.num_q_heads * p.head_dim * 2
+    nseq = int(np.searchsorted(np.cumsum(per_seq), 5e10, side="right"))
+    nseq = max(1, min(p.batch, nseq))
+    rows = np.array([(b, hh) for b in range(nseq) for hh in range(p.num_q_heads)],
+                    dtype=np.int32)
+    t0 = time.perf_counter()
+    oracle.decode_attention(kv_dtype=kv_code, rows=rows, **h)
+    dt = time.perf_counter() - t0
+    elt = 2 if p.kv_dtype == "bf16" else 1
+    kv = int(L[:nseq].sum()) * p.num_kv_heads * p.head_dim * 2 * elt
+    return {
+        "value": kv / dt / 1e9,
+        "unit": "GB/s",
+        "cores": oracle.max_threads(),
+        "kind": "oracle",
+        "sample": "%d of %d sequences (%d query-head rows, all tokens), fp64, %.2f s; "
+                  "%.1f query-tokens/s" % (nseq, p.batch, len(rows), dt, nseq / dt),
+        "seconds": dt,
+    }
+
+
+def main():
+    args = parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(decode attention shards by sequence or kv head with no exchange; "
+              "the per-GPU figure is the --gpus 1 line)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2512_22492_amd import binding, workloads
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    print("bench: generating %s (%s)" % (args.config, workloads.describe(args.config)),
+          file=sys.stderr, flush=True)
+    base = workloads.make_config(args.config, device=dev)
+    replicas = [base]
+    for _ in range(1, max(1, args.replicas)):
+        replicas.append(workloads.DecodeProblem(**{
+            **base.__dict__, "k_pool": base.k_pool.clone(), "v_pool": base.v_pool.clone(),
+            "k_scale": None if base.k_scale is None else base.k_scale.clone(),
+            "v_scale": None if base.v_scale is None else base.v_scale.clone()}))
+    out = torch.empty_like(base.q)
+    flags = binding.RL_DA_SCORES_ON_VALU if args.scores == "valu" else 0
+    attn = binding.DecodeAttention.for_problem(base, flags=flags,
+                                               split_tokens=args.split_tokens)
+    split_tokens, num_splits = attn.split_info(base.max_pages)
+    stream = torch.cuda.current_stream()
+
+    nev = args.steps
+    ev_b = [torch.cuda.Event(enable_timing=True) for _ in range(nev)]
+    ev_e = [torch.cuda.Event(enable_timing=True) for _ in range(nev)]
+    for e in ev_b + ev_e:
+        e.record(stream)          # materialises the underlying hipEvent_t
+    torch.cuda.synchronize()
+
+    for i in range(args.warmup):
+        attn.run_problem(replicas[i % len(replicas)], out, stream)
+    torch.cuda.synchronize()
+    print("bench: warmup done, timing %d steps" % args.steps, file=sys.stderr, flush=True)
+
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        if not args.no_kernel_events:
+            binding.rl_decode_attn_set_timing_events(attn.handle, ev_b[i].cuda_event,
+                                                     ev_e[i].cuda_event)
+        attn.run_problem(replicas[i % len(replicas)], out, stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    binding.rl_decode_attn_set_timing_events(attn.handle, None, None)
+
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    alg_bytes, kv_bytes = algorithmic_bytes(base)
+    value = kv_bytes / (ms_per_step / 1e3) / 1e9
+    record = {
+        "metric": "decode-attention KV-read GB/s (fraction of HBM peak) + query-tokens/s, 1 GPU",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": base.kv_dtype if base.kv_dtype == "bf16" else "fp8_e4m3",
+        "data": "synthetic",
+        "config": {
+            "workload": "%s: %s" % (args.config, workloads.describe(args.config)),
+            "batch": base.batch, "num_q_heads": base.num_q_heads,
+            "num_kv_heads": base.num_kv_heads, "head_dim": base.head_dim,
+            "page_size": base.page_size, "seq_len_mean": float(base.lengths().mean()),
+            "split_tokens": split_tokens, "num_splits": num_splits,
+            "scores": args.scores, "replicas": len(replicas),
+        },
+        "query_tokens_per_s": round(base.batch / (ms_per_step / 1e3), 1),
+        "kv_bytes_per_step": kv_bytes,
+        "hbm_frac": round(value / HBM_PEAK_GBS, 4),
+    }
+    if not args.no_kernel_events:
+        split_ms = np.array([b.elapsed_time(e) for b, e in zip(ev_b, ev_e)])
+        avg = float(split_ms.mean())
+        achieved = alg_bytes / (avg / 1e3) / 1e9
+        record["roofline"] = {
+            "bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
+            "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": load_traffic(args.config, kernel_source_sha()),
+            "kernel": "split-K decode kernel", "avg_us": round(avg * 1e3, 2),
+            "min_us": round(float(split_ms.min()) * 1e3, 2),
+            "bytes_per_launch": alg_bytes,
+        }
+    attn.close()
+    if not args.no_cpu_baseline:
+        print("bench: timing the CPU oracle", file=sys.stderr, flush=True)
+        record["cpu_baseline"] = cpu_baseline(base)
+        del record["cpu_baseline"]["seconds"]
+    print(json.dumps(record), flush=True)
+
+
+if __name__ == "__main__":
+    main()

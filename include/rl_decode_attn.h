@@ -1,0 +1,158 @@
+/*
+ * rl_decode_attn.h -- paged grouped-query decode attention for MI355X (gfx950).
+ *
+ * One call computes one decode step of one attention layer for a batch of
+ * sequences: the operation that dominates rollout generation in RL
+ * post-training (arXiv 2512.22492, Sec. 1 and Sec. 2.1: rollout runs in an
+ * inference engine over a paged KV cache and takes most of post-training
+ * time).  For every sequence b and query head h,
+ *
+ *     out[b,h,:] = sum_t softmax_t( scale * <q[b,h,:], K_b[t,kvh,:]> ) V_b[t,kvh,:]
+ *
+ * over the t = 0 .. seq_lens[b]-1 cached tokens, with kv head
+ * kvh = h / (Hq / Hkv) (grouped-query attention: consecutive query heads share
+ * a kv head).  Token t of sequence b is stored in physical page
+ * block_table[b][t / page_size], slot t % page_size.
+ *
+ * Memory layouts (row-major, innermost last).  Every device pointer below is
+ * owned by the caller; the library never frees or retains it past the call.
+ *   q            [batch][Hq][head_dim]                         bf16
+ *   k_pool       [num_pages][Hkv][page_size][head_dim]         bf16 or e4m3
+ *   v_pool       same as k_pool
+ *   k_scale      [num_pages][Hkv] fp32, fp8 pools only: a stored code c of
+ *   v_scale      slab (page, kvh) stands for e4m3(c) * scale[page][kvh]
+ *   block_table  [batch][max_pages] int32 (row stride max_pages)
+ *   seq_lens     [batch] int32
+ *   out          [batch][Hq][head_dim]                         bf16
+ * e4m3 is the OCP 8-bit float E4M3FN (bias 7, largest finite 448, no infinity).
+ *
+ * Execution.  run() enqueues its kernels on the caller's HIP stream and
+ * returns without synchronising; the result is ready when the stream has
+ * reached that point.  run() never allocates: the handle owns a workspace
+ * sized at create() for max_batch and max_pages_per_seq.  One handle must not
+ * be used by two runs that can overlap (two streams); use one handle per
+ * stream.  Results are deterministic: no atomics take part in any reduction,
+ * the split size is fixed per handle and partial results merge in a fixed
+ * order, so a sequence's output does not depend on the rest of the batch or
+ * on where its pages sit in the pool.
+ *
+ * Errors.  Every entry point returns an rl_da_status; nothing is thrown
+ * across the interface.  run() checks its host-visible arguments and returns
+ * RL_DA_ERR_INVALID_ARG or RL_DA_ERR_UNSUPPORTED before launching anything.
+ * It does not read device memory to check, so these are preconditions:
+ *   0 <= block_table[b][j] < num_pages  for j < ceil(seq_lens[b] / page_size)
+ *   seq_lens[b] <= max_pages * page_size
+ * Block-table entries past a sequence's last page and token slots past its
+ * length are never read, and may hold anything (including NaN values).  A
+ * sequence with seq_lens[b] <= 0 produces zeros.  With RL_DA_CHECKED set at
+ * create(), the kernels test the preconditions, skip the offending work, and
+ * record the violation in a device error word read by
+ * rl_decode_attn_check_error().
+ */
+#ifndef RL_DECODE_ATTN_H
+#define RL_DECODE_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct rl_decode_attn rl_decode_attn; /* opaque handle */
+
+typedef enum {
+    RL_DA_OK = 0,
+    RL_DA_ERR_INVALID_ARG = 1,   /* null/misaligned pointer, bad size         */
+    RL_DA_ERR_UNSUPPORTED = 2,   /* valid request this build does not serve   */
+    RL_DA_ERR_OUT_OF_MEMORY = 3, /* workspace allocation failed in create()   */
+    RL_DA_ERR_HIP = 4            /* a HIP runtime call or launch failed       */
+} rl_da_status;
+
+typedef enum { RL_DA_KV_BF16 = 0, RL_DA_KV_FP8_E4M3 = 1 } rl_da_kv_dtype;
+
+/* create() flag: kernels check block-table entries and lengths on device. */
+#define RL_DA_CHECKED 0x1u
+/* create() flag: form q.k with bf16 dot2 ops and DPP row sums on the vector
+ * ALUs instead of packing the query group into an MFMA tile (same results up
+ * to fp32 rounding; kept to measure one path against the other). */
+#define RL_DA_SCORES_ON_VALU 0x2u
+
+/* Device error word bits reported by rl_decode_attn_check_error(). */
+#define RL_DA_DEVERR_PAGE_OUT_OF_RANGE 0x1
+#define RL_DA_DEVERR_LENGTH_TOO_LONG 0x2
+
+typedef struct {
+    int32_t num_q_heads;       /* Hq; a multiple of num_kv_heads               */
+    int32_t num_kv_heads;      /* Hkv; Hq / Hkv in {1, 2, 4, 8}                 */
+    int32_t head_dim;          /* 128                                         */
+    int32_t page_size;         /* tokens per page: 16                         */
+    int32_t max_batch;         /* largest batch a run() may pass (>= 1)       */
+    int32_t max_pages_per_seq; /* largest block-table width a run() may pass  */
+    int32_t kv_dtype;          /* rl_da_kv_dtype                              */
+    int32_t split_tokens;      /* tokens per split-K work unit; 0 = 512;      */
+                               /* a multiple of page_size, at most 1024       */
+    uint32_t flags;            /* RL_DA_CHECKED | RL_DA_SCORES_ON_VALU or 0   */
+} rl_da_config;
+
+/*
+ * Validates cfg and allocates a handle plus its device workspace on the
+ * current HIP device.  On success *out owns both; on failure *out is NULL.
+ * INVALID_ARG for null pointers or non-positive sizes, UNSUPPORTED for shapes
+ * this build has no kernel for, OUT_OF_MEMORY / HIP when allocation fails.
+ */
+rl_da_status rl_decode_attn_create(const rl_da_config* cfg, rl_decode_attn** out);
+
+/*
+ * Enqueues one decode step on `stream` (a hipStream_t; NULL = null stream).
+ * Pointers as in the layout table above; q, the pools and out must be 16-byte
+ * aligned.  k_scale and v_scale must be non-NULL exactly for fp8 handles.
+ * 0 <= batch <= max_batch, 1 <= max_pages <= max_pages_per_seq, num_pages >= 1,
+ * scale finite.  batch == 0 enqueues nothing.
+ */
+rl_da_status rl_decode_attn_run(rl_decode_attn* h, const void* q,
+                                const void* k_pool, const void* v_pool,
+                                const float* k_scale, const float* v_scale,
+                                int64_t num_pages, const int32_t* block_table,
+                                int32_t max_pages, const int32_t* seq_lens,
+                                int32_t batch, float scale, void* out,
+                                void* stream);
+
+/* Frees the handle and its workspace.  NULL is accepted.  The caller must
+ * ensure no enqueued run() still uses the handle. */
+rl_da_status rl_decode_attn_destroy(rl_decode_attn* h);
+
+/* Static description of a status code. */
+const char* rl_da_status_string(rl_da_status s);
+
+/* Device workspace bytes create() would allocate for cfg (host only). */
+rl_da_status rl_decode_attn_workspace_size(const rl_da_config* cfg,
+                                           size_t* bytes);
+
+/*
+ * Checked handles only: synchronises the device, stores the accumulated
+ * RL_DA_DEVERR_* bits in *device_error and clears them.  UNSUPPORTED for a
+ * handle created without RL_DA_CHECKED.
+ */
+rl_da_status rl_decode_attn_check_error(rl_decode_attn* h, int32_t* device_error);
+
+/* Split-K geometry of a handle: tokens per split and the number of splits a
+ * block table of max_pages columns is divided into. */
+rl_da_status rl_decode_attn_split_info(const rl_decode_attn* h, int32_t max_pages,
+                                       int32_t* split_tokens, int32_t* num_splits);
+
+/*
+ * Measurement hook (no counterpart in the paper): with both events non-NULL,
+ * every later run() records split_begin on its stream just before the split-K
+ * kernel and split_end just after it, so hipEventElapsedTime gives that
+ * kernel's duration.  Events are hipEvent_t owned by the caller; NULL, NULL
+ * turns recording off.  INVALID_ARG if exactly one event is NULL.
+ */
+rl_da_status rl_decode_attn_set_timing_events(rl_decode_attn* h, void* split_begin,
+                                              void* split_end);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif

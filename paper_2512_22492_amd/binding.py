@@ -1,0 +1,248 @@
+"""ctypes binding of the C interface declared in include/rl_decode_attn.h.
+
+Argument marshalling only: every step of the attention runs in the HIP
+library.  Functions keep the C names.  Pointer arguments accept either an
+integer device address or a torch tensor (its data_ptr is passed); `stream`
+accepts an integer hipStream_t, a torch.cuda.Stream or None (null stream).
+The library is loaded on first use and a missing build is an error.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+from . import build as _build
+
+RL_DA_OK = 0
+RL_DA_ERR_INVALID_ARG = 1
+RL_DA_ERR_UNSUPPORTED = 2
+RL_DA_ERR_OUT_OF_MEMORY = 3
+RL_DA_ERR_HIP = 4
+
+RL_DA_KV_BF16 = 0
+RL_DA_KV_FP8_E4M3 = 1
+
+RL_DA_CHECKED = 0x1
+RL_DA_SCORES_ON_VALU = 0x2
+
+RL_DA_DEVERR_PAGE_OUT_OF_RANGE = 0x1
+RL_DA_DEVERR_LENGTH_TOO_LONG = 0x2
+
+# Every function the header declares, in declaration order.
+EXPORTED = [
+    "rl_decode_attn_create",
+    "rl_decode_attn_run",
+    "rl_decode_attn_destroy",
+    "rl_da_status_string",
+    "rl_decode_attn_workspace_size",
+    "rl_decode_attn_check_error",
+    "rl_decode_attn_split_info",
+    "rl_decode_attn_set_timing_events",
+]
+
+
+class rl_da_config(ctypes.Structure):
+    _fields_ = [
+        ("num_q_heads", ctypes.c_int32),
+        ("num_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("page_size", ctypes.c_int32),
+        ("max_batch", ctypes.c_int32),
+        ("max_pages_per_seq", ctypes.c_int32),
+        ("kv_dtype", ctypes.c_int32),
+        ("split_tokens", ctypes.c_int32),
+        ("flags", ctypes.c_uint32),
+    ]
+
+
+class RLDecodeAttnError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__("%s failed: %s (status %d)" % (what, _status_text(status), status))
+        self.status = status
+
+
+_lib = None
+
+
+def library_path() -> str:
+    return _build.LIB_PATH
+
+
+def load_library():
+    """Loads the built library; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    path = _build.LIB_PATH
+    if not os.path.exists(path):
+        raise RuntimeError(
+            "HIP library %s is not built; run __graft_entry__.build()" % path)
+    # torch carries its own HIP runtime under the same soname
+    # (libamdhip64.so.7).  Loading torch first makes the library bind to that
+    # one copy, so device pointers, streams and events are shared; loading it
+    # first would pull a second runtime into the process.
+    import torch  # noqa: F401
+    lib = ctypes.CDLL(path)
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    lib.rl_decode_attn_create.argtypes = [ctypes.POINTER(rl_da_config), ctypes.POINTER(vp)]
+    lib.rl_decode_attn_create.restype = ctypes.c_int
+    lib.rl_decode_attn_run.argtypes = [vp, vp, vp, vp, vp, vp, i64, vp, i32, vp, i32,
+                                       ctypes.c_float, vp, vp]
+    lib.rl_decode_attn_run.restype = ctypes.c_int
+    lib.rl_decode_attn_destroy.argtypes = [vp]
+    lib.rl_decode_attn_destroy.restype = ctypes.c_int
+    lib.rl_da_status_string.argtypes = [ctypes.c_int]
+    lib.rl_da_status_string.restype = ctypes.c_char_p
+    lib.rl_decode_attn_workspace_size.argtypes = [ctypes.POINTER(rl_da_config),
+                                                  ctypes.POINTER(ctypes.c_size_t)]
+    lib.rl_decode_attn_workspace_size.restype = ctypes.c_int
+    lib.rl_decode_attn_check_error.argtypes = [vp, ctypes.POINTER(i32)]
+    lib.rl_decode_attn_check_error.restype = ctypes.c_int
+    lib.rl_decode_attn_split_info.argtypes = [vp, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)]
+    lib.rl_decode_attn_split_info.restype = ctypes.c_int
+    lib.rl_decode_attn_set_timing_events.argtypes = [vp, vp, vp]
+    lib.rl_decode_attn_set_timing_events.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _status_text(status: int) -> str:
+    try:
+        return load_library().rl_da_status_string(status).decode()
+    except Exception:
+        return "status %d" % status
+
+
+def _ptr(x):
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _stream(s):
+    if s is None:
+        return None
+    if isinstance(s, int):
+        return s
+    return s.cuda_stream
+
+
+def make_config(num_q_heads, num_kv_heads, max_batch, max_pages_per_seq, *,
+                head_dim=128, page_size=16, kv_dtype=RL_DA_KV_BF16, split_tokens=0,
+                flags=0) -> rl_da_config:
+    return rl_da_config(num_q_heads, num_kv_heads, head_dim, page_size, max_batch,
+                        max_pages_per_seq, kv_dtype, split_tokens, flags)
+
+
+# ------------------------------------------------- C functions, same names ---
+
+def rl_da_status_string(status: int) -> str:
+    return load_library().rl_da_status_string(int(status)).decode()
+
+
+def rl_decode_attn_create(cfg: rl_da_config):
+    """Returns (status, handle); handle is None unless status is RL_DA_OK."""
+    h = ctypes.c_void_p()
+    rc = load_library().rl_decode_attn_create(ctypes.byref(cfg), ctypes.byref(h))
+    return rc, (h.value if rc == RL_DA_OK else None)
+
+
+def rl_decode_attn_run(h, q, k_pool, v_pool, k_scale, v_scale, num_pages, block_table,
+                       max_pages, seq_lens, batch, scale, out, stream=None) -> int:
+    return load_library().rl_decode_attn_run(
+        h, _ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(k_scale), _ptr(v_scale),
+        int(num_pages), _ptr(block_table), int(max_pages), _ptr(seq_lens), int(batch),
+        float(scale), _ptr(out), _stream(stream))
+
+
+def rl_decode_attn_destroy(h) -> int:
+    return load_library().rl_decode_attn_destroy(h)
+
+
+def rl_decode_attn_workspace_size(cfg: rl_da_config):
+    n = ctypes.c_size_t()
+    rc = load_library().rl_decode_attn_workspace_size(ctypes.byref(cfg), ctypes.byref(n))
+    return rc, n.value
+
+
+def rl_decode_attn_check_error(h):
+    v = ctypes.c_int32()
+    rc = load_library().rl_decode_attn_check_error(h, ctypes.byref(v))
+    return rc, v.value
+
+
+def rl_decode_attn_split_info(h, max_pages):
+    st, ns = ctypes.c_int32(), ctypes.c_int32()
+    rc = load_library().rl_decode_attn_split_info(h, int(max_pages), ctypes.byref(st),
+                                                  ctypes.byref(ns))
+    return rc, st.value, ns.value
+
+
+def rl_decode_attn_set_timing_events(h, split_begin, split_end) -> int:
+    return load_library().rl_decode_attn_set_timing_events(h, split_begin, split_end)
+
+
+# --------------------------------------------------------- handle wrapper ---
+
+class DecodeAttention:
+    """Owns one library handle; run() enqueues one decode step."""
+
+    def __init__(self, num_q_heads, num_kv_heads, max_batch, max_pages_per_seq, *,
+                 kv_dtype="bf16", split_tokens=0, flags=0, head_dim=128, page_size=16):
+        dt = {"bf16": RL_DA_KV_BF16, "fp8_e4m3": RL_DA_KV_FP8_E4M3}[kv_dtype]
+        self.kv_dtype = kv_dtype
+        self.cfg = make_config(num_q_heads, num_kv_heads, max_batch, max_pages_per_seq,
+                               head_dim=head_dim, page_size=page_size, kv_dtype=dt,
+                               split_tokens=split_tokens, flags=flags)
+        rc, h = rl_decode_attn_create(self.cfg)
+        if rc != RL_DA_OK:
+            raise RLDecodeAttnError(rc, "rl_decode_attn_create")
+        self.handle = h
+
+    @classmethod
+    def for_problem(cls, p, **kw):
+        return cls(p.num_q_heads, p.num_kv_heads, p.batch, p.max_pages,
+                   kv_dtype=p.kv_dtype, **kw)
+
+    def run(self, q, k_pool, v_pool, k_scale, v_scale, block_table, seq_lens, scale, out,
+            stream=None):
+        rc = rl_decode_attn_run(self.handle, q, k_pool, v_pool, k_scale, v_scale,
+                                k_pool.shape[0], block_table, block_table.shape[1],
+                                seq_lens, q.shape[0], scale, out, stream)
+        if rc != RL_DA_OK:
+            raise RLDecodeAttnError(rc, "rl_decode_attn_run")
+
+    def run_problem(self, p, out, stream=None):
+        self.run(p.q, p.k_pool, p.v_pool, p.k_scale, p.v_scale, p.block_table, p.seq_lens,
+                 p.scale, out, stream)
+
+    def split_info(self, max_pages):
+        rc, st, ns = rl_decode_attn_split_info(self.handle, max_pages)
+        if rc != RL_DA_OK:
+            raise RLDecodeAttnError(rc, "rl_decode_attn_split_info")
+        return st, ns
+
+    def check_error(self):
+        rc, v = rl_decode_attn_check_error(self.handle)
+        if rc != RL_DA_OK:
+            raise RLDecodeAttnError(rc, "rl_decode_attn_check_error")
+        return v
+
+    def close(self):
+        if self.handle is not None:
+            rl_decode_attn_destroy(self.handle)
+            self.handle = None
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

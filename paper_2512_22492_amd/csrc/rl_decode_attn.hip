@@ -1,0 +1,884 @@
+// rl_decode_attn.hip -- paged grouped-query decode attention for gfx950.
+//
+// One decode step of one attention layer (the rollout inner loop of
+// arXiv 2512.22492, Sec. 2.1): out[b,h] = softmax(scale * q[b,h] K_b^T) V_b
+// over a paged KV cache, kv head h / G.  The operation is split-K
+// ("flash-decoding"): each work unit (sequence b, kv head, split s) scans
+// split_tokens consecutive cached tokens and keeps an online softmax (running
+// max m, running sum l, weighted value sum acc) for the G query heads that
+// share the kv head; a second kernel merges the per-split partials with the
+// log-sum-exp rule.  Sequences that fit in one split are finished by the first
+// kernel directly.
+//
+// Data movement is the whole cost: every K/V byte is read once from HBM.  A
+// (page, kv head) slab is 16 tokens x 128 dims x 2 bytes = 4 KiB, contiguous in
+// the [page][kv head][slot][dim] pool layout, and is read by one wavefront
+// with four 16-byte-per-lane loads.  Scores are computed once per kv head for
+// all G query heads of the group (the GQA reuse), either with one MFMA per
+// 32 dims (the G query rows packed into a 16-row tile) or with bf16 dot2 ops
+// and DPP row reductions; the value accumulation runs in fp32 on the VALU.
+//
+// All arithmetic is fp32; scores are kept in the log2 domain (scale folded
+// with log2(e)) so that every exponential is one v_exp_f32.
+
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+
+#include "rl_decode_attn.h"
+
+namespace {
+
+constexpr int kHeadDim = 128;
+constexpr int kPageSize = 16;
+constexpr int kWave = 64;
+constexpr int kDefaultSplitTokens = 512;
+constexpr int kMaxSplitTokens = 1024;  // split pages must fit one wavefront
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kSlabBytesBf16 = kPageSize * kHeadDim * 2;
+
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float floatx4_t __attribute__((ext_vector_type(4)));
+
+struct SplitArgs {
+    const uint16_t* q;          // bf16 bits [B][Hq][D]
+    const uint8_t* k_pool;      // [P][Hkv][16][D] elements
+    const uint8_t* v_pool;
+    const float* k_scale;       // [P][Hkv] (fp8 only)
+    const float* v_scale;
+    const int32_t* block_table; // [B][max_pages]
+    const int32_t* seq_lens;    // [B]
+    uint16_t* out;              // bf16 bits [B][Hq][D]
+    float* ws_acc;              // [B][Hq][num_splits][D]
+    float* ws_ml;               // [B][Hq][num_splits][2]  (m in log2 units, l)
+    int32_t* dev_error;
+    int64_t num_pages;
+    int32_t num_q_heads;
+    int32_t num_kv_heads;
+    int32_t max_pages;
+    int32_t split_pages;
+    int32_t num_splits;         // ceil(max_pages / split_pages)
+    float scale_log2;           // scale * log2(e)
+};
+
+// ------------------------------------------------------------ helpers ---
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// fp32 -> bf16 bits, round to nearest even (quiet NaN kept NaN).
+__device__ __forceinline__ uint32_t f32_to_bf16(float f)
+{
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u)
+        return 0x7fc0u;
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return u >> 16;
+}
+
+__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c)
+{
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a),
+                                           __builtin_bit_cast(bf16x2_t, b), c, false);
+}
+
+// DPP lane permutations inside a 16-lane row.  quad_perm [1,0,3,2] and
+// [2,3,0,1] pair lanes within a quad; row_half_mirror pairs the two quads of
+// each 8-lane half; row_mirror pairs the two halves.  Applied in turn they
+// combine all 16 lanes of a row.
+constexpr int kDppQuadXor1 = 0xB1;
+constexpr int kDppQuadXor2 = 0x4E;
+constexpr int kDppRowHalfMirror = 0x141;
+constexpr int kDppRowMirror = 0x140;
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v)
+{
+    return __int_as_float(
+        __builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xf, 0xf, false));
+}
+
+__device__ __forceinline__ float row16_sum(float v)
+{
+    v += dpp_f32<kDppQuadXor1>(v);
+    v += dpp_f32<kDppQuadXor2>(v);
+    v += dpp_f32<kDppRowHalfMirror>(v);
+    v += dpp_f32<kDppRowMirror>(v);
+    return v;
+}
+
+__device__ __forceinline__ float row16_max(float v)
+{
+    v = fmaxf(v, dpp_f32<kDppQuadXor1>(v));
+    v = fmaxf(v, dpp_f32<kDppQuadXor2>(v));
+    v = fmaxf(v, dpp_f32<kDppRowHalfMirror>(v));
+    v = fmaxf(v, dpp_f32<kDppRowMirror>(v));
+    return v;
+}
+
+__device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Orders LDS traffic between the lanes of one wavefront (the work-group is
+// a single wavefront, so no s_barrier and no wait on global loads is needed).
+__device__ __forceinline__ void wave_lds_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__device__ __forceinline__ void unpack8(const uint4& w, float (&v)[8])
+{
+    v[0] = bf16_lo(w.x); v[1] = bf16_hi(w.x);
+    v[2] = bf16_lo(w.y); v[3] = bf16_hi(w.y);
+    v[4] = bf16_lo(w.z); v[5] = bf16_hi(w.z);
+    v[6] = bf16_lo(w.w); v[7] = bf16_hi(w.w);
+}
+
+struct UnitCoords {
+    int b, kvh, s;
+    int seq_len;   // clamped to max_pages * page_size
+    int npages;    // pages holding the sequence
+    int p0, p1;    // this unit's page range [p0, p1)
+    int nsplit;    // splits of this sequence
+};
+
+// Decodes blockIdx.x into (b, kvh, s); returns false when the unit is empty.
+template <bool CHECKED>
+__device__ __forceinline__ bool unit_coords(const SplitArgs& a, UnitCoords& u)
+{
+    const int unit = blockIdx.x;
+    u.s = unit % a.num_splits;
+    const int bk = unit / a.num_splits;
+    u.kvh = bk % a.num_kv_heads;
+    u.b = bk / a.num_kv_heads;
+    int L = a.seq_lens[u.b];
+    const int cap = a.max_pages * kPageSize;
+    if (L > cap) {
+        if (CHECKED && threadIdx.x == 0 && u.s == 0 && u.kvh == 0)
+            atomicOr(a.dev_error, RL_DA_DEVERR_LENGTH_TOO_LONG);
+        L = cap;
+    }
+    u.seq_len = L;
+    u.npages = L > 0 ? (L + kPageSize - 1) / kPageSize : 0;
+    u.nsplit = (u.npages + a.split_pages - 1) / a.split_pages;
+    u.p0 = u.s * a.split_pages;
+    u.p1 = min(u.p0 + a.split_pages, u.npages);
+    return u.p0 < u.p1;
+}
+
+// An empty sequence produces zeros (written once, by split 0).
+template <int G>
+__device__ __forceinline__ void write_zero_rows(const SplitArgs& a, const UnitCoords& u)
+{
+    if (u.npages != 0 || u.s != 0)
+        return;
+    const int lane = threadIdx.x;
+    for (int e = lane; e < G * (kHeadDim / 8); e += kWave) {
+        const int g = e / (kHeadDim / 8), chunk = e % (kHeadDim / 8);
+        uint4* dst = reinterpret_cast<uint4*>(
+            a.out + ((int64_t)u.b * a.num_q_heads + u.kvh * G + g) * kHeadDim + chunk * 8);
+        *dst = make_uint4(0, 0, 0, 0);
+    }
+}
+
+// Block-table entries of the unit's pages, one per lane (lane i: page p0+i).
+template <bool CHECKED>
+__device__ __forceinline__ bool load_unit_pages(const SplitArgs& a, const UnitCoords& u,
+                                                int32_t& my_page)
+{
+    const int lane = threadIdx.x;
+    const int32_t* bt = a.block_table + (int64_t)u.b * a.max_pages;
+    const bool in_unit = u.p0 + lane < u.p1;
+    my_page = in_unit ? bt[u.p0 + lane] : 0;
+    if (CHECKED) {
+        const bool bad = in_unit && (my_page < 0 || (int64_t)my_page >= a.num_pages);
+        if (__any(bad)) {
+            if (lane == 0)
+                atomicOr(a.dev_error, RL_DA_DEVERR_PAGE_OUT_OF_RANGE);
+            return false;
+        }
+    }
+    return true;
+}
+
+__device__ __forceinline__ const uint8_t* slab_base(const uint8_t* pool, int64_t page,
+                                                    int num_kv_heads, int kvh, int slab_bytes)
+{
+    return pool + (page * num_kv_heads + kvh) * (int64_t)slab_bytes;
+}
+
+// Writes the unit's result for query head g of the group: the final bf16 row
+// when the sequence has one split, else the (m, l, acc) partial.
+__device__ __forceinline__ void store_unit_row(const SplitArgs& a, const UnitCoords& u, int h,
+                                               int chunk, const float (&acc)[8], float m,
+                                               float l)
+{
+    const int64_t row = (int64_t)u.b * a.num_q_heads + h;
+    if (u.nsplit == 1) {
+        const float inv = 1.0f / l;
+        uint4 o;
+        o.x = f32_to_bf16(acc[0] * inv) | (f32_to_bf16(acc[1] * inv) << 16);
+        o.y = f32_to_bf16(acc[2] * inv) | (f32_to_bf16(acc[3] * inv) << 16);
+        o.z = f32_to_bf16(acc[4] * inv) | (f32_to_bf16(acc[5] * inv) << 16);
+        o.w = f32_to_bf16(acc[6] * inv) | (f32_to_bf16(acc[7] * inv) << 16);
+        *reinterpret_cast<uint4*>(a.out + row * kHeadDim + chunk * 8) = o;
+        return;
+    }
+    const int64_t part = row * a.num_splits + u.s;
+    float4* dst = reinterpret_cast<float4*>(a.ws_acc + part * kHeadDim + chunk * 8);
+    dst[0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
+    dst[1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
+    if (chunk == 0)
+        *reinterpret_cast<float2*>(a.ws_ml + part * 2) = make_float2(m, l);
+}
+
+// Streams a unit's pages through two register buffers (A and B): while one
+// page is consumed from one buffer the next is in flight into the other, and
+// the load two pages ahead is issued as soon as a buffer has been consumed.
+// The steady-state loop issues unconditionally, so the compiler's wait before
+// each consume only covers the buffer being consumed.
+template <typename Issue, typename Consume>
+__device__ __forceinline__ void stream_pages(int p0, int p1, uint4 (&ka)[4], uint4 (&va)[4],
+                                             uint4 (&kb)[4], uint4 (&vb)[4], Issue issue,
+                                             Consume consume)
+{
+    int j = p0;
+    if (p1 - p0 >= 4) {
+        issue(ka, va, j);
+        issue(kb, vb, j + 1);
+        for (; j + 3 < p1; j += 2) {
+            consume(ka, va, j);
+            issue(ka, va, j + 2);
+            consume(kb, vb, j + 1);
+            issue(kb, vb, j + 3);
+        }
+    } else {
+        issue(ka, va, j);
+        if (p1 - p0 >= 2)
+            issue(kb, vb, j + 1);
+    }
+    const int rest = p1 - j;  // 1..3 pages left; pages j and j+1 already issued
+    consume(ka, va, j);
+    if (rest == 3)
+        issue(ka, va, j + 2);
+    if (rest >= 2)
+        consume(kb, vb, j + 1);
+    if (rest == 3)
+        consume(ka, va, j + 2);
+}
+
+// ------------------------------------------------ split kernel, MFMA QK ---
+//
+// Lane roles.  For the score MFMA (v_mfma_f32_16x16x32_bf16, A = queries
+// 16x32, B = keys 32x16), lane l holds key token n = l%16 and 8 dims of each
+// 32-dim block; query head g sits in tile row 4g, so after the four MFMAs of
+// a page lane l holds score (g = l/16, token l%16) in its first accumulator.
+// For the value pass lane l = 16r + c holds dims 8c..8c+7 of tokens 4i + r,
+// i = 0..3 (each 16-byte-per-lane load covers 1 KiB of the slab).  The
+// probabilities cross from the score layout to the value layout through 272
+// bytes of LDS.
+
+template <int G, bool CHECKED>
+__global__ __launch_bounds__(kWave) void split_mfma_bf16(SplitArgs a)
+{
+    static_assert(G >= 1 && G <= 4, "MFMA score tile packs at most 4 query heads");
+    __shared__ __attribute__((aligned(16))) float lds_p[kPageSize * 4];  // [token][g]
+    __shared__ __attribute__((aligned(16))) float lds_alpha[4];
+
+    UnitCoords u;
+    if (!unit_coords<CHECKED>(a, u)) {
+        write_zero_rows<G>(a, u);
+        return;
+    }
+    int32_t my_page;
+    if (!load_unit_pages<CHECKED>(a, u, my_page))
+        return;
+
+    const int lane = threadIdx.x;
+    const int n = lane & 15, kg = lane >> 4;  // score layout
+    const int r = lane >> 4, c = lane & 15;   // value layout
+    const int h0 = u.kvh * G;
+
+    // Query tile: rows 4g hold query head g, every other row is zero.
+    uint4 qa[4];
+    {
+        const int row = lane & 15;
+        const int g = row >> 2;
+        const bool has = (row & 3) == 0 && g < G;
+        const uint16_t* qrow =
+            a.q + ((int64_t)u.b * a.num_q_heads + h0 + (has ? g : 0)) * kHeadDim;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            qa[i] = has ? *reinterpret_cast<const uint4*>(qrow + 32 * i + 8 * kg)
+                        : make_uint4(0, 0, 0, 0);
+    }
+
+    float m = -INFINITY;      // running max of row g = lane/16 (log2 units)
+    float lsum = 0.0f;        // this lane's share of the running sum
+    float acc[G][8];
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int d = 0; d < 8; ++d)
+            acc[g][d] = 0.0f;
+
+    const int koff = n * (kHeadDim * 2) + 16 * kg;  // byte offset in a K slab
+    const int voff = lane * 16;                      // byte offset in a V slab
+
+    auto issue = [&](uint4 (&kbuf)[4], uint4 (&vbuf)[4], int j) {
+        const int64_t page = __builtin_amdgcn_readlane(my_page, j - u.p0);
+        const uint8_t* ks = slab_base(a.k_pool, page, a.num_kv_heads, u.kvh, kSlabBytesBf16);
+        const uint8_t* vs = slab_base(a.v_pool, page, a.num_kv_heads, u.kvh, kSlabBytesBf16);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            kbuf[i] = *reinterpret_cast<const uint4*>(ks + koff + 64 * i);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            vbuf[i] = *reinterpret_cast<const uint4*>(vs + voff + 1024 * i);
+    };
+
+    auto consume = [&](uint4 (&kbuf)[4], uint4 (&vbuf)[4], int j) {
+        // Scores of the 16 tokens of page j for the G query heads.
+        floatx4_t sacc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8_t, qa[i]), __builtin_bit_cast(bf16x8_t, kbuf[i]),
+                sacc, 0, 0, 0);
+
+        const int valid = u.seq_len - j * kPageSize;  // >= 1 tokens valid in page j
+        float s = sacc[0] * a.scale_log2;
+        s = (n < valid) ? s : -INFINITY;
+        const float m_new = fmaxf(m, row16_max(s));  // finite: token 0 is valid
+        const float alpha = exp2_fast(m - m_new);
+        const float pexp = exp2_fast(s - m_new);
+        lsum = lsum * alpha + pexp;
+        m = m_new;
+
+        lds_p[n * 4 + kg] = pexp;
+        if (n == 0)
+            lds_alpha[kg] = alpha;
+        wave_lds_sync();
+        const float4 al = *reinterpret_cast<const float4*>(lds_alpha);
+        float4 pv[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            pv[i] = *reinterpret_cast<const float4*>(&lds_p[(4 * i + r) * 4]);
+        wave_lds_sync();
+
+        const float alv[4] = {al.x, al.y, al.z, al.w};
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+#pragma unroll
+            for (int d = 0; d < 8; ++d)
+                acc[g][d] *= alv[g];
+
+        if (valid < kPageSize) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                if (4 * i + r >= valid)
+                    vbuf[i] = make_uint4(0, 0, 0, 0);  // unread slots may hold NaN
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            float v[8];
+            unpack8(vbuf[i], v);
+            const float pg[4] = {pv[i].x, pv[i].y, pv[i].z, pv[i].w};
+#pragma unroll
+            for (int g = 0; g < G; ++g)
+#pragma unroll
+                for (int d = 0; d < 8; ++d)
+                    acc[g][d] = fmaf(pg[g], v[d], acc[g][d]);
+        }
+    };
+
+    uint4 ka[4], va[4], kb[4], vb[4];
+    stream_pages(u.p0, u.p1, ka, va, kb, vb, issue, consume);
+
+    // Every lane of a value row holds a partial over tokens = r (mod 4); all
+    // rows share the running max, so the partials simply add.
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int d = 0; d < 8; ++d) {
+            float v = acc[g][d];
+            v += __shfl_xor(v, 16);
+            v += __shfl_xor(v, 32);
+            acc[g][d] = v;
+        }
+    const float l_row = row16_sum(lsum);  // l of query head g = lane/16
+
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+        if (r == g)
+            store_unit_row(a, u, h0 + g, c, acc[g], m, l_row);
+}
+
+// ------------------------------------------- split kernel, VALU dot2 QK ---
+//
+// Lane l = 16r + c holds dims 8c..8c+7 of tokens 4i + r (i = 0..3) for both
+// K and V.  Partial dots over those 8 dims (bf16 dot2) are summed over the 16
+// lanes of the row with DPP; each row r keeps its own online softmax over its
+// tokens and the four rows are merged with the log-sum-exp rule at the end.
+
+template <int G, bool CHECKED>
+__global__ __launch_bounds__(kWave) void split_valu_bf16(SplitArgs a)
+{
+    UnitCoords u;
+    if (!unit_coords<CHECKED>(a, u)) {
+        write_zero_rows<G>(a, u);
+        return;
+    }
+    int32_t my_page;
+    if (!load_unit_pages<CHECKED>(a, u, my_page))
+        return;
+
+    const int lane = threadIdx.x;
+    const int r = lane >> 4, c = lane & 15;
+    const int h0 = u.kvh * G;
+
+    uint4 qv[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+        qv[g] = *reinterpret_cast<const uint4*>(
+            a.q + ((int64_t)u.b * a.num_q_heads + h0 + g) * kHeadDim + 8 * c);
+
+    float m[G], l[G], acc[G][8];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+        m[g] = -INFINITY;
+        l[g] = 0.0f;
+#pragma unroll
+        for (int d = 0; d < 8; ++d)
+            acc[g][d] = 0.0f;
+    }
+
+    const int off = lane * 16;
+    auto issue = [&](uint4 (&kbuf)[4], uint4 (&vbuf)[4], int j) {
+        const int64_t page = __builtin_amdgcn_readlane(my_page, j - u.p0);
+        const uint8_t* ks = slab_base(a.k_pool, page, a.num_kv_heads, u.kvh, kSlabBytesBf16);
+        const uint8_t* vs = slab_base(a.v_pool, page, a.num_kv_heads, u.kvh, kSlabBytesBf16);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            kbuf[i] = *reinterpret_cast<const uint4*>(ks + off + 1024 * i);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            vbuf[i] = *reinterpret_cast<const uint4*>(vs + off + 1024 * i);
+    };
+
+    auto consume = [&](uint4 (&kbuf)[4], uint4 (&vbuf)[4], int j) {
+        const int valid = u.seq_len - j * kPageSize;
+        float sc[G][4];
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                float t = dot2_bf16(qv[g].x, kbuf[i].x, 0.0f);
+                t = dot2_bf16(qv[g].y, kbuf[i].y, t);
+                t = dot2_bf16(qv[g].z, kbuf[i].z, t);
+                t = dot2_bf16(qv[g].w, kbuf[i].w, t);
+                t = row16_sum(t) * a.scale_log2;
+                sc[g][i] = (4 * i + r < valid) ? t : -INFINITY;
+            }
+
+        float p[G][4];
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            const float mx = fmaxf(fmaxf(sc[g][0], sc[g][1]), fmaxf(sc[g][2], sc[g][3]));
+            const float m_new = fmaxf(m[g], mx);
+            // A row may see no valid token of a short last page: keep it empty.
+            const bool empty = m_new == -INFINITY;
+            const float alpha = empty ? 1.0f : exp2_fast(m[g] - m_new);
+            float sum = 0.0f;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                p[g][i] = empty ? 0.0f : exp2_fast(sc[g][i] - m_new);
+                sum += p[g][i];
+            }
+            l[g] = l[g] * alpha + sum;
+            m[g] = m_new;
+#pragma unroll
+            for (int d = 0; d < 8; ++d)
+                acc[g][d] *= alpha;
+        }
+
+        if (valid < kPageSize) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                if (4 * i + r >= valid)
+                    vbuf[i] = make_uint4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            float v[8];
+            unpack8(vbuf[i], v);
+#pragma unroll
+            for (int g = 0; g < G; ++g)
+#pragma unroll
+                for (int d = 0; d < 8; ++d)
+                    acc[g][d] = fmaf(p[g][i], v[d], acc[g][d]);
+        }
+    };
+
+    uint4 ka[4], va[4], kb[4], vb[4];
+    stream_pages(u.p0, u.p1, ka, va, kb, vb, issue, consume);
+
+    // Merge the four rows: rescale each to the common max, then add.
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+        float M = fmaxf(m[g], __shfl_xor(m[g], 16));
+        M = fmaxf(M, __shfl_xor(M, 32));  // finite: row 0 holds token 0 of page p0
+        const float w = (m[g] == -INFINITY) ? 0.0f : exp2_fast(m[g] - M);
+        float lw = l[g] * w;
+        lw += __shfl_xor(lw, 16);
+        lw += __shfl_xor(lw, 32);
+        l[g] = lw;
+        m[g] = M;
+#pragma unroll
+        for (int d = 0; d < 8; ++d) {
+            float v = acc[g][d] * w;
+            v += __shfl_xor(v, 16);
+            v += __shfl_xor(v, 32);
+            acc[g][d] = v;
+        }
+    }
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+        if ((g & 3) == r)
+            store_unit_row(a, u, h0 + g, c, acc[g], m[g], l[g]);
+}
+
+// -------------------------------------------------------- merge kernel ---
+//
+// One wavefront per (b, h): M = max_s m_s, w_s = 2^(m_s - M),
+// out = sum_s w_s acc_s / sum_s w_s l_s, summed in split order.
+
+struct MergeArgs {
+    const int32_t* seq_lens;
+    const float* ws_acc;
+    const float* ws_ml;
+    uint16_t* out;
+    int32_t num_q_heads;
+    int32_t max_pages;
+    int32_t split_pages;
+    int32_t num_splits;
+};
+
+__global__ __launch_bounds__(kWave) void merge_splits(MergeArgs a)
+{
+    const int64_t row = blockIdx.x;  // b * Hq + h
+    const int b = (int)(row / a.num_q_heads);
+    const int L = min(a.seq_lens[b], a.max_pages * kPageSize);
+    const int npages = L > 0 ? (L + kPageSize - 1) / kPageSize : 0;
+    const int n = (npages + a.split_pages - 1) / a.split_pages;
+    if (n <= 1)
+        return;  // finished by the split kernel
+    const int lane = threadIdx.x;
+    const float* ml = a.ws_ml + row * a.num_splits * 2;
+    float M = -INFINITY;
+    for (int s = 0; s < n; ++s)
+        M = fmaxf(M, ml[2 * s]);
+    float den = 0.0f, num0 = 0.0f, num1 = 0.0f;
+    const float* acc = a.ws_acc + row * a.num_splits * kHeadDim + 2 * lane;
+    for (int s = 0; s < n; ++s) {
+        const float w = exp2_fast(ml[2 * s] - M);
+        den = fmaf(w, ml[2 * s + 1], den);
+        const float2 v = *reinterpret_cast<const float2*>(acc + (int64_t)s * kHeadDim);
+        num0 = fmaf(w, v.x, num0);
+        num1 = fmaf(w, v.y, num1);
+    }
+    const float inv = 1.0f / den;
+    *reinterpret_cast<uint32_t*>(a.out + row * kHeadDim + 2 * lane) =
+        f32_to_bf16(num0 * inv) | (f32_to_bf16(num1 * inv) << 16);
+}
+
+// ------------------------------------------------------------ dispatch ---
+
+typedef void (*SplitKernel)(SplitArgs);
+
+template <int G, bool CHECKED>
+SplitKernel pick_bf16(bool mfma)
+{
+    if constexpr (G <= 4) {
+        if (mfma)
+            return split_mfma_bf16<G, CHECKED>;
+    }
+    return split_valu_bf16<G, CHECKED>;
+}
+
+SplitKernel select_split_kernel(int G, bool checked, bool mfma)
+{
+    switch (G) {
+    case 1: return checked ? pick_bf16<1, true>(mfma) : pick_bf16<1, false>(mfma);
+    case 2: return checked ? pick_bf16<2, true>(mfma) : pick_bf16<2, false>(mfma);
+    case 4: return checked ? pick_bf16<4, true>(mfma) : pick_bf16<4, false>(mfma);
+    case 8: return checked ? pick_bf16<8, true>(mfma) : pick_bf16<8, false>(mfma);
+    default: return nullptr;
+    }
+}
+
+}  // namespace
+
+// ----------------------------------------------------------- C interface ---
+
+struct rl_decode_attn {
+    rl_da_config cfg;
+    int split_tokens;
+    int split_pages;
+    int max_splits;
+    int device;
+    bool use_mfma;
+    SplitKernel split_kernel;
+    void* workspace;
+    size_t workspace_bytes;
+    float* ws_acc;
+    float* ws_ml;
+    int32_t* dev_error;
+    hipEvent_t ev_split_begin;
+    hipEvent_t ev_split_end;
+};
+
+namespace {
+
+// Validates cfg; on success fills the derived split geometry.
+rl_da_status check_config(const rl_da_config* cfg, int* split_tokens, int* split_pages,
+                          int* max_splits)
+{
+    if (cfg == nullptr)
+        return RL_DA_ERR_INVALID_ARG;
+    if (cfg->num_q_heads <= 0 || cfg->num_kv_heads <= 0 || cfg->head_dim <= 0 ||
+        cfg->page_size <= 0 || cfg->max_batch <= 0 || cfg->max_pages_per_seq <= 0 ||
+        cfg->split_tokens < 0)
+        return RL_DA_ERR_INVALID_ARG;
+    if (cfg->num_q_heads % cfg->num_kv_heads != 0)
+        return RL_DA_ERR_INVALID_ARG;
+    if ((cfg->flags & ~(RL_DA_CHECKED | RL_DA_SCORES_ON_VALU)) != 0)
+        return RL_DA_ERR_INVALID_ARG;
+    if (cfg->kv_dtype != RL_DA_KV_BF16 && cfg->kv_dtype != RL_DA_KV_FP8_E4M3)
+        return RL_DA_ERR_INVALID_ARG;
+    const int G = cfg->num_q_heads / cfg->num_kv_heads;
+    if (cfg->head_dim != kHeadDim || cfg->page_size != kPageSize ||
+        (G != 1 && G != 2 && G != 4 && G != 8))
+        return RL_DA_ERR_UNSUPPORTED;
+    if (cfg->kv_dtype != RL_DA_KV_BF16)
+        return RL_DA_ERR_UNSUPPORTED;
+    const int st = cfg->split_tokens == 0 ? kDefaultSplitTokens : cfg->split_tokens;
+    if (st % kPageSize != 0 || st > kMaxSplitTokens)
+        return RL_DA_ERR_UNSUPPORTED;
+    *split_tokens = st;
+    *split_pages = st / kPageSize;
+    *max_splits = (cfg->max_pages_per_seq + *split_pages - 1) / *split_pages;
+    return RL_DA_OK;
+}
+
+size_t workspace_bytes_for(const rl_da_config* cfg, int max_splits)
+{
+    const size_t rows = (size_t)cfg->max_batch * (size_t)cfg->num_q_heads * (size_t)max_splits;
+    size_t bytes = rows * kHeadDim * sizeof(float);      // acc
+    bytes += rows * 2 * sizeof(float);                    // (m, l)
+    bytes = (bytes + 255) & ~(size_t)255;
+    return bytes + 256;                                   // device error word
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+const char* rl_da_status_string(rl_da_status s)
+{
+    switch (s) {
+    case RL_DA_OK: return "ok";
+    case RL_DA_ERR_INVALID_ARG: return "invalid argument";
+    case RL_DA_ERR_UNSUPPORTED: return "unsupported configuration";
+    case RL_DA_ERR_OUT_OF_MEMORY: return "out of device memory";
+    case RL_DA_ERR_HIP: return "HIP runtime error";
+    }
+    return "unknown status";
+}
+
+rl_da_status rl_decode_attn_workspace_size(const rl_da_config* cfg, size_t* bytes)
+{
+    int st, sp, ms;
+    if (bytes == nullptr)
+        return RL_DA_ERR_INVALID_ARG;
+    const rl_da_status rc = check_config(cfg, &st, &sp, &ms);
+    if (rc != RL_DA_OK)
+        return rc;
+    *bytes = workspace_bytes_for(cfg, ms);
+    return RL_DA_OK;
+}
+
+rl_da_status rl_decode_attn_create(const rl_da_config* cfg, rl_decode_attn** out)
+{
+    if (out == nullptr)
+        return RL_DA_ERR_INVALID_ARG;
+    *out = nullptr;
+    int st, sp, ms;
+    const rl_da_status rc = check_config(cfg, &st, &sp, &ms);
+    if (rc != RL_DA_OK)
+        return rc;
+    rl_decode_attn* h = (rl_decode_attn*)calloc(1, sizeof(rl_decode_attn));
+    if (h == nullptr)
+        return RL_DA_ERR_OUT_OF_MEMORY;
+    h->cfg = *cfg;
+    h->split_tokens = st;
+    h->split_pages = sp;
+    h->max_splits = ms;
+    const int G = cfg->num_q_heads / cfg->num_kv_heads;
+    h->use_mfma = G <= 4 && (cfg->flags & RL_DA_SCORES_ON_VALU) == 0;
+    h->split_kernel = select_split_kernel(G, (cfg->flags & RL_DA_CHECKED) != 0, h->use_mfma);
+    if (hipGetDevice(&h->device) != hipSuccess) {
+        free(h);
+        return RL_DA_ERR_HIP;
+    }
+    h->workspace_bytes = workspace_bytes_for(cfg, ms);
+    if (hipMalloc(&h->workspace, h->workspace_bytes) != hipSuccess) {
+        (void)hipGetLastError();
+        free(h);
+        return RL_DA_ERR_OUT_OF_MEMORY;
+    }
+    const size_t rows = (size_t)cfg->max_batch * (size_t)cfg->num_q_heads * (size_t)ms;
+    h->ws_acc = (float*)h->workspace;
+    h->ws_ml = h->ws_acc + rows * kHeadDim;
+    h->dev_error = (int32_t*)((char*)h->workspace + h->workspace_bytes - 256);
+    if (hipMemset(h->dev_error, 0, sizeof(int32_t)) != hipSuccess) {
+        (void)hipFree(h->workspace);
+        free(h);
+        return RL_DA_ERR_HIP;
+    }
+    *out = h;
+    return RL_DA_OK;
+}
+
+rl_da_status rl_decode_attn_destroy(rl_decode_attn* h)
+{
+    if (h == nullptr)
+        return RL_DA_OK;
+    const hipError_t e = hipFree(h->workspace);
+    free(h);
+    return e == hipSuccess ? RL_DA_OK : RL_DA_ERR_HIP;
+}
+
+rl_da_status rl_decode_attn_split_info(const rl_decode_attn* h, int32_t max_pages,
+                                       int32_t* split_tokens, int32_t* num_splits)
+{
+    if (h == nullptr || split_tokens == nullptr || num_splits == nullptr || max_pages < 1 ||
+        max_pages > h->cfg.max_pages_per_seq)
+        return RL_DA_ERR_INVALID_ARG;
+    *split_tokens = h->split_tokens;
+    *num_splits = (max_pages + h->split_pages - 1) / h->split_pages;
+    return RL_DA_OK;
+}
+
+rl_da_status rl_decode_attn_run(rl_decode_attn* h, const void* q, const void* k_pool,
+                                const void* v_pool, const float* k_scale,
+                                const float* v_scale, int64_t num_pages,
+                                const int32_t* block_table, int32_t max_pages,
+                                const int32_t* seq_lens, int32_t batch, float scale, void* out,
+                                void* stream)
+{
+    if (h == nullptr)
+        return RL_DA_ERR_INVALID_ARG;
+    const rl_da_config& cfg = h->cfg;
+    if (batch < 0 || batch > cfg.max_batch)
+        return RL_DA_ERR_INVALID_ARG;
+    if (max_pages < 1 || max_pages > cfg.max_pages_per_seq || num_pages < 1)
+        return RL_DA_ERR_INVALID_ARG;
+    if (!isfinite(scale))
+        return RL_DA_ERR_INVALID_ARG;
+    if (q == nullptr || k_pool == nullptr || v_pool == nullptr || block_table == nullptr ||
+        seq_lens == nullptr || out == nullptr)
+        return RL_DA_ERR_INVALID_ARG;
+    if (!aligned16(q) || !aligned16(k_pool) || !aligned16(v_pool) || !aligned16(out))
+        return RL_DA_ERR_INVALID_ARG;
+    const bool fp8 = cfg.kv_dtype == RL_DA_KV_FP8_E4M3;
+    if (fp8 != (k_scale != nullptr) || fp8 != (v_scale != nullptr))
+        return RL_DA_ERR_INVALID_ARG;
+    if (batch == 0)
+        return RL_DA_OK;
+
+    const int num_splits = (max_pages + h->split_pages - 1) / h->split_pages;
+    const int64_t units = (int64_t)batch * cfg.num_kv_heads * num_splits;
+    if (units > INT32_MAX)
+        return RL_DA_ERR_UNSUPPORTED;
+
+    SplitArgs sa;
+    sa.q = (const uint16_t*)q;
+    sa.k_pool = (const uint8_t*)k_pool;
+    sa.v_pool = (const uint8_t*)v_pool;
+    sa.k_scale = k_scale;
+    sa.v_scale = v_scale;
+    sa.block_table = block_table;
+    sa.seq_lens = seq_lens;
+    sa.out = (uint16_t*)out;
+    sa.ws_acc = h->ws_acc;
+    sa.ws_ml = h->ws_ml;
+    sa.dev_error = h->dev_error;
+    sa.num_pages = num_pages;
+    sa.num_q_heads = cfg.num_q_heads;
+    sa.num_kv_heads = cfg.num_kv_heads;
+    sa.max_pages = max_pages;
+    sa.split_pages = h->split_pages;
+    sa.num_splits = num_splits;
+    sa.scale_log2 = scale * kLog2e;
+
+    hipStream_t st = (hipStream_t)stream;
+    if (h->ev_split_begin != nullptr && hipEventRecord(h->ev_split_begin, st) != hipSuccess)
+        return RL_DA_ERR_HIP;
+    hipLaunchKernelGGL(h->split_kernel, dim3((unsigned)units), dim3(kWave), 0, st, sa);
+    if (hipGetLastError() != hipSuccess)
+        return RL_DA_ERR_HIP;
+    if (h->ev_split_end != nullptr && hipEventRecord(h->ev_split_end, st) != hipSuccess)
+        return RL_DA_ERR_HIP;
+    if (num_splits > 1) {
+        MergeArgs ma;
+        ma.seq_lens = seq_lens;
+        ma.ws_acc = h->ws_acc;
+        ma.ws_ml = h->ws_ml;
+        ma.out = (uint16_t*)out;
+        ma.num_q_heads = cfg.num_q_heads;
+        ma.max_pages = max_pages;
+        ma.split_pages = h->split_pages;
+        ma.num_splits = num_splits;
+        hipLaunchKernelGGL(merge_splits, dim3((unsigned)((int64_t)batch * cfg.num_q_heads)),
+                           dim3(kWave), 0, st, ma);
+        if (hipGetLastError() != hipSuccess)
+            return RL_DA_ERR_HIP;
+    }
+    return RL_DA_OK;
+}
+
+rl_da_status rl_decode_attn_set_timing_events(rl_decode_attn* h, void* split_begin,
+                                              void* split_end)
+{
+    if (h == nullptr || (split_begin == nullptr) != (split_end == nullptr))
+        return RL_DA_ERR_INVALID_ARG;
+    h->ev_split_begin = (hipEvent_t)split_begin;
+    h->ev_split_end = (hipEvent_t)split_end;
+    return RL_DA_OK;
+}
+
+rl_da_status rl_decode_attn_check_error(rl_decode_attn* h, int32_t* device_error)
+{
+    if (h == nullptr || device_error == nullptr)
+        return RL_DA_ERR_INVALID_ARG;
+    if ((h->cfg.flags & RL_DA_CHECKED) == 0)
+        return RL_DA_ERR_UNSUPPORTED;
+    if (hipDeviceSynchronize() != hipSuccess)
+        return RL_DA_ERR_HIP;
+    int32_t v = 0;
+    if (hipMemcpy(&v, h->dev_error, sizeof v, hipMemcpyDeviceToHost) != hipSuccess)
+        return RL_DA_ERR_HIP;
+    if (hipMemset(h->dev_error, 0, sizeof v) != hipSuccess)
+        return RL_DA_ERR_HIP;
+    *device_error = v;
+    return RL_DA_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,103 @@
+"""The C interface: every declared symbol is exported, and host-side
+validation answers with the documented status codes (CPU only: create()
+validates its configuration before touching the HIP runtime)."""
+import ctypes
+import glob
+import os
+import re
+
+import pytest
+
+from paper_2512_22492_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    names = []
+    for path in glob.glob(os.path.join(ROOT, "include", "*.h")):
+        text = open(path).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        names += re.findall(r"\b(rl_\w+)\s*\(", text)
+    return names
+
+
+def test_every_declared_function_is_exported():
+    lib = B.load_library()
+    names = declared_functions()
+    assert set(names) == set(B.EXPORTED)
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def test_library_needs_no_torch():
+    # The boundary is plain C over the HIP runtime: no torch/c10 dependency.
+    import subprocess
+    out = subprocess.run(["readelf", "-d", B.library_path()], stdout=subprocess.PIPE,
+                         universal_newlines=True, check=True).stdout
+    needed = re.findall(r"\(NEEDED\)\s+Shared library: \[(.+?)\]", out)
+    assert "libamdhip64.so.7" in needed
+    assert not [n for n in needed if "torch" in n or "c10" in n], needed
+
+
+def test_status_strings():
+    assert B.rl_da_status_string(B.RL_DA_OK) == "ok"
+    for s in (1, 2, 3, 4):
+        assert B.rl_da_status_string(s) not in ("ok", "unknown status")
+    assert B.rl_da_status_string(99) == "unknown status"
+
+
+def cfg(**kw):
+    base = dict(num_q_heads=32, num_kv_heads=8, max_batch=64, max_pages_per_seq=256)
+    base.update(kw)
+    hq, hkv, mb, mp = (base.pop(k) for k in ("num_q_heads", "num_kv_heads", "max_batch",
+                                             "max_pages_per_seq"))
+    return B.make_config(hq, hkv, mb, mp, **base)
+
+
+def test_workspace_size_formula():
+    rc, n = B.rl_decode_attn_workspace_size(cfg())
+    assert rc == B.RL_DA_OK
+    splits = 256 // 32                       # 512-token splits of 16-token pages
+    rows = 64 * 32 * splits
+    expect = (rows * 128 * 4 + rows * 2 * 4 + 255) // 256 * 256 + 256
+    assert n == expect
+    rc, n2 = B.rl_decode_attn_workspace_size(cfg(split_tokens=1024))
+    assert rc == B.RL_DA_OK and n2 < n
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(num_q_heads=0), B.RL_DA_ERR_INVALID_ARG),
+    (dict(num_kv_heads=-1), B.RL_DA_ERR_INVALID_ARG),
+    (dict(num_q_heads=30, num_kv_heads=8), B.RL_DA_ERR_INVALID_ARG),
+    (dict(max_batch=0), B.RL_DA_ERR_INVALID_ARG),
+    (dict(max_pages_per_seq=0), B.RL_DA_ERR_INVALID_ARG),
+    (dict(split_tokens=-16), B.RL_DA_ERR_INVALID_ARG),
+    (dict(flags=0x80), B.RL_DA_ERR_INVALID_ARG),
+    (dict(kv_dtype=7), B.RL_DA_ERR_INVALID_ARG),
+    (dict(head_dim=64), B.RL_DA_ERR_UNSUPPORTED),
+    (dict(page_size=32), B.RL_DA_ERR_UNSUPPORTED),
+    (dict(num_q_heads=24, num_kv_heads=8), B.RL_DA_ERR_UNSUPPORTED),   # G = 3
+    (dict(num_q_heads=128, num_kv_heads=8), B.RL_DA_ERR_UNSUPPORTED),  # G = 16
+    (dict(split_tokens=24), B.RL_DA_ERR_UNSUPPORTED),
+    (dict(split_tokens=2048), B.RL_DA_ERR_UNSUPPORTED),
+])
+def test_create_rejects_bad_config_without_gpu(kw, status):
+    c = cfg(**kw)
+    rc, h = B.rl_decode_attn_create(c)
+    assert rc == status and h is None
+    rc2, _ = B.rl_decode_attn_workspace_size(c)
+    assert rc2 == status
+
+
+def test_null_arguments():
+    lib = B.load_library()
+    h = ctypes.c_void_p()
+    assert lib.rl_decode_attn_create(None, ctypes.byref(h)) == B.RL_DA_ERR_INVALID_ARG
+    assert lib.rl_decode_attn_create(ctypes.byref(cfg()), None) == B.RL_DA_ERR_INVALID_ARG
+    assert B.rl_decode_attn_destroy(None) == B.RL_DA_OK
+    assert lib.rl_decode_attn_run(None, 1, 1, 1, None, None, 1, 1, 1, 1, 1, 1.0, 1,
+                                  None) == B.RL_DA_ERR_INVALID_ARG
+    v = ctypes.c_int32()
+    assert lib.rl_decode_attn_check_error(None, ctypes.byref(v)) == B.RL_DA_ERR_INVALID_ARG
+    assert lib.rl_decode_attn_workspace_size(None, None) == B.RL_DA_ERR_INVALID_ARG
