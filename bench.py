@@ -22,6 +22,62 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+COPY_CALIBRATION_BYTES = 1 << 30
+
+
+def bench_kernels():
+    """ctypes handle of the measurement-only kernel library."""
+    import ctypes
+    import torch  # noqa: F401  (binds the library to torch's HIP runtime)
+    from paper_2512_22492_amd import build
+    lib = ctypes.CDLL(build.BENCH_LIB_PATH)
+    vp, sz, i32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32
+    lib.rl_bench_copy.argtypes = [vp, vp, sz, vp]
+    lib.rl_bench_stream_read.argtypes = [vp, sz, vp, ctypes.c_int, vp]
+    lib.rl_bench_page_read.argtypes = [vp, vp, vp, i32, vp, i32, i32, i32, vp, vp]
+    for f in (lib.rl_bench_copy, lib.rl_bench_stream_read, lib.rl_bench_page_read):
+        f.restype = ctypes.c_int
+    return lib
+
+
+def read_ceilings(p, split_pages, stream):
+    """Achievable read bandwidth: a contiguous 4 GiB stream, and the decode
+    step's own K/V page reads with no arithmetic.  Best of several runs."""
+    import torch
+    lib = bench_kernels()
+    s = stream.cuda_stream
+    nbytes = 4 << 30
+    buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    best_stream = 0.0
+    for grid in (2048, 4096, 8192):
+        sink = torch.empty(grid * 256, dtype=torch.int32, device="cuda")
+        for it in range(6):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            assert lib.rl_bench_stream_read(buf.data_ptr(), nbytes, sink.data_ptr(), grid, s) == 0
+            e1.record(stream)
+            e1.synchronize()
+            if it:
+                best_stream = max(best_stream, nbytes / (e0.elapsed_time(e1) / 1e3) / 1e9)
+    del buf
+    units = p.batch * p.num_kv_heads * ((p.max_pages + split_pages - 1) // split_pages)
+    sink = torch.empty(units * 64, dtype=torch.int32, device="cuda")
+    best_page = 0.0
+    kv = p.kv_bytes()
+    if p.kv_dtype == "bf16":
+        for it in range(6):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            assert lib.rl_bench_page_read(p.k_pool.data_ptr(), p.v_pool.data_ptr(),
+                                          p.block_table.data_ptr(), p.max_pages,
+                                          p.seq_lens.data_ptr(), p.batch, p.num_kv_heads,
+                                          split_pages, sink.data_ptr(), s) == 0
+            e1.record(stream)
+            e1.synchronize()
+            if it:
+                best_page = max(best_page, kv / (e0.elapsed_time(e1) / 1e3) / 1e9)
+    return {"stream_read_GBs": round(best_stream, 1),
+            "page_read_GBs": round(best_page, 1) if best_page else None}
 
 
 def parse_args():
@@ -40,7 +96,66 @@ def parse_args():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-events", action="store_true",
                     help="do not record events around the split kernel (profiling runs)")
+    ap.add_argument("--no-ceilings", action="store_true",
+                    help="skip the read-ceiling measurements")
+    ap.add_argument("--pmc-calibrate", action="store_true",
+                    help="launch one plain copy of %d bytes first, so that a counter "
+                         "run can scale FETCH_SIZE/WRITE_SIZE" % COPY_CALIBRATION_BYTES)
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="turn two rocprofv3 --pmc counter_collection.csv files (FETCH_SIZE, "
+                         "WRITE_SIZE) of a --pmc-calibrate run into profiles/traffic.json")
     return ap.parse_args()
+
+
+def _pmc_means(path, counter):
+    """Mean counter value per kernel name in a rocprofv3 counter_collection.csv."""
+    import csv
+    sums = {}
+    with open(path) as f:
+        for row in csv.DictReader(f):
+            if row.get("Counter_Name") != counter:
+                continue
+            name = row["Kernel_Name"]
+            tot, n = sums.get(name, (0.0, 0))
+            sums[name] = (tot + float(row["Counter_Value"]), n + 1)
+    return {k: v[0] / v[1] for k, v in sums.items()}
+
+
+def summarize_pmc(fetch_csv, write_csv, config):
+    """HBM bytes per split-kernel launch, each counter scaled by its reading for
+    the calibration copy (which moves COPY_CALIBRATION_BYTES each way)."""
+    fetch = _pmc_means(fetch_csv, "FETCH_SIZE")
+    write = _pmc_means(write_csv, "WRITE_SIZE")
+
+    def pick(d, key):
+        names = [k for k in d if k.startswith(key)]
+        if len(names) != 1:
+            raise SystemExit("expected one kernel matching %r, got %s" % (key, names))
+        return d[names[0]]
+
+    copy_kib = COPY_CALIBRATION_BYTES / 1024.0
+    copy_name = "(anonymous namespace)::copy_kernel"
+    split_name = "void (anonymous namespace)::split_"
+    f_scale = copy_kib / pick(fetch, copy_name)
+    w_scale = copy_kib / pick(write, copy_name)
+    split_f = pick(fetch, split_name)
+    split_w = pick(write, split_name)
+    entry = {
+        "kernel_source_sha256": kernel_source_sha(),
+        "fetch_kib_raw": split_f, "write_kib_raw": split_w,
+        "fetch_scale": f_scale, "write_scale": w_scale,
+        "bytes_per_launch": int(round((split_f * f_scale + split_w * w_scale) * 1024)),
+    }
+    try:
+        with open(TRAFFIC_FILE) as f:
+            data = json.load(f)
+    except (OSError, ValueError):
+        data = {}
+    data[config] = entry
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(data, f, indent=1, sort_keys=True)
+        f.write("\n")
+    print(json.dumps(entry))
 
 
 def algorithmic_bytes(p):
@@ -105,6 +220,9 @@ def cpu_baseline(p, rows_per_call=None):
 
 def main():
     args = parse_args()
+    if args.summarize_pmc:
+        summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.config)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -143,6 +261,14 @@ def main():
     for e in ev_b + ev_e:
         e.record(stream)          # materialises the underlying hipEvent_t
     torch.cuda.synchronize()
+
+    if args.pmc_calibrate:
+        src = torch.empty(COPY_CALIBRATION_BYTES, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        assert bench_kernels().rl_bench_copy(dst.data_ptr(), src.data_ptr(),
+                                             COPY_CALIBRATION_BYTES, stream.cuda_stream) == 0
+        torch.cuda.synchronize()
+        del src, dst
 
     for i in range(args.warmup):
         attn.run_problem(replicas[i % len(replicas)], out, stream)
@@ -200,6 +326,13 @@ def main():
             "bytes_per_launch": alg_bytes,
         }
     attn.close()
+    if not args.no_ceilings:
+        print("bench: measuring read ceilings", file=sys.stderr, flush=True)
+        ceil = read_ceilings(base, split_tokens // base.page_size, stream)
+        record["read_ceiling"] = ceil
+        if "roofline" in record and ceil["stream_read_GBs"]:
+            record["roofline"]["frac_of_stream_read"] = round(
+                record["roofline"]["achieved"] / ceil["stream_read_GBs"], 4)
     if not args.no_cpu_baseline:
         print("bench: timing the CPU oracle", file=sys.stderr, flush=True)
         record["cpu_baseline"] = cpu_baseline(base)

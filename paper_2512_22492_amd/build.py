@@ -9,6 +9,9 @@ ROOT = os.path.dirname(PKG_DIR)
 SOURCES = [os.path.join(PKG_DIR, "csrc", "rl_decode_attn.hip")]
 INCLUDE = os.path.join(ROOT, "include")
 LIB_PATH = os.path.join(PKG_DIR, "librl_decode_attn.so")
+# measurement-only kernels used by bench.py (stream-read ceiling, copy)
+BENCH_SOURCES = [os.path.join(PKG_DIR, "csrc", "rl_bench_kernels.hip")]
+BENCH_LIB_PATH = os.path.join(PKG_DIR, "librl_bench_kernels.so")
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
@@ -24,16 +27,29 @@ def hipcc() -> str:
     return path if os.path.exists(path) else "hipcc"
 
 
-def build_library(verbose: bool = False) -> str:
-    """Compile the library (always), atomically replacing any previous build."""
-    tmp = LIB_PATH + ".tmp%d" % os.getpid()
-    cmd = [hipcc()] + HIPCC_FLAGS + ["-I", INCLUDE] + SOURCES + ["-o", tmp]
+def _compile(sources, out, verbose):
+    tmp = out + ".tmp%d" % os.getpid()
+    cmd = [hipcc()] + HIPCC_FLAGS + ["-I", INCLUDE] + sources + ["-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB_PATH)
-    return LIB_PATH
+    os.replace(tmp, out)
+    return out
+
+
+def build_library(verbose: bool = False) -> str:
+    """Compile the attention library (always), atomically replacing any
+    previous build."""
+    return _compile(SOURCES, LIB_PATH, verbose)
+
+
+def build_bench_library(verbose: bool = False) -> str:
+    return _compile(BENCH_SOURCES, BENCH_LIB_PATH, verbose)
+
+
+def build_all(verbose: bool = False):
+    return build_library(verbose), build_bench_library(verbose)
 
 
 if __name__ == "__main__":
-    print(build_library(verbose=True))
+    print(build_all(verbose=True))

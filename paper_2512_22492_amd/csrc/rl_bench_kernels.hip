@@ -1,0 +1,148 @@
+// rl_bench_kernels.hip -- measurement-only kernels for the decode-attention
+// benchmark (not part of the attention path).
+//
+//   rl_bench_copy         plain 16-byte-per-lane copy of a known byte count; its
+//                         FETCH_SIZE / WRITE_SIZE readings calibrate the HBM
+//                         traffic counters.
+//   rl_bench_stream_read  contiguous read of a buffer: the achievable HBM read
+//                         bandwidth on this GPU.
+//   rl_bench_page_read    reads exactly the K/V bytes one decode step reads, in
+//                         the same (sequence, kv head, split) work units and
+//                         the same per-lane load pattern as the split-K
+//                         attention kernel, with no arithmetic: the ceiling of
+//                         that access pattern.
+//
+// All pointers are device pointers owned by the caller.  Each function
+// enqueues one kernel on `stream` and returns 0, or -1 on bad arguments, or the
+// HIP error code of the launch.
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace {
+
+constexpr int kBlock = 256;
+
+__global__ __launch_bounds__(kBlock) void copy_kernel(uint4* __restrict__ dst,
+                                                      const uint4* __restrict__ src, size_t n)
+{
+    const size_t stride = (size_t)gridDim.x * kBlock;
+    for (size_t i = (size_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += stride)
+        dst[i] = src[i];
+}
+
+__global__ __launch_bounds__(kBlock) void stream_read_kernel(const uint4* __restrict__ src,
+                                                             size_t n, uint32_t* sink)
+{
+    const size_t stride = (size_t)gridDim.x * kBlock;
+    uint32_t acc = 0;
+    size_t i = (size_t)blockIdx.x * kBlock + threadIdx.x;
+    for (; i + 3 * stride < n; i += 4 * stride) {
+        const uint4 a = src[i], b = src[i + stride], c = src[i + 2 * stride],
+                    d = src[i + 3 * stride];
+        acc ^= a.x ^ a.y ^ a.z ^ a.w ^ b.x ^ b.y ^ b.z ^ b.w ^ c.x ^ c.y ^ c.z ^ c.w ^ d.x ^
+               d.y ^ d.z ^ d.w;
+    }
+    for (; i < n; i += stride) {
+        const uint4 a = src[i];
+        acc ^= a.x ^ a.y ^ a.z ^ a.w;
+    }
+    // one value per thread keeps every load live; the sink holds grid*block words
+    sink[(size_t)blockIdx.x * kBlock + threadIdx.x] = acc;
+}
+
+struct PageReadArgs {
+    const uint8_t* k_pool;
+    const uint8_t* v_pool;
+    const int32_t* block_table;
+    const int32_t* seq_lens;
+    uint32_t* sink;
+    int32_t num_kv_heads;
+    int32_t max_pages;
+    int32_t split_pages;
+    int32_t num_splits;
+};
+
+__global__ __launch_bounds__(64) void page_read_kernel(PageReadArgs a)
+{
+    const int unit = blockIdx.x;
+    const int s = unit % a.num_splits;
+    const int bk = unit / a.num_splits;
+    const int kvh = bk % a.num_kv_heads;
+    const int b = bk / a.num_kv_heads;
+    const int lane = threadIdx.x;
+    const int L = min(a.seq_lens[b], a.max_pages * 16);
+    const int npages = L > 0 ? (L + 15) / 16 : 0;
+    const int p0 = s * a.split_pages;
+    const int p1 = min(p0 + a.split_pages, npages);
+    uint32_t acc = 0;
+    const int koff = (lane & 15) * 256 + 16 * (lane >> 4);
+    const int voff = lane * 16;
+    for (int j = p0; j < p1; ++j) {
+        const int64_t page = a.block_table[(int64_t)b * a.max_pages + j];
+        const int64_t slab = (page * a.num_kv_heads + kvh) * 4096;
+        uint4 k[4], v[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            k[i] = *reinterpret_cast<const uint4*>(a.k_pool + slab + koff + 64 * i);
+            v[i] = *reinterpret_cast<const uint4*>(a.v_pool + slab + voff + 1024 * i);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            acc ^= k[i].x ^ k[i].y ^ k[i].z ^ k[i].w ^ v[i].x ^ v[i].y ^ v[i].z ^ v[i].w;
+    }
+    a.sink[(size_t)unit * 64 + lane] = acc;
+}
+
+}  // namespace
+
+extern "C" {
+
+int rl_bench_copy(void* dst, const void* src, size_t bytes, void* stream)
+{
+    if (dst == nullptr || src == nullptr || bytes % 16 != 0)
+        return -1;
+    const size_t n = bytes / 16;
+    const unsigned grid = 256 * 32;
+    hipLaunchKernelGGL(copy_kernel, dim3(grid), dim3(kBlock), 0, (hipStream_t)stream,
+                       (uint4*)dst, (const uint4*)src, n);
+    return (int)hipGetLastError();
+}
+
+// sink must hold grid_blocks * 256 uint32 words.
+int rl_bench_stream_read(const void* src, size_t bytes, uint32_t* sink, int grid_blocks,
+                         void* stream)
+{
+    if (src == nullptr || sink == nullptr || bytes % 16 != 0 || grid_blocks <= 0)
+        return -1;
+    hipLaunchKernelGGL(stream_read_kernel, dim3((unsigned)grid_blocks), dim3(kBlock), 0,
+                       (hipStream_t)stream, (const uint4*)src, bytes / 16, sink);
+    return (int)hipGetLastError();
+}
+
+// bf16 pools [P][Hkv][16][128]; sink must hold batch*num_kv_heads*num_splits*64 words.
+int rl_bench_page_read(const void* k_pool, const void* v_pool, const int32_t* block_table,
+                       int32_t max_pages, const int32_t* seq_lens, int32_t batch,
+                       int32_t num_kv_heads, int32_t split_pages, uint32_t* sink, void* stream)
+{
+    if (k_pool == nullptr || v_pool == nullptr || block_table == nullptr ||
+        seq_lens == nullptr || sink == nullptr || batch <= 0 || num_kv_heads <= 0 ||
+        max_pages <= 0 || split_pages <= 0)
+        return -1;
+    PageReadArgs a;
+    a.k_pool = (const uint8_t*)k_pool;
+    a.v_pool = (const uint8_t*)v_pool;
+    a.block_table = block_table;
+    a.seq_lens = seq_lens;
+    a.sink = sink;
+    a.num_kv_heads = num_kv_heads;
+    a.max_pages = max_pages;
+    a.split_pages = split_pages;
+    a.num_splits = (max_pages + split_pages - 1) / split_pages;
+    const int64_t units = (int64_t)batch * num_kv_heads * a.num_splits;
+    hipLaunchKernelGGL(page_read_kernel, dim3((unsigned)units), dim3(64), 0,
+                       (hipStream_t)stream, a);
+    return (int)hipGetLastError();
+}
+
+}  // extern "C"
