@@ -2,21 +2,28 @@
 //
 // One decode step of one attention layer (the rollout inner loop of
 // arXiv 2512.22492, Sec. 2.1): out[b,h] = softmax(scale * q[b,h] K_b^T) V_b
-// over a paged KV cache, kv head h / G.  The operation is split-K
-// ("flash-decoding"): each work unit (sequence b, kv head, split s) scans
-// split_tokens consecutive cached tokens and keeps an online softmax (running
-// max m, running sum l, weighted value sum acc) for the G query heads that
-// share the kv head; a second kernel merges the per-split partials with the
-// log-sum-exp rule.  Sequences that fit in one split are finished by the first
-// kernel directly.
+// over a paged KV cache, kv head h / G.
+//
+// Decomposition (split-K, "flash-decoding").  A work unit is one work-group of
+// four wavefronts for (sequence b, kv head, split s), where a split is
+// split_tokens consecutive cached tokens (4096 by default).  The wavefronts
+// take the split's pages in turn (wavefront w: pages w, w+4, w+8, ...); each
+// keeps an online softmax (running max m, running sum l, weighted value sum
+// acc) for the G query heads that share the kv head.  The four partial states
+// are merged with the log-sum-exp rule through LDS at the end of the unit, so a
+// sequence that fits one split is finished by one work-group; longer sequences
+// write one partial per split and a second kernel merges them.  How a
+// sequence's tokens are divided depends only on its own length and the
+// handle's split size, never on the rest of the batch.
 //
 // Data movement is the whole cost: every K/V byte is read once from HBM.  A
 // (page, kv head) slab is 16 tokens x 128 dims x 2 bytes = 4 KiB, contiguous in
 // the [page][kv head][slot][dim] pool layout, and is read by one wavefront
-// with four 16-byte-per-lane loads.  Scores are computed once per kv head for
-// all G query heads of the group (the GQA reuse), either with one MFMA per
-// 32 dims (the G query rows packed into a 16-row tile) or with bf16 dot2 ops
-// and DPP row reductions; the value accumulation runs in fp32 on the VALU.
+// with four 16-byte-per-lane non-temporal loads.  Scores are computed once per
+// kv head for all G query heads of the group (the GQA reuse), either with one
+// MFMA per 32 dims (the G query rows packed into a 16-row tile) or with bf16
+// dot2 ops and DPP row reductions; the value accumulation runs in fp32 on the
+// VALU.
 //
 // All arithmetic is fp32; scores are kept in the log2 domain (scale folded
 // with log2(e)) so that every exponential is one v_exp_f32.
@@ -34,14 +41,17 @@ namespace {
 constexpr int kHeadDim = 128;
 constexpr int kPageSize = 16;
 constexpr int kWave = 64;
-constexpr int kDefaultSplitTokens = 512;
-constexpr int kMaxSplitTokens = 1024;  // split pages must fit one wavefront
+constexpr int kUnitWaves = 4;                       // wavefronts per work unit
+constexpr int kDefaultSplitTokens = 4096;
+// each wavefront holds its pages' block-table entries one per lane
+constexpr int kMaxSplitTokens = kWave * kUnitWaves * kPageSize;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kSlabBytesBf16 = kPageSize * kHeadDim * 2;
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float floatx4_t __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
 struct SplitArgs {
     const uint16_t* q;          // bf16 bits [B][Hq][D]
@@ -121,6 +131,14 @@ __device__ __forceinline__ float row16_max(float v)
 
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// 16-byte load with the non-temporal hint: K/V bytes are read exactly once, so
+// they are streamed past the caches rather than kept.
+__device__ __forceinline__ uint4 load_stream16(const uint8_t* p)
+{
+    const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 // Orders LDS traffic between the lanes of one wavefront (the work-group is
 // a single wavefront, so no s_barrier and no wait on global loads is needed).
 __device__ __forceinline__ void wave_lds_sync()
@@ -138,71 +156,72 @@ __device__ __forceinline__ void unpack8(const uint4& w, float (&v)[8])
     v[6] = bf16_lo(w.w); v[7] = bf16_hi(w.w);
 }
 
-struct UnitCoords {
-    int b, kvh, s;
+// One wavefront's share of a work unit: pages p0 + wave + 4i, i < count.
+struct WaveTask {
+    int b, kvh, s, wave, lane;
     int seq_len;   // clamped to max_pages * page_size
     int npages;    // pages holding the sequence
-    int p0, p1;    // this unit's page range [p0, p1)
     int nsplit;    // splits of this sequence
+    int p0;        // first page of the unit
+    int count;     // pages of this wavefront (may be 0)
 };
 
-// Decodes blockIdx.x into (b, kvh, s); returns false when the unit is empty.
+// Decodes (blockIdx.x, wavefront) into a task and loads its block-table
+// entries (lane i: page p0 + wave + 4i) together with the sequence length.
+// Entries past the sequence's end lie inside the table row and are loaded
+// but never used.  Returns false, for every wavefront of the unit alike, when
+// the unit holds no page of its sequence.
 template <bool CHECKED>
-__device__ __forceinline__ bool unit_coords(const SplitArgs& a, UnitCoords& u)
+__device__ __forceinline__ bool begin_task(const SplitArgs& a, WaveTask& t, int32_t& my_page)
 {
+    t.lane = threadIdx.x % kWave;
+    t.wave = threadIdx.x / kWave;
     const int unit = blockIdx.x;
-    u.s = unit % a.num_splits;
+    t.s = unit % a.num_splits;
     const int bk = unit / a.num_splits;
-    u.kvh = bk % a.num_kv_heads;
-    u.b = bk / a.num_kv_heads;
-    int L = a.seq_lens[u.b];
+    t.kvh = bk % a.num_kv_heads;
+    t.b = bk / a.num_kv_heads;
+    t.p0 = t.s * a.split_pages;
+    const int col = t.p0 + t.wave + kUnitWaves * t.lane;
+    const bool in_split = col < t.p0 + a.split_pages && col < a.max_pages;
+    my_page = in_split ? a.block_table[(int64_t)t.b * a.max_pages + col] : 0;
+    int L = a.seq_lens[t.b];
     const int cap = a.max_pages * kPageSize;
     if (L > cap) {
-        if (CHECKED && threadIdx.x == 0 && u.s == 0 && u.kvh == 0)
+        if (CHECKED && threadIdx.x == 0 && t.s == 0 && t.kvh == 0)
             atomicOr(a.dev_error, RL_DA_DEVERR_LENGTH_TOO_LONG);
         L = cap;
     }
-    u.seq_len = L;
-    u.npages = L > 0 ? (L + kPageSize - 1) / kPageSize : 0;
-    u.nsplit = (u.npages + a.split_pages - 1) / a.split_pages;
-    u.p0 = u.s * a.split_pages;
-    u.p1 = min(u.p0 + a.split_pages, u.npages);
-    return u.p0 < u.p1;
-}
-
-// An empty sequence produces zeros (written once, by split 0).
-template <int G>
-__device__ __forceinline__ void write_zero_rows(const SplitArgs& a, const UnitCoords& u)
-{
-    if (u.npages != 0 || u.s != 0)
-        return;
-    const int lane = threadIdx.x;
-    for (int e = lane; e < G * (kHeadDim / 8); e += kWave) {
-        const int g = e / (kHeadDim / 8), chunk = e % (kHeadDim / 8);
-        uint4* dst = reinterpret_cast<uint4*>(
-            a.out + ((int64_t)u.b * a.num_q_heads + u.kvh * G + g) * kHeadDim + chunk * 8);
-        *dst = make_uint4(0, 0, 0, 0);
-    }
-}
-
-// Block-table entries of the unit's pages, one per lane (lane i: page p0+i).
-template <bool CHECKED>
-__device__ __forceinline__ bool load_unit_pages(const SplitArgs& a, const UnitCoords& u,
-                                                int32_t& my_page)
-{
-    const int lane = threadIdx.x;
-    const int32_t* bt = a.block_table + (int64_t)u.b * a.max_pages;
-    const bool in_unit = u.p0 + lane < u.p1;
-    my_page = in_unit ? bt[u.p0 + lane] : 0;
+    t.seq_len = L;
+    t.npages = L > 0 ? (L + kPageSize - 1) / kPageSize : 0;
+    t.nsplit = (t.npages + a.split_pages - 1) / a.split_pages;
+    const int p1 = min(t.p0 + a.split_pages, t.npages);
+    if (t.p0 >= p1)
+        return false;
+    t.count = max(0, (p1 - t.p0 - t.wave + kUnitWaves - 1) / kUnitWaves);
     if (CHECKED) {
-        const bool bad = in_unit && (my_page < 0 || (int64_t)my_page >= a.num_pages);
+        const bool bad = t.lane < t.count && (my_page < 0 || (int64_t)my_page >= a.num_pages);
         if (__any(bad)) {
-            if (lane == 0)
+            if (t.lane == 0)
                 atomicOr(a.dev_error, RL_DA_DEVERR_PAGE_OUT_OF_RANGE);
-            return false;
+            t.count = 0;  // read nothing; the unit's output is unspecified
         }
     }
     return true;
+}
+
+// An empty sequence produces zeros (written once, by the first unit).
+template <int G>
+__device__ __forceinline__ void write_zero_rows(const SplitArgs& a, const WaveTask& t)
+{
+    if (t.npages != 0 || t.s != 0)
+        return;
+    for (int e = threadIdx.x; e < G * (kHeadDim / 8); e += kWave * kUnitWaves) {
+        const int g = e / (kHeadDim / 8), chunk = e % (kHeadDim / 8);
+        uint4* dst = reinterpret_cast<uint4*>(
+            a.out + ((int64_t)t.b * a.num_q_heads + t.kvh * G + g) * kHeadDim + chunk * 8);
+        *dst = make_uint4(0, 0, 0, 0);
+    }
 }
 
 __device__ __forceinline__ const uint8_t* slab_base(const uint8_t* pool, int64_t page,
@@ -211,64 +230,108 @@ __device__ __forceinline__ const uint8_t* slab_base(const uint8_t* pool, int64_t
     return pool + (page * num_kv_heads + kvh) * (int64_t)slab_bytes;
 }
 
-// Writes the unit's result for query head g of the group: the final bf16 row
-// when the sequence has one split, else the (m, l, acc) partial.
-__device__ __forceinline__ void store_unit_row(const SplitArgs& a, const UnitCoords& u, int h,
-                                               int chunk, const float (&acc)[8], float m,
-                                               float l)
+// Global page index of a wavefront's i-th page.
+__device__ __forceinline__ int task_page(const WaveTask& t, int i)
 {
-    const int64_t row = (int64_t)u.b * a.num_q_heads + h;
-    if (u.nsplit == 1) {
-        const float inv = 1.0f / l;
-        uint4 o;
-        o.x = f32_to_bf16(acc[0] * inv) | (f32_to_bf16(acc[1] * inv) << 16);
-        o.y = f32_to_bf16(acc[2] * inv) | (f32_to_bf16(acc[3] * inv) << 16);
-        o.z = f32_to_bf16(acc[4] * inv) | (f32_to_bf16(acc[5] * inv) << 16);
-        o.w = f32_to_bf16(acc[6] * inv) | (f32_to_bf16(acc[7] * inv) << 16);
-        *reinterpret_cast<uint4*>(a.out + row * kHeadDim + chunk * 8) = o;
-        return;
-    }
-    const int64_t part = row * a.num_splits + u.s;
-    float4* dst = reinterpret_cast<float4*>(a.ws_acc + part * kHeadDim + chunk * 8);
-    dst[0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
-    dst[1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
-    if (chunk == 0)
-        *reinterpret_cast<float2*>(a.ws_ml + part * 2) = make_float2(m, l);
+    return t.p0 + t.wave + kUnitWaves * i;
 }
 
-// Streams a unit's pages through two register buffers (A and B): while one
-// page is consumed from one buffer the next is in flight into the other, and
-// the load two pages ahead is issued as soon as a buffer has been consumed.
-// The steady-state loop issues unconditionally, so the compiler's wait before
-// each consume only covers the buffer being consumed.
+// LDS holding each wavefront's final state for the unit merge.
+template <int G>
+struct UnitShared {
+    float acc[kUnitWaves][G][kHeadDim];
+    float m[kUnitWaves][G];
+    float l[kUnitWaves][G];
+};
+
+// Stores one wavefront's state for query head g: 8 dims of acc from lane
+// chunk c, and (m, l) from chunk 0.
+template <int G>
+__device__ __forceinline__ void stash_state(UnitShared<G>& sh, int wave, int g, int c,
+                                            const float (&acc)[8], float m, float l)
+{
+    float4* dst = reinterpret_cast<float4*>(&sh.acc[wave][g][c * 8]);
+    dst[0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
+    dst[1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
+    if (c == 0) {
+        sh.m[wave][g] = m;
+        sh.l[wave][g] = l;
+    }
+}
+
+// After every wavefront has stashed its state: merges the four states of each
+// query head in wavefront order (M = max m_w, weights 2^(m_w - M)) and writes
+// the bf16 output row, or the unit's (M, l, acc) partial when the sequence has
+// more than one split.  Wavefront w merges heads w, w+4, ...; two dims per lane.
+template <int G>
+__device__ __forceinline__ void merge_unit(const SplitArgs& a, const WaveTask& t,
+                                           const UnitShared<G>& sh)
+{
+    for (int g = t.wave; g < G; g += kUnitWaves) {
+        float M = -INFINITY;
+#pragma unroll
+        for (int w = 0; w < kUnitWaves; ++w)
+            M = fmaxf(M, sh.m[w][g]);  // finite: the unit holds at least one token
+        float den = 0.0f, n0 = 0.0f, n1 = 0.0f;
+#pragma unroll
+        for (int w = 0; w < kUnitWaves; ++w) {
+            const float wt = exp2_fast(sh.m[w][g] - M);  // 0 for a wavefront with no page
+            den = fmaf(wt, sh.l[w][g], den);
+            const float2 v = *reinterpret_cast<const float2*>(&sh.acc[w][g][2 * t.lane]);
+            n0 = fmaf(wt, v.x, n0);
+            n1 = fmaf(wt, v.y, n1);
+        }
+        const int64_t row = (int64_t)t.b * a.num_q_heads + t.kvh * G + g;
+        if (t.nsplit == 1) {
+            const float inv = 1.0f / den;
+            *reinterpret_cast<uint32_t*>(a.out + row * kHeadDim + 2 * t.lane) =
+                f32_to_bf16(n0 * inv) | (f32_to_bf16(n1 * inv) << 16);
+        } else {
+            const int64_t part = row * a.num_splits + t.s;
+            *reinterpret_cast<float2*>(a.ws_acc + part * kHeadDim + 2 * t.lane) =
+                make_float2(n0, n1);
+            if (t.lane == 0)
+                *reinterpret_cast<float2*>(a.ws_ml + part * 2) = make_float2(M, den);
+        }
+    }
+}
+
+// Streams a wavefront's pages through two register buffers (A and B): while
+// one page is consumed from one buffer the next is in flight into the other,
+// and the load two pages ahead is issued as soon as a buffer has been
+// consumed.  The steady-state loop issues unconditionally, so the compiler's
+// wait before each consume only covers the buffer being consumed.  issue and
+// consume take the wavefront-local page index.
 template <typename Issue, typename Consume>
-__device__ __forceinline__ void stream_pages(int p0, int p1, uint4 (&ka)[4], uint4 (&va)[4],
+__device__ __forceinline__ void stream_pages(int n, uint4 (&ka)[4], uint4 (&va)[4],
                                              uint4 (&kb)[4], uint4 (&vb)[4], Issue issue,
                                              Consume consume)
 {
-    int j = p0;
-    if (p1 - p0 >= 4) {
-        issue(ka, va, j);
-        issue(kb, vb, j + 1);
-        for (; j + 3 < p1; j += 2) {
-            consume(ka, va, j);
-            issue(ka, va, j + 2);
-            consume(kb, vb, j + 1);
-            issue(kb, vb, j + 3);
+    if (n <= 0)
+        return;
+    int i = 0;
+    if (n >= 4) {
+        issue(ka, va, 0);
+        issue(kb, vb, 1);
+        for (; i + 3 < n; i += 2) {
+            consume(ka, va, i);
+            issue(ka, va, i + 2);
+            consume(kb, vb, i + 1);
+            issue(kb, vb, i + 3);
         }
     } else {
-        issue(ka, va, j);
-        if (p1 - p0 >= 2)
-            issue(kb, vb, j + 1);
+        issue(ka, va, 0);
+        if (n >= 2)
+            issue(kb, vb, 1);
     }
-    const int rest = p1 - j;  // 1..3 pages left; pages j and j+1 already issued
-    consume(ka, va, j);
+    const int rest = n - i;  // 1..3 pages left; pages i and i+1 already issued
+    consume(ka, va, i);
     if (rest == 3)
-        issue(ka, va, j + 2);
+        issue(ka, va, i + 2);
     if (rest >= 2)
-        consume(kb, vb, j + 1);
+        consume(kb, vb, i + 1);
     if (rest == 3)
-        consume(ka, va, j + 2);
+        consume(ka, va, i + 2);
 }
 
 // ------------------------------------------------ split kernel, MFMA QK ---
@@ -280,28 +343,29 @@ __device__ __forceinline__ void stream_pages(int p0, int p1, uint4 (&ka)[4], uin
 // For the value pass lane l = 16r + c holds dims 8c..8c+7 of tokens 4i + r,
 // i = 0..3 (each 16-byte-per-lane load covers 1 KiB of the slab).  The
 // probabilities cross from the score layout to the value layout through 272
-// bytes of LDS.
+// bytes of LDS per wavefront.
 
 template <int G, bool CHECKED>
-__global__ __launch_bounds__(kWave) void split_mfma_bf16(SplitArgs a)
+__global__ __launch_bounds__(kWave * kUnitWaves) void split_mfma_bf16(SplitArgs a)
 {
     static_assert(G >= 1 && G <= 4, "MFMA score tile packs at most 4 query heads");
-    __shared__ __attribute__((aligned(16))) float lds_p[kPageSize * 4];  // [token][g]
-    __shared__ __attribute__((aligned(16))) float lds_alpha[4];
+    __shared__ __attribute__((aligned(16))) float lds_p_all[kUnitWaves][kPageSize * 4];
+    __shared__ __attribute__((aligned(16))) float lds_alpha_all[kUnitWaves][4];
+    __shared__ __attribute__((aligned(16))) UnitShared<G> sh;
 
-    UnitCoords u;
-    if (!unit_coords<CHECKED>(a, u)) {
-        write_zero_rows<G>(a, u);
+    WaveTask t;
+    int32_t my_page;
+    if (!begin_task<CHECKED>(a, t, my_page)) {
+        write_zero_rows<G>(a, t);
         return;
     }
-    int32_t my_page;
-    if (!load_unit_pages<CHECKED>(a, u, my_page))
-        return;
+    float* lds_p = lds_p_all[t.wave];          // [token][g]
+    float* lds_alpha = lds_alpha_all[t.wave];
 
-    const int lane = threadIdx.x;
+    const int lane = t.lane;
     const int n = lane & 15, kg = lane >> 4;  // score layout
     const int r = lane >> 4, c = lane & 15;   // value layout
-    const int h0 = u.kvh * G;
+    const int h0 = t.kvh * G;
 
     // Query tile: rows 4g hold query head g, every other row is zero.
     uint4 qa[4];
@@ -310,7 +374,7 @@ __global__ __launch_bounds__(kWave) void split_mfma_bf16(SplitArgs a)
         const int g = row >> 2;
         const bool has = (row & 3) == 0 && g < G;
         const uint16_t* qrow =
-            a.q + ((int64_t)u.b * a.num_q_heads + h0 + (has ? g : 0)) * kHeadDim;
+            a.q + ((int64_t)t.b * a.num_q_heads + h0 + (has ? g : 0)) * kHeadDim;
 #pragma unroll
         for (int i = 0; i < 4; ++i)
             qa[i] = has ? *reinterpret_cast<const uint4*>(qrow + 32 * i + 8 * kg)
@@ -329,28 +393,28 @@ __global__ __launch_bounds__(kWave) void split_mfma_bf16(SplitArgs a)
     const int koff = n * (kHeadDim * 2) + 16 * kg;  // byte offset in a K slab
     const int voff = lane * 16;                      // byte offset in a V slab
 
-    auto issue = [&](uint4 (&kbuf)[4], uint4 (&vbuf)[4], int j) {
-        const int64_t page = __builtin_amdgcn_readlane(my_page, j - u.p0);
-        const uint8_t* ks = slab_base(a.k_pool, page, a.num_kv_heads, u.kvh, kSlabBytesBf16);
-        const uint8_t* vs = slab_base(a.v_pool, page, a.num_kv_heads, u.kvh, kSlabBytesBf16);
+    auto issue = [&](uint4 (&kbuf)[4], uint4 (&vbuf)[4], int i) {
+        const int64_t page = __builtin_amdgcn_readlane(my_page, i);
+        const uint8_t* ks = slab_base(a.k_pool, page, a.num_kv_heads, t.kvh, kSlabBytesBf16);
+        const uint8_t* vs = slab_base(a.v_pool, page, a.num_kv_heads, t.kvh, kSlabBytesBf16);
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-            kbuf[i] = *reinterpret_cast<const uint4*>(ks + koff + 64 * i);
+        for (int k = 0; k < 4; ++k)
+            kbuf[k] = load_stream16(ks + koff + 64 * k);
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-            vbuf[i] = *reinterpret_cast<const uint4*>(vs + voff + 1024 * i);
+        for (int k = 0; k < 4; ++k)
+            vbuf[k] = load_stream16(vs + voff + 1024 * k);
     };
 
-    auto consume = [&](uint4 (&kbuf)[4], uint4 (&vbuf)[4], int j) {
-        // Scores of the 16 tokens of page j for the G query heads.
+    auto consume = [&](uint4 (&kbuf)[4], uint4 (&vbuf)[4], int i) {
+        // Scores of the 16 tokens of the page for the G query heads.
         floatx4_t sacc = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int k = 0; k < 4; ++k)
             sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                __builtin_bit_cast(bf16x8_t, qa[i]), __builtin_bit_cast(bf16x8_t, kbuf[i]),
+                __builtin_bit_cast(bf16x8_t, qa[k]), __builtin_bit_cast(bf16x8_t, kbuf[k]),
                 sacc, 0, 0, 0);
 
-        const int valid = u.seq_len - j * kPageSize;  // >= 1 tokens valid in page j
+        const int valid = t.seq_len - task_page(t, i) * kPageSize;  // >= 1 valid tokens
         float s = sacc[0] * a.scale_log2;
         s = (n < valid) ? s : -INFINITY;
         const float m_new = fmaxf(m, row16_max(s));  // finite: token 0 is valid
@@ -366,8 +430,8 @@ __global__ __launch_bounds__(kWave) void split_mfma_bf16(SplitArgs a)
         const float4 al = *reinterpret_cast<const float4*>(lds_alpha);
         float4 pv[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-            pv[i] = *reinterpret_cast<const float4*>(&lds_p[(4 * i + r) * 4]);
+        for (int k = 0; k < 4; ++k)
+            pv[k] = *reinterpret_cast<const float4*>(&lds_p[(4 * k + r) * 4]);
         wave_lds_sync();
 
         const float alv[4] = {al.x, al.y, al.z, al.w};
@@ -379,15 +443,15 @@ __global__ __launch_bounds__(kWave) void split_mfma_bf16(SplitArgs a)
 
         if (valid < kPageSize) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-                if (4 * i + r >= valid)
-                    vbuf[i] = make_uint4(0, 0, 0, 0);  // unread slots may hold NaN
+            for (int k = 0; k < 4; ++k)
+                if (4 * k + r >= valid)
+                    vbuf[k] = make_uint4(0, 0, 0, 0);  // unread slots may hold NaN
         }
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
+        for (int k = 0; k < 4; ++k) {
             float v[8];
-            unpack8(vbuf[i], v);
-            const float pg[4] = {pv[i].x, pv[i].y, pv[i].z, pv[i].w};
+            unpack8(vbuf[k], v);
+            const float pg[4] = {pv[k].x, pv[k].y, pv[k].z, pv[k].w};
 #pragma unroll
             for (int g = 0; g < G; ++g)
 #pragma unroll
@@ -397,7 +461,7 @@ __global__ __launch_bounds__(kWave) void split_mfma_bf16(SplitArgs a)
     };
 
     uint4 ka[4], va[4], kb[4], vb[4];
-    stream_pages(u.p0, u.p1, ka, va, kb, vb, issue, consume);
+    stream_pages(t.count, ka, va, kb, vb, issue, consume);
 
     // Every lane of a value row holds a partial over tokens = r (mod 4); all
     // rows share the running max, so the partials simply add.
@@ -415,7 +479,9 @@ __global__ __launch_bounds__(kWave) void split_mfma_bf16(SplitArgs a)
 #pragma unroll
     for (int g = 0; g < G; ++g)
         if (r == g)
-            store_unit_row(a, u, h0 + g, c, acc[g], m, l_row);
+            stash_state<G>(sh, t.wave, g, c, acc[g], m, l_row);
+    __syncthreads();
+    merge_unit<G>(a, t, sh);
 }
 
 // ------------------------------------------- split kernel, VALU dot2 QK ---
@@ -426,26 +492,26 @@ __global__ __launch_bounds__(kWave) void split_mfma_bf16(SplitArgs a)
 // tokens and the four rows are merged with the log-sum-exp rule at the end.
 
 template <int G, bool CHECKED>
-__global__ __launch_bounds__(kWave) void split_valu_bf16(SplitArgs a)
+__global__ __launch_bounds__(kWave * kUnitWaves) void split_valu_bf16(SplitArgs a)
 {
-    UnitCoords u;
-    if (!unit_coords<CHECKED>(a, u)) {
-        write_zero_rows<G>(a, u);
+    __shared__ __attribute__((aligned(16))) UnitShared<G> sh;
+
+    WaveTask t;
+    int32_t my_page;
+    if (!begin_task<CHECKED>(a, t, my_page)) {
+        write_zero_rows<G>(a, t);
         return;
     }
-    int32_t my_page;
-    if (!load_unit_pages<CHECKED>(a, u, my_page))
-        return;
 
-    const int lane = threadIdx.x;
+    const int lane = t.lane;
     const int r = lane >> 4, c = lane & 15;
-    const int h0 = u.kvh * G;
+    const int h0 = t.kvh * G;
 
     uint4 qv[G];
 #pragma unroll
     for (int g = 0; g < G; ++g)
         qv[g] = *reinterpret_cast<const uint4*>(
-            a.q + ((int64_t)u.b * a.num_q_heads + h0 + g) * kHeadDim + 8 * c);
+            a.q + ((int64_t)t.b * a.num_q_heads + h0 + g) * kHeadDim + 8 * c);
 
     float m[G], l[G], acc[G][8];
 #pragma unroll
@@ -458,31 +524,31 @@ __global__ __launch_bounds__(kWave) void split_valu_bf16(SplitArgs a)
     }
 
     const int off = lane * 16;
-    auto issue = [&](uint4 (&kbuf)[4], uint4 (&vbuf)[4], int j) {
-        const int64_t page = __builtin_amdgcn_readlane(my_page, j - u.p0);
-        const uint8_t* ks = slab_base(a.k_pool, page, a.num_kv_heads, u.kvh, kSlabBytesBf16);
-        const uint8_t* vs = slab_base(a.v_pool, page, a.num_kv_heads, u.kvh, kSlabBytesBf16);
+    auto issue = [&](uint4 (&kbuf)[4], uint4 (&vbuf)[4], int i) {
+        const int64_t page = __builtin_amdgcn_readlane(my_page, i);
+        const uint8_t* ks = slab_base(a.k_pool, page, a.num_kv_heads, t.kvh, kSlabBytesBf16);
+        const uint8_t* vs = slab_base(a.v_pool, page, a.num_kv_heads, t.kvh, kSlabBytesBf16);
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-            kbuf[i] = *reinterpret_cast<const uint4*>(ks + off + 1024 * i);
+        for (int k = 0; k < 4; ++k)
+            kbuf[k] = load_stream16(ks + off + 1024 * k);
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-            vbuf[i] = *reinterpret_cast<const uint4*>(vs + off + 1024 * i);
+        for (int k = 0; k < 4; ++k)
+            vbuf[k] = load_stream16(vs + off + 1024 * k);
     };
 
-    auto consume = [&](uint4 (&kbuf)[4], uint4 (&vbuf)[4], int j) {
-        const int valid = u.seq_len - j * kPageSize;
+    auto consume = [&](uint4 (&kbuf)[4], uint4 (&vbuf)[4], int i) {
+        const int valid = t.seq_len - task_page(t, i) * kPageSize;
         float sc[G][4];
 #pragma unroll
         for (int g = 0; g < G; ++g)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                float t = dot2_bf16(qv[g].x, kbuf[i].x, 0.0f);
-                t = dot2_bf16(qv[g].y, kbuf[i].y, t);
-                t = dot2_bf16(qv[g].z, kbuf[i].z, t);
-                t = dot2_bf16(qv[g].w, kbuf[i].w, t);
-                t = row16_sum(t) * a.scale_log2;
-                sc[g][i] = (4 * i + r < valid) ? t : -INFINITY;
+            for (int k = 0; k < 4; ++k) {
+                float x = dot2_bf16(qv[g].x, kbuf[k].x, 0.0f);
+                x = dot2_bf16(qv[g].y, kbuf[k].y, x);
+                x = dot2_bf16(qv[g].z, kbuf[k].z, x);
+                x = dot2_bf16(qv[g].w, kbuf[k].w, x);
+                x = row16_sum(x) * a.scale_log2;
+                sc[g][k] = (4 * k + r < valid) ? x : -INFINITY;
             }
 
         float p[G][4];
@@ -495,9 +561,9 @@ __global__ __launch_bounds__(kWave) void split_valu_bf16(SplitArgs a)
             const float alpha = empty ? 1.0f : exp2_fast(m[g] - m_new);
             float sum = 0.0f;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                p[g][i] = empty ? 0.0f : exp2_fast(sc[g][i] - m_new);
-                sum += p[g][i];
+            for (int k = 0; k < 4; ++k) {
+                p[g][k] = empty ? 0.0f : exp2_fast(sc[g][k] - m_new);
+                sum += p[g][k];
             }
             l[g] = l[g] * alpha + sum;
             m[g] = m_new;
@@ -508,30 +574,31 @@ __global__ __launch_bounds__(kWave) void split_valu_bf16(SplitArgs a)
 
         if (valid < kPageSize) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-                if (4 * i + r >= valid)
-                    vbuf[i] = make_uint4(0, 0, 0, 0);
+            for (int k = 0; k < 4; ++k)
+                if (4 * k + r >= valid)
+                    vbuf[k] = make_uint4(0, 0, 0, 0);
         }
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
+        for (int k = 0; k < 4; ++k) {
             float v[8];
-            unpack8(vbuf[i], v);
+            unpack8(vbuf[k], v);
 #pragma unroll
             for (int g = 0; g < G; ++g)
 #pragma unroll
                 for (int d = 0; d < 8; ++d)
-                    acc[g][d] = fmaf(p[g][i], v[d], acc[g][d]);
+                    acc[g][d] = fmaf(p[g][k], v[d], acc[g][d]);
         }
     };
 
     uint4 ka[4], va[4], kb[4], vb[4];
-    stream_pages(u.p0, u.p1, ka, va, kb, vb, issue, consume);
+    stream_pages(t.count, ka, va, kb, vb, issue, consume);
 
-    // Merge the four rows: rescale each to the common max, then add.
+    // Merge the four rows: rescale each to the common max, then add.  A
+    // wavefront without pages keeps m = -inf, l = 0, acc = 0.
 #pragma unroll
     for (int g = 0; g < G; ++g) {
         float M = fmaxf(m[g], __shfl_xor(m[g], 16));
-        M = fmaxf(M, __shfl_xor(M, 32));  // finite: row 0 holds token 0 of page p0
+        M = fmaxf(M, __shfl_xor(M, 32));
         const float w = (m[g] == -INFINITY) ? 0.0f : exp2_fast(m[g] - M);
         float lw = l[g] * w;
         lw += __shfl_xor(lw, 16);
@@ -549,13 +616,19 @@ __global__ __launch_bounds__(kWave) void split_valu_bf16(SplitArgs a)
 #pragma unroll
     for (int g = 0; g < G; ++g)
         if ((g & 3) == r)
-            store_unit_row(a, u, h0 + g, c, acc[g], m[g], l[g]);
+            stash_state<G>(sh, t.wave, g, c, acc[g], m[g], l[g]);
+    __syncthreads();
+    merge_unit<G>(a, t, sh);
 }
 
 // -------------------------------------------------------- merge kernel ---
 //
-// One wavefront per (b, h): M = max_s m_s, w_s = 2^(m_s - M),
-// out = sum_s w_s acc_s / sum_s w_s l_s, summed in split order.
+// One work-group of four wavefronts per (b, h) of sequences with more than one
+// split: M = max_s m_s, then wavefront w sums w_s l_s and w_s acc_s
+// (w_s = 2^(m_s - M)) over splits s = w, w+4, ... (two dims per lane), and the
+// four partial sums are added in wavefront order.
+
+constexpr int kMergeWaves = 4;
 
 struct MergeArgs {
     const int32_t* seq_lens;
@@ -568,32 +641,50 @@ struct MergeArgs {
     int32_t num_splits;
 };
 
-__global__ __launch_bounds__(kWave) void merge_splits(MergeArgs a)
+__global__ __launch_bounds__(kWave * kMergeWaves) void merge_splits(MergeArgs a)
 {
+    __shared__ float part[kMergeWaves][kHeadDim + 1];
     const int64_t row = blockIdx.x;  // b * Hq + h
     const int b = (int)(row / a.num_q_heads);
     const int L = min(a.seq_lens[b], a.max_pages * kPageSize);
     const int npages = L > 0 ? (L + kPageSize - 1) / kPageSize : 0;
     const int n = (npages + a.split_pages - 1) / a.split_pages;
-    if (n <= 1)
+    if (n < 2)
         return;  // finished by the split kernel
-    const int lane = threadIdx.x;
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const float* ml = a.ws_ml + row * a.num_splits * 2;
     float M = -INFINITY;
-    for (int s = 0; s < n; ++s)
+    for (int s = lane; s < n; s += kWave)
         M = fmaxf(M, ml[2 * s]);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1)
+        M = fmaxf(M, __shfl_xor(M, off));
     float den = 0.0f, num0 = 0.0f, num1 = 0.0f;
     const float* acc = a.ws_acc + row * a.num_splits * kHeadDim + 2 * lane;
-    for (int s = 0; s < n; ++s) {
+    for (int s = wave; s < n; s += kMergeWaves) {
         const float w = exp2_fast(ml[2 * s] - M);
         den = fmaf(w, ml[2 * s + 1], den);
         const float2 v = *reinterpret_cast<const float2*>(acc + (int64_t)s * kHeadDim);
         num0 = fmaf(w, v.x, num0);
         num1 = fmaf(w, v.y, num1);
     }
-    const float inv = 1.0f / den;
+    part[wave][2 * lane] = num0;
+    part[wave][2 * lane + 1] = num1;
+    if (lane == 0)
+        part[wave][kHeadDim] = den;
+    __syncthreads();
+    if (wave != 0)
+        return;
+    float d = 0.0f, x0 = 0.0f, x1 = 0.0f;
+#pragma unroll
+    for (int w = 0; w < kMergeWaves; ++w) {
+        d += part[w][kHeadDim];
+        x0 += part[w][2 * lane];
+        x1 += part[w][2 * lane + 1];
+    }
+    const float inv = 1.0f / d;
     *reinterpret_cast<uint32_t*>(a.out + row * kHeadDim + 2 * lane) =
-        f32_to_bf16(num0 * inv) | (f32_to_bf16(num1 * inv) << 16);
+        f32_to_bf16(x0 * inv) | (f32_to_bf16(x1 * inv) << 16);
 }
 
 // ------------------------------------------------------------ dispatch ---
@@ -675,13 +766,19 @@ rl_da_status check_config(const rl_da_config* cfg, int* split_tokens, int* split
     return RL_DA_OK;
 }
 
-size_t workspace_bytes_for(const rl_da_config* cfg, int max_splits)
+// Workspace: per-split partial accumulators and (m, l) pairs, then one
+// 256-byte block for the device error word.
+size_t partials_bytes(const rl_da_config* cfg, int max_splits)
 {
     const size_t rows = (size_t)cfg->max_batch * (size_t)cfg->num_q_heads * (size_t)max_splits;
     size_t bytes = rows * kHeadDim * sizeof(float);      // acc
     bytes += rows * 2 * sizeof(float);                    // (m, l)
-    bytes = (bytes + 255) & ~(size_t)255;
-    return bytes + 256;                                   // device error word
+    return (bytes + 255) & ~(size_t)255;
+}
+
+size_t workspace_bytes_for(const rl_da_config* cfg, int max_splits)
+{
+    return partials_bytes(cfg, max_splits) + 256;
 }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
@@ -831,7 +928,8 @@ rl_da_status rl_decode_attn_run(rl_decode_attn* h, const void* q, const void* k_
     hipStream_t st = (hipStream_t)stream;
     if (h->ev_split_begin != nullptr && hipEventRecord(h->ev_split_begin, st) != hipSuccess)
         return RL_DA_ERR_HIP;
-    hipLaunchKernelGGL(h->split_kernel, dim3((unsigned)units), dim3(kWave), 0, st, sa);
+    hipLaunchKernelGGL(h->split_kernel, dim3((unsigned)units), dim3(kWave * kUnitWaves), 0, st,
+                       sa);
     if (hipGetLastError() != hipSuccess)
         return RL_DA_ERR_HIP;
     if (h->ev_split_end != nullptr && hipEventRecord(h->ev_split_end, st) != hipSuccess)
@@ -847,7 +945,7 @@ rl_da_status rl_decode_attn_run(rl_decode_attn* h, const void* q, const void* k_
         ma.split_pages = h->split_pages;
         ma.num_splits = num_splits;
         hipLaunchKernelGGL(merge_splits, dim3((unsigned)((int64_t)batch * cfg.num_q_heads)),
-                           dim3(kWave), 0, st, ma);
+                           dim3(kWave * kMergeWaves), 0, st, ma);
         if (hipGetLastError() != hipSuccess)
             return RL_DA_ERR_HIP;
     }

@@ -58,12 +58,12 @@ def cfg(**kw):
 def test_workspace_size_formula():
     rc, n = B.rl_decode_attn_workspace_size(cfg())
     assert rc == B.RL_DA_OK
-    splits = 256 // 32                       # 512-token splits of 16-token pages
+    splits = 256 // 256                      # default 4096-token splits of 16-token pages
     rows = 64 * 32 * splits
     expect = (rows * 128 * 4 + rows * 2 * 4 + 255) // 256 * 256 + 256
     assert n == expect
-    rc, n2 = B.rl_decode_attn_workspace_size(cfg(split_tokens=1024))
-    assert rc == B.RL_DA_OK and n2 < n
+    rc, n2 = B.rl_decode_attn_workspace_size(cfg(split_tokens=512))
+    assert rc == B.RL_DA_OK and n2 > n
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -80,7 +80,7 @@ def test_workspace_size_formula():
     (dict(num_q_heads=24, num_kv_heads=8), B.RL_DA_ERR_UNSUPPORTED),   # G = 3
     (dict(num_q_heads=128, num_kv_heads=8), B.RL_DA_ERR_UNSUPPORTED),  # G = 16
     (dict(split_tokens=24), B.RL_DA_ERR_UNSUPPORTED),
-    (dict(split_tokens=2048), B.RL_DA_ERR_UNSUPPORTED),
+    (dict(split_tokens=4112), B.RL_DA_ERR_UNSUPPORTED),
 ])
 def test_create_rejects_bad_config_without_gpu(kw, status):
     c = cfg(**kw)
