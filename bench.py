@@ -49,7 +49,7 @@ def read_ceilings(p, split_pages, stream):
     nbytes = 4 << 30
     buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
     best_stream = 0.0
-    for grid in (2048, 4096, 8192):
+    for grid in (1024, 2048, 8192):
         sink = torch.empty(grid * 256, dtype=torch.int32, device="cuda")
         for it in range(6):
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -61,7 +61,7 @@ def read_ceilings(p, split_pages, stream):
                 best_stream = max(best_stream, nbytes / (e0.elapsed_time(e1) / 1e3) / 1e9)
     del buf
     units = p.batch * p.num_kv_heads * ((p.max_pages + split_pages - 1) // split_pages)
-    sink = torch.empty(units * 64, dtype=torch.int32, device="cuda")
+    sink = torch.empty(units * 256, dtype=torch.int32, device="cuda")
     best_page = 0.0
     kv = p.kv_bytes()
     if p.kv_dtype == "bf16":

@@ -4,11 +4,12 @@
 //   rl_bench_copy         plain 16-byte-per-lane copy of a known byte count; its
 //                         FETCH_SIZE / WRITE_SIZE readings calibrate the HBM
 //                         traffic counters.
-//   rl_bench_stream_read  contiguous read of a buffer: the achievable HBM read
-//                         bandwidth on this GPU.
+//   rl_bench_stream_read  contiguous read of a buffer, one contiguous share per
+//                         work-group: the achievable HBM read bandwidth.
 //   rl_bench_page_read    reads exactly the K/V bytes one decode step reads, in
-//                         the same (sequence, kv head, split) work units and
-//                         the same per-lane load pattern as the split-K
+//                         the same work units (four wavefronts per (sequence,
+//                         kv head, split), pages taken in turn) and the same
+//                         per-lane non-temporal load pattern as the split-K
 //                         attention kernel, with no arithmetic: the ceiling of
 //                         that access pattern.
 //
@@ -22,6 +23,15 @@
 namespace {
 
 constexpr int kBlock = 256;
+constexpr int kUnitWaves = 4;
+
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint4 load_stream16(const uint8_t* p)
+{
+    const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
 
 __global__ __launch_bounds__(kBlock) void copy_kernel(uint4* __restrict__ dst,
                                                       const uint4* __restrict__ src, size_t n)
@@ -31,20 +41,28 @@ __global__ __launch_bounds__(kBlock) void copy_kernel(uint4* __restrict__ dst,
         dst[i] = src[i];
 }
 
+// Each work-group reads its own contiguous share of the buffer with
+// non-temporal 16-byte loads, four in flight per lane (the fastest read
+// pattern measured on this GPU).
 __global__ __launch_bounds__(kBlock) void stream_read_kernel(const uint4* __restrict__ src,
                                                              size_t n, uint32_t* sink)
 {
-    const size_t stride = (size_t)gridDim.x * kBlock;
+    const size_t per = (n + gridDim.x - 1) / gridDim.x;
+    const size_t b0 = (size_t)blockIdx.x * per;
+    const size_t b1 = b0 + per < n ? b0 + per : n;
+    const uint8_t* base = reinterpret_cast<const uint8_t*>(src);
     uint32_t acc = 0;
-    size_t i = (size_t)blockIdx.x * kBlock + threadIdx.x;
-    for (; i + 3 * stride < n; i += 4 * stride) {
-        const uint4 a = src[i], b = src[i + stride], c = src[i + 2 * stride],
-                    d = src[i + 3 * stride];
+    size_t i = b0 + threadIdx.x;
+    for (; i + 3 * kBlock < b1; i += 4 * kBlock) {
+        const uint4 a = load_stream16(base + 16 * i);
+        const uint4 b = load_stream16(base + 16 * (i + kBlock));
+        const uint4 c = load_stream16(base + 16 * (i + 2 * kBlock));
+        const uint4 d = load_stream16(base + 16 * (i + 3 * kBlock));
         acc ^= a.x ^ a.y ^ a.z ^ a.w ^ b.x ^ b.y ^ b.z ^ b.w ^ c.x ^ c.y ^ c.z ^ c.w ^ d.x ^
                d.y ^ d.z ^ d.w;
     }
-    for (; i < n; i += stride) {
-        const uint4 a = src[i];
+    for (; i < b1; i += kBlock) {
+        const uint4 a = load_stream16(base + 16 * i);
         acc ^= a.x ^ a.y ^ a.z ^ a.w;
     }
     // one value per thread keeps every load live; the sink holds grid*block words
@@ -63,14 +81,14 @@ struct PageReadArgs {
     int32_t num_splits;
 };
 
-__global__ __launch_bounds__(64) void page_read_kernel(PageReadArgs a)
+__global__ __launch_bounds__(64 * kUnitWaves) void page_read_kernel(PageReadArgs a)
 {
     const int unit = blockIdx.x;
     const int s = unit % a.num_splits;
     const int bk = unit / a.num_splits;
     const int kvh = bk % a.num_kv_heads;
     const int b = bk / a.num_kv_heads;
-    const int lane = threadIdx.x;
+    const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
     const int L = min(a.seq_lens[b], a.max_pages * 16);
     const int npages = L > 0 ? (L + 15) / 16 : 0;
     const int p0 = s * a.split_pages;
@@ -78,20 +96,20 @@ __global__ __launch_bounds__(64) void page_read_kernel(PageReadArgs a)
     uint32_t acc = 0;
     const int koff = (lane & 15) * 256 + 16 * (lane >> 4);
     const int voff = lane * 16;
-    for (int j = p0; j < p1; ++j) {
+    for (int j = p0 + wave; j < p1; j += kUnitWaves) {
         const int64_t page = a.block_table[(int64_t)b * a.max_pages + j];
         const int64_t slab = (page * a.num_kv_heads + kvh) * 4096;
         uint4 k[4], v[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            k[i] = *reinterpret_cast<const uint4*>(a.k_pool + slab + koff + 64 * i);
-            v[i] = *reinterpret_cast<const uint4*>(a.v_pool + slab + voff + 1024 * i);
+            k[i] = load_stream16(a.k_pool + slab + koff + 64 * i);
+            v[i] = load_stream16(a.v_pool + slab + voff + 1024 * i);
         }
 #pragma unroll
         for (int i = 0; i < 4; ++i)
             acc ^= k[i].x ^ k[i].y ^ k[i].z ^ k[i].w ^ v[i].x ^ v[i].y ^ v[i].z ^ v[i].w;
     }
-    a.sink[(size_t)unit * 64 + lane] = acc;
+    a.sink[(size_t)unit * 64 * kUnitWaves + threadIdx.x] = acc;
 }
 
 }  // namespace
@@ -120,7 +138,7 @@ int rl_bench_stream_read(const void* src, size_t bytes, uint32_t* sink, int grid
     return (int)hipGetLastError();
 }
 
-// bf16 pools [P][Hkv][16][128]; sink must hold batch*num_kv_heads*num_splits*64 words.
+// bf16 pools [P][Hkv][16][128]; sink must hold batch*num_kv_heads*num_splits*256 words.
 int rl_bench_page_read(const void* k_pool, const void* v_pool, const int32_t* block_table,
                        int32_t max_pages, const int32_t* seq_lens, int32_t batch,
                        int32_t num_kv_heads, int32_t split_pages, uint32_t* sink, void* stream)
@@ -140,7 +158,7 @@ int rl_bench_page_read(const void* k_pool, const void* v_pool, const int32_t* bl
     a.split_pages = split_pages;
     a.num_splits = (max_pages + split_pages - 1) / split_pages;
     const int64_t units = (int64_t)batch * num_kv_heads * a.num_splits;
-    hipLaunchKernelGGL(page_read_kernel, dim3((unsigned)units), dim3(64), 0,
+    hipLaunchKernelGGL(page_read_kernel, dim3((unsigned)units), dim3(64 * kUnitWaves), 0,
                        (hipStream_t)stream, a);
     return (int)hipGetLastError();
 }
