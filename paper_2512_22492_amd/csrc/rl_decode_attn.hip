@@ -51,7 +51,9 @@ constexpr int kSlabBytesBf16 = kPageSize * kHeadDim * 2;
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float floatx4_t __attribute__((ext_vector_type(4)));
+typedef float floatx2_t __attribute__((ext_vector_type(2)));
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
 
 struct SplitArgs {
     const uint16_t* q;          // bf16 bits [B][Hq][D]
@@ -131,12 +133,18 @@ __device__ __forceinline__ float row16_max(float v)
 
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// 16-byte load with the non-temporal hint: K/V bytes are read exactly once, so
-// they are streamed past the caches rather than kept.
+// Loads with the non-temporal hint: K/V bytes are read exactly once, so they
+// are streamed past the caches rather than kept.
 __device__ __forceinline__ uint4 load_stream16(const uint8_t* p)
 {
     const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
     return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+__device__ __forceinline__ uint2 load_stream8(const uint8_t* p)
+{
+    const u32x2_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x2_t*>(p));
+    return make_uint2(v.x, v.y);
 }
 
 // Orders LDS traffic between the lanes of one wavefront (the work-group is
@@ -296,57 +304,142 @@ __device__ __forceinline__ void merge_unit(const SplitArgs& a, const WaveTask& t
     }
 }
 
-// Streams a wavefront's pages through two register buffers (A and B): while
-// one page is consumed from one buffer the next is in flight into the other,
-// and the load two pages ahead is issued as soon as a buffer has been
-// consumed.  The steady-state loop issues unconditionally, so the compiler's
-// wait before each consume only covers the buffer being consumed.  issue and
-// consume take the wavefront-local page index.
-template <typename Issue, typename Consume>
-__device__ __forceinline__ void stream_pages(int n, uint4 (&ka)[4], uint4 (&va)[4],
-                                             uint4 (&kb)[4], uint4 (&vb)[4], Issue issue,
-                                             Consume consume)
+// Streams a wavefront's pages through two buffers (A and B): while one page is
+// consumed from one buffer the next is in flight into the other, and the load
+// two pages ahead is issued as soon as a buffer has been consumed.  The
+// steady-state loop issues unconditionally, so the compiler's wait before each
+// consume only covers the buffer being consumed.  issue and consume take the
+// wavefront-local page index.
+template <typename Buf, typename Issue, typename Consume>
+__device__ __forceinline__ void stream_pages(int n, Buf& a, Buf& b, Issue issue, Consume consume)
 {
     if (n <= 0)
         return;
     int i = 0;
     if (n >= 4) {
-        issue(ka, va, 0);
-        issue(kb, vb, 1);
+        issue(a, 0);
+        issue(b, 1);
         for (; i + 3 < n; i += 2) {
-            consume(ka, va, i);
-            issue(ka, va, i + 2);
-            consume(kb, vb, i + 1);
-            issue(kb, vb, i + 3);
+            consume(a, i);
+            issue(a, i + 2);
+            consume(b, i + 1);
+            issue(b, i + 3);
         }
     } else {
-        issue(ka, va, 0);
+        issue(a, 0);
         if (n >= 2)
-            issue(kb, vb, 1);
+            issue(b, 1);
     }
     const int rest = n - i;  // 1..3 pages left; pages i and i+1 already issued
-    consume(ka, va, i);
+    consume(a, i);
     if (rest == 3)
-        issue(ka, va, i + 2);
+        issue(a, i + 2);
     if (rest >= 2)
-        consume(kb, vb, i + 1);
+        consume(b, i + 1);
     if (rest == 3)
-        consume(ka, va, i + 2);
+        consume(a, i + 2);
 }
+
+// ------------------------------------------------------ K/V page formats ---
+//
+// A wavefront consumes one (page, kv head) slab at a time.  For the score MFMA
+// (v_mfma_f32_16x16x32_bf16, A = queries 16x32, B = keys 32x16) lane l supplies
+// key token n = l%16 and 8 of the 32 dims of each of the four k-blocks; which
+// 8 dims is the format's choice (q_dim), as long as the query tile uses the
+// same ones.  For the value pass lane l = 16r + c holds dims 8c..8c+7 of
+// tokens 4k + r, k = 0..3.
+
+// bf16 slab: 4 KiB, four 16-byte loads per lane for K and for V.
+struct KvBf16 {
+    static constexpr int kSlabBytes = kPageSize * kHeadDim * 2;
+    static constexpr bool kScaled = false;
+    struct Buf {
+        uint4 k[4];
+        uint4 v[4];
+    };
+    // first dim of the 8 query dims lane group kg holds for k-block i
+    __device__ static int q_dim(int i, int kg) { return 32 * i + 8 * kg; }
+    __device__ static void load(Buf& b, const uint8_t* ks, const uint8_t* vs, int lane)
+    {
+        const int koff = (lane & 15) * (kHeadDim * 2) + 16 * (lane >> 4);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            b.k[i] = load_stream16(ks + koff + 64 * i);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            b.v[i] = load_stream16(vs + lane * 16 + 1024 * i);
+    }
+    __device__ static uint4 k_block(const Buf& b, int i) { return b.k[i]; }
+    __device__ static void values(const Buf& b, int k, float (&v)[8]) { unpack8(b.v[k], v); }
+    __device__ static void clear_values(Buf& b, int k) { b.v[k] = make_uint4(0, 0, 0, 0); }
+};
+
+// OCP e4m3 slab: 2 KiB.  K: two 16-byte loads per lane (dims 16kg..16kg+15 and
+// 64+16kg..64+16kg+15 of token l%16); each 8-code half converts exactly to
+// bf16 for one k-block.  V: four 8-byte loads per lane in the value layout,
+// converted to fp32.  The slab scales stay out of the conversions: k_scale
+// multiplies the score and v_scale the probability.
+struct KvFp8 {
+    static constexpr int kSlabBytes = kPageSize * kHeadDim;
+    static constexpr bool kScaled = true;
+    struct Buf {
+        uint4 k[2];
+        uint2 v[4];
+    };
+    __device__ static int q_dim(int i, int kg) { return (i >> 1) * 64 + 16 * kg + (i & 1) * 8; }
+    __device__ static void load(Buf& b, const uint8_t* ks, const uint8_t* vs, int lane)
+    {
+        const int koff = (lane & 15) * kHeadDim + 16 * (lane >> 4);
+        b.k[0] = load_stream16(ks + koff);
+        b.k[1] = load_stream16(ks + koff + 64);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            b.v[i] = load_stream8(vs + lane * 8 + 512 * i);
+    }
+    // Two e4m3 codes (bytes 2*HI, 2*HI+1 of x) as a bf16 pair; exact.
+    template <bool HI>
+    __device__ static uint32_t cvt2(uint32_t x)
+    {
+        return __builtin_bit_cast(uint32_t,
+                                  __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(x, 1.0f, HI));
+    }
+    __device__ static uint4 k_block(const Buf& b, int i)
+    {
+        const uint4& w = b.k[i >> 1];
+        const uint32_t lo = (i & 1) ? w.z : w.x;
+        const uint32_t hi = (i & 1) ? w.w : w.y;
+        return make_uint4(cvt2<false>(lo), cvt2<true>(lo), cvt2<false>(hi), cvt2<true>(hi));
+    }
+    __device__ static void values(const Buf& b, int k, float (&v)[8])
+    {
+        const floatx2_t a0 = __builtin_amdgcn_cvt_pk_f32_fp8(b.v[k].x, false);
+        const floatx2_t a1 = __builtin_amdgcn_cvt_pk_f32_fp8(b.v[k].x, true);
+        const floatx2_t a2 = __builtin_amdgcn_cvt_pk_f32_fp8(b.v[k].y, false);
+        const floatx2_t a3 = __builtin_amdgcn_cvt_pk_f32_fp8(b.v[k].y, true);
+        v[0] = a0.x; v[1] = a0.y; v[2] = a1.x; v[3] = a1.y;
+        v[4] = a2.x; v[5] = a2.y; v[6] = a3.x; v[7] = a3.y;
+    }
+    __device__ static void clear_values(Buf& b, int k) { b.v[k] = make_uint2(0, 0); }
+};
 
 // ------------------------------------------------ split kernel, MFMA QK ---
 //
-// Lane roles.  For the score MFMA (v_mfma_f32_16x16x32_bf16, A = queries
-// 16x32, B = keys 32x16), lane l holds key token n = l%16 and 8 dims of each
-// 32-dim block; query head g sits in tile row 4g, so after the four MFMAs of
-// a page lane l holds score (g = l/16, token l%16) in its first accumulator.
-// For the value pass lane l = 16r + c holds dims 8c..8c+7 of tokens 4i + r,
-// i = 0..3 (each 16-byte-per-lane load covers 1 KiB of the slab).  The
-// probabilities cross from the score layout to the value layout through 272
-// bytes of LDS per wavefront.
+// Query head g sits in row 4g of the 16-row query tile, so after the four
+// MFMAs of a page lane l holds score (g = l/16, token l%16) in its first
+// accumulator.  The probabilities cross from that layout to the value layout
+// through 272 bytes of LDS per wavefront.
+//
+// The running max m of each query head moves only when a page's max exceeds
+// it by more than kMaxSlack (log2 units); between moves the probabilities
+// 2^(s - m) may exceed 1 (by at most 2^kMaxSlack) and the accumulators need no
+// rescaling, so the rescale and its LDS exchange run only on the rare pages
+// where some head's max moves.  Results are the same up to fp32 rounding: m
+// cancels in acc / l.
 
-template <int G, bool CHECKED>
-__global__ __launch_bounds__(kWave * kUnitWaves) void split_mfma_bf16(SplitArgs a)
+constexpr float kMaxSlack = 8.0f;
+
+template <int G, bool CHECKED, typename KV>
+__global__ __launch_bounds__(kWave * kUnitWaves) void split_mfma(SplitArgs a)
 {
     static_assert(G >= 1 && G <= 4, "MFMA score tile packs at most 4 query heads");
     __shared__ __attribute__((aligned(16))) float lds_p_all[kUnitWaves][kPageSize * 4];
@@ -367,6 +460,14 @@ __global__ __launch_bounds__(kWave * kUnitWaves) void split_mfma_bf16(SplitArgs 
     const int r = lane >> 4, c = lane & 15;   // value layout
     const int h0 = t.kvh * G;
 
+    // Slab scales of this wavefront's pages, one per lane like the pages.
+    float my_kscale = 1.0f, my_vscale = 1.0f;
+    if (KV::kScaled && lane < t.count) {
+        const int64_t slab = (int64_t)my_page * a.num_kv_heads + t.kvh;
+        my_kscale = a.k_scale[slab];
+        my_vscale = a.v_scale[slab];
+    }
+
     // Query tile: rows 4g hold query head g, every other row is zero.
     uint4 qa[4];
     {
@@ -377,11 +478,11 @@ __global__ __launch_bounds__(kWave * kUnitWaves) void split_mfma_bf16(SplitArgs 
             a.q + ((int64_t)t.b * a.num_q_heads + h0 + (has ? g : 0)) * kHeadDim;
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-            qa[i] = has ? *reinterpret_cast<const uint4*>(qrow + 32 * i + 8 * kg)
+            qa[i] = has ? *reinterpret_cast<const uint4*>(qrow + KV::q_dim(i, kg))
                         : make_uint4(0, 0, 0, 0);
     }
 
-    float m = -INFINITY;      // running max of row g = lane/16 (log2 units)
+    float m = -INFINITY;      // reference max of row g = lane/16 (log2 units)
     float lsum = 0.0f;        // this lane's share of the running sum
     float acc[G][8];
 #pragma unroll
@@ -390,67 +491,70 @@ __global__ __launch_bounds__(kWave * kUnitWaves) void split_mfma_bf16(SplitArgs 
         for (int d = 0; d < 8; ++d)
             acc[g][d] = 0.0f;
 
-    const int koff = n * (kHeadDim * 2) + 16 * kg;  // byte offset in a K slab
-    const int voff = lane * 16;                      // byte offset in a V slab
-
-    auto issue = [&](uint4 (&kbuf)[4], uint4 (&vbuf)[4], int i) {
+    auto issue = [&](typename KV::Buf& buf, int i) {
         const int64_t page = __builtin_amdgcn_readlane(my_page, i);
-        const uint8_t* ks = slab_base(a.k_pool, page, a.num_kv_heads, t.kvh, kSlabBytesBf16);
-        const uint8_t* vs = slab_base(a.v_pool, page, a.num_kv_heads, t.kvh, kSlabBytesBf16);
-#pragma unroll
-        for (int k = 0; k < 4; ++k)
-            kbuf[k] = load_stream16(ks + koff + 64 * k);
-#pragma unroll
-        for (int k = 0; k < 4; ++k)
-            vbuf[k] = load_stream16(vs + voff + 1024 * k);
+        KV::load(buf, slab_base(a.k_pool, page, a.num_kv_heads, t.kvh, KV::kSlabBytes),
+                 slab_base(a.v_pool, page, a.num_kv_heads, t.kvh, KV::kSlabBytes), lane);
     };
 
-    auto consume = [&](uint4 (&kbuf)[4], uint4 (&vbuf)[4], int i) {
+    auto consume = [&](typename KV::Buf& buf, int i) {
         // Scores of the 16 tokens of the page for the G query heads.
         floatx4_t sacc = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
         for (int k = 0; k < 4; ++k)
             sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                __builtin_bit_cast(bf16x8_t, qa[k]), __builtin_bit_cast(bf16x8_t, kbuf[k]),
-                sacc, 0, 0, 0);
+                __builtin_bit_cast(bf16x8_t, qa[k]),
+                __builtin_bit_cast(bf16x8_t, KV::k_block(buf, k)), sacc, 0, 0, 0);
 
         const int valid = t.seq_len - task_page(t, i) * kPageSize;  // >= 1 valid tokens
-        float s = sacc[0] * a.scale_log2;
+        float sl = a.scale_log2;
+        if (KV::kScaled)
+            sl *= __int_as_float(__builtin_amdgcn_readlane(__float_as_int(my_kscale), i));
+        float s = sacc[0] * sl;
         s = (n < valid) ? s : -INFINITY;
-        const float m_new = fmaxf(m, row16_max(s));  // finite: token 0 is valid
-        const float alpha = exp2_fast(m - m_new);
-        const float pexp = exp2_fast(s - m_new);
-        lsum = lsum * alpha + pexp;
-        m = m_new;
+        const float mx = row16_max(s);  // finite: token 0 is valid
+        const bool grow = mx > m + kMaxSlack;
+        if (__any(grow)) {
+            const float m_new = grow ? mx : m;
+            const float alpha = exp2_fast(m - m_new);  // 0 on the first page
+            lsum *= alpha;
+            m = m_new;
+            if (n == 0)
+                lds_alpha[kg] = alpha;
+            wave_lds_sync();
+            const float4 al = *reinterpret_cast<const float4*>(lds_alpha);
+            wave_lds_sync();
+            const float alv[4] = {al.x, al.y, al.z, al.w};
+#pragma unroll
+            for (int g = 0; g < G; ++g)
+#pragma unroll
+                for (int d = 0; d < 8; ++d)
+                    acc[g][d] *= alv[g];
+        }
+        const float pexp = exp2_fast(s - m);
+        lsum += pexp;
+        float pv_scale = pexp;
+        if (KV::kScaled)
+            pv_scale *= __int_as_float(__builtin_amdgcn_readlane(__float_as_int(my_vscale), i));
 
-        lds_p[n * 4 + kg] = pexp;
-        if (n == 0)
-            lds_alpha[kg] = alpha;
+        lds_p[n * 4 + kg] = pv_scale;
         wave_lds_sync();
-        const float4 al = *reinterpret_cast<const float4*>(lds_alpha);
         float4 pv[4];
 #pragma unroll
         for (int k = 0; k < 4; ++k)
             pv[k] = *reinterpret_cast<const float4*>(&lds_p[(4 * k + r) * 4]);
         wave_lds_sync();
 
-        const float alv[4] = {al.x, al.y, al.z, al.w};
-#pragma unroll
-        for (int g = 0; g < G; ++g)
-#pragma unroll
-            for (int d = 0; d < 8; ++d)
-                acc[g][d] *= alv[g];
-
         if (valid < kPageSize) {
 #pragma unroll
             for (int k = 0; k < 4; ++k)
                 if (4 * k + r >= valid)
-                    vbuf[k] = make_uint4(0, 0, 0, 0);  // unread slots may hold NaN
+                    KV::clear_values(buf, k);  // unread slots may hold NaN
         }
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             float v[8];
-            unpack8(vbuf[k], v);
+            KV::values(buf, k, v);
             const float pg[4] = {pv[k].x, pv[k].y, pv[k].z, pv[k].w};
 #pragma unroll
             for (int g = 0; g < G; ++g)
@@ -460,11 +564,11 @@ __global__ __launch_bounds__(kWave * kUnitWaves) void split_mfma_bf16(SplitArgs 
         }
     };
 
-    uint4 ka[4], va[4], kb[4], vb[4];
-    stream_pages(t.count, ka, va, kb, vb, issue, consume);
+    typename KV::Buf buf_a, buf_b;
+    stream_pages(t.count, buf_a, buf_b, issue, consume);
 
     // Every lane of a value row holds a partial over tokens = r (mod 4); all
-    // rows share the running max, so the partials simply add.
+    // rows share the reference max, so the partials simply add.
 #pragma unroll
     for (int g = 0; g < G; ++g)
 #pragma unroll
@@ -524,19 +628,21 @@ __global__ __launch_bounds__(kWave * kUnitWaves) void split_valu_bf16(SplitArgs 
     }
 
     const int off = lane * 16;
-    auto issue = [&](uint4 (&kbuf)[4], uint4 (&vbuf)[4], int i) {
+    auto issue = [&](KvBf16::Buf& buf, int i) {
         const int64_t page = __builtin_amdgcn_readlane(my_page, i);
         const uint8_t* ks = slab_base(a.k_pool, page, a.num_kv_heads, t.kvh, kSlabBytesBf16);
         const uint8_t* vs = slab_base(a.v_pool, page, a.num_kv_heads, t.kvh, kSlabBytesBf16);
 #pragma unroll
         for (int k = 0; k < 4; ++k)
-            kbuf[k] = load_stream16(ks + off + 1024 * k);
+            buf.k[k] = load_stream16(ks + off + 1024 * k);
 #pragma unroll
         for (int k = 0; k < 4; ++k)
-            vbuf[k] = load_stream16(vs + off + 1024 * k);
+            buf.v[k] = load_stream16(vs + off + 1024 * k);
     };
 
-    auto consume = [&](uint4 (&kbuf)[4], uint4 (&vbuf)[4], int i) {
+    auto consume = [&](KvBf16::Buf& buf, int i) {
+        uint4 (&kbuf)[4] = buf.k;
+        uint4 (&vbuf)[4] = buf.v;
         const int valid = t.seq_len - task_page(t, i) * kPageSize;
         float sc[G][4];
 #pragma unroll
@@ -590,8 +696,8 @@ __global__ __launch_bounds__(kWave * kUnitWaves) void split_valu_bf16(SplitArgs 
         }
     };
 
-    uint4 ka[4], va[4], kb[4], vb[4];
-    stream_pages(t.count, ka, va, kb, vb, issue, consume);
+    KvBf16::Buf buf_a, buf_b;
+    stream_pages(t.count, buf_a, buf_b, issue, consume);
 
     // Merge the four rows: rescale each to the common max, then add.  A
     // wavefront without pages keeps m = -inf, l = 0, acc = 0.
@@ -692,24 +798,35 @@ __global__ __launch_bounds__(kWave * kMergeWaves) void merge_splits(MergeArgs a)
 typedef void (*SplitKernel)(SplitArgs);
 
 template <int G, bool CHECKED>
-SplitKernel pick_bf16(bool mfma)
+SplitKernel pick(bool fp8, bool mfma)
 {
     if constexpr (G <= 4) {
+        if (fp8)
+            return split_mfma<G, CHECKED, KvFp8>;
         if (mfma)
-            return split_mfma_bf16<G, CHECKED>;
+            return split_mfma<G, CHECKED, KvBf16>;
     }
+    if (fp8)
+        return nullptr;  // fp8 pools are served through the MFMA score tile only
     return split_valu_bf16<G, CHECKED>;
 }
 
-SplitKernel select_split_kernel(int G, bool checked, bool mfma)
+template <bool CHECKED>
+SplitKernel select_for_group(int G, bool fp8, bool mfma)
 {
     switch (G) {
-    case 1: return checked ? pick_bf16<1, true>(mfma) : pick_bf16<1, false>(mfma);
-    case 2: return checked ? pick_bf16<2, true>(mfma) : pick_bf16<2, false>(mfma);
-    case 4: return checked ? pick_bf16<4, true>(mfma) : pick_bf16<4, false>(mfma);
-    case 8: return checked ? pick_bf16<8, true>(mfma) : pick_bf16<8, false>(mfma);
+    case 1: return pick<1, CHECKED>(fp8, mfma);
+    case 2: return pick<2, CHECKED>(fp8, mfma);
+    case 4: return pick<4, CHECKED>(fp8, mfma);
+    case 8: return pick<8, CHECKED>(fp8, mfma);
     default: return nullptr;
     }
+}
+
+SplitKernel select_split_kernel(int G, bool checked, bool fp8, bool mfma)
+{
+    return checked ? select_for_group<true>(G, fp8, mfma)
+                   : select_for_group<false>(G, fp8, mfma);
 }
 
 }  // namespace
@@ -755,7 +872,8 @@ rl_da_status check_config(const rl_da_config* cfg, int* split_tokens, int* split
     if (cfg->head_dim != kHeadDim || cfg->page_size != kPageSize ||
         (G != 1 && G != 2 && G != 4 && G != 8))
         return RL_DA_ERR_UNSUPPORTED;
-    if (cfg->kv_dtype != RL_DA_KV_BF16)
+    if (cfg->kv_dtype == RL_DA_KV_FP8_E4M3 &&
+        (G > 4 || (cfg->flags & RL_DA_SCORES_ON_VALU) != 0))
         return RL_DA_ERR_UNSUPPORTED;
     const int st = cfg->split_tokens == 0 ? kDefaultSplitTokens : cfg->split_tokens;
     if (st % kPageSize != 0 || st > kMaxSplitTokens)
@@ -829,7 +947,8 @@ rl_da_status rl_decode_attn_create(const rl_da_config* cfg, rl_decode_attn** out
     h->max_splits = ms;
     const int G = cfg->num_q_heads / cfg->num_kv_heads;
     h->use_mfma = G <= 4 && (cfg->flags & RL_DA_SCORES_ON_VALU) == 0;
-    h->split_kernel = select_split_kernel(G, (cfg->flags & RL_DA_CHECKED) != 0, h->use_mfma);
+    h->split_kernel = select_split_kernel(G, (cfg->flags & RL_DA_CHECKED) != 0,
+                                          cfg->kv_dtype == RL_DA_KV_FP8_E4M3, h->use_mfma);
     if (hipGetDevice(&h->device) != hipSuccess) {
         free(h);
         return RL_DA_ERR_HIP;

@@ -80,6 +80,8 @@ def test_workspace_size_formula():
     (dict(num_q_heads=24, num_kv_heads=8), B.RL_DA_ERR_UNSUPPORTED),   # G = 3
     (dict(num_q_heads=128, num_kv_heads=8), B.RL_DA_ERR_UNSUPPORTED),  # G = 16
     (dict(split_tokens=24), B.RL_DA_ERR_UNSUPPORTED),
+    (dict(num_q_heads=64, num_kv_heads=8, kv_dtype=B.RL_DA_KV_FP8_E4M3), B.RL_DA_ERR_UNSUPPORTED),
+    (dict(kv_dtype=B.RL_DA_KV_FP8_E4M3, flags=B.RL_DA_SCORES_ON_VALU), B.RL_DA_ERR_UNSUPPORTED),
     (dict(split_tokens=4112), B.RL_DA_ERR_UNSUPPORTED),
 ])
 def test_create_rejects_bad_config_without_gpu(kw, status):
