@@ -42,8 +42,9 @@
  * It does not read device memory to check, so these are preconditions:
  *   0 <= block_table[b][j] < num_pages  for j < ceil(seq_lens[b] / page_size)
  *   seq_lens[b] <= max_pages * page_size
- * Block-table entries past a sequence's last page and token slots past its
- * length are never read, and may hold anything (including NaN values).  A
+ * Block-table entries past a sequence's last page (inside the table row) may
+ * hold anything and are never used as page indices; token slots past a
+ * sequence's length are masked and may hold anything, including NaN.  A
  * sequence with seq_lens[b] <= 0 produces zeros.  With RL_DA_CHECKED set at
  * create(), the kernels test the preconditions, skip the offending work, and
  * record the violation in a device error word read by
