@@ -79,6 +79,7 @@ struct PageReadArgs {
     int32_t max_pages;
     int32_t split_pages;
     int32_t num_splits;
+    int32_t slab_bytes;  // 4096 (bf16) or 2048 (e4m3)
 };
 
 __global__ __launch_bounds__(64 * kUnitWaves) void page_read_kernel(PageReadArgs a)
@@ -98,16 +99,29 @@ __global__ __launch_bounds__(64 * kUnitWaves) void page_read_kernel(PageReadArgs
     const int voff = lane * 16;
     for (int j = p0 + wave; j < p1; j += kUnitWaves) {
         const int64_t page = a.block_table[(int64_t)b * a.max_pages + j];
-        const int64_t slab = (page * a.num_kv_heads + kvh) * 4096;
-        uint4 k[4], v[4];
+        const int64_t slab = (page * a.num_kv_heads + kvh) * a.slab_bytes;
+        if (a.slab_bytes == 4096) {
+            uint4 k[4], v[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            k[i] = load_stream16(a.k_pool + slab + koff + 64 * i);
-            v[i] = load_stream16(a.v_pool + slab + voff + 1024 * i);
+            for (int i = 0; i < 4; ++i) {
+                k[i] = load_stream16(a.k_pool + slab + koff + 64 * i);
+                v[i] = load_stream16(a.v_pool + slab + voff + 1024 * i);
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                acc ^= k[i].x ^ k[i].y ^ k[i].z ^ k[i].w ^ v[i].x ^ v[i].y ^ v[i].z ^ v[i].w;
+        } else {
+            const int koff8 = (lane & 15) * 128 + 16 * (lane >> 4);
+            uint4 k[2], v[2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                k[i] = load_stream16(a.k_pool + slab + koff8 + 64 * i);
+                v[i] = load_stream16(a.v_pool + slab + voff + 1024 * i);
+            }
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+                acc ^= k[i].x ^ k[i].y ^ k[i].z ^ k[i].w ^ v[i].x ^ v[i].y ^ v[i].z ^ v[i].w;
         }
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-            acc ^= k[i].x ^ k[i].y ^ k[i].z ^ k[i].w ^ v[i].x ^ v[i].y ^ v[i].z ^ v[i].w;
     }
     a.sink[(size_t)unit * 64 * kUnitWaves + threadIdx.x] = acc;
 }
@@ -138,14 +152,16 @@ int rl_bench_stream_read(const void* src, size_t bytes, uint32_t* sink, int grid
     return (int)hipGetLastError();
 }
 
-// bf16 pools [P][Hkv][16][128]; sink must hold batch*num_kv_heads*num_splits*256 words.
+// Pools [P][Hkv][16][128] of 2-byte (slab_bytes 4096) or 1-byte (2048)
+// elements; sink must hold batch*num_kv_heads*num_splits*256 words.
 int rl_bench_page_read(const void* k_pool, const void* v_pool, const int32_t* block_table,
                        int32_t max_pages, const int32_t* seq_lens, int32_t batch,
-                       int32_t num_kv_heads, int32_t split_pages, uint32_t* sink, void* stream)
+                       int32_t num_kv_heads, int32_t split_pages, int32_t slab_bytes,
+                       uint32_t* sink, void* stream)
 {
     if (k_pool == nullptr || v_pool == nullptr || block_table == nullptr ||
         seq_lens == nullptr || sink == nullptr || batch <= 0 || num_kv_heads <= 0 ||
-        max_pages <= 0 || split_pages <= 0)
+        max_pages <= 0 || split_pages <= 0 || (slab_bytes != 4096 && slab_bytes != 2048))
         return -1;
     PageReadArgs a;
     a.k_pool = (const uint8_t*)k_pool;
@@ -157,6 +173,7 @@ int rl_bench_page_read(const void* k_pool, const void* v_pool, const int32_t* bl
     a.max_pages = max_pages;
     a.split_pages = split_pages;
     a.num_splits = (max_pages + split_pages - 1) / split_pages;
+    a.slab_bytes = slab_bytes;
     const int64_t units = (int64_t)batch * num_kv_heads * a.num_splits;
     hipLaunchKernelGGL(page_read_kernel, dim3((unsigned)units), dim3(64 * kUnitWaves), 0,
                        (hipStream_t)stream, a);

@@ -438,8 +438,11 @@ struct KvFp8 {
 
 constexpr float kMaxSlack = 8.0f;
 
+// Three wavefronts per SIMD: the register budget (168) fits both page buffers
+// and the accumulators without spilling.
 template <int G, bool CHECKED, typename KV>
-__global__ __launch_bounds__(kWave * kUnitWaves) void split_mfma(SplitArgs a)
+__global__ __launch_bounds__(kWave * kUnitWaves)
+__attribute__((amdgpu_waves_per_eu(3))) void split_mfma(SplitArgs a)
 {
     static_assert(G >= 1 && G <= 4, "MFMA score tile packs at most 4 query heads");
     __shared__ __attribute__((aligned(16))) float lds_p_all[kUnitWaves][kPageSize * 4];
