@@ -49,6 +49,26 @@ def build(force: bool = True) -> str:
     return LIB_PATH
 
 
+class _Append(ctypes.Structure):
+    _fields_ = [
+        ("batch", ctypes.c_int32),
+        ("num_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("page_size", ctypes.c_int32),
+        ("kv_dtype", ctypes.c_int32),
+        ("max_pages", ctypes.c_int32),
+        ("num_pages", ctypes.c_int64),
+        ("k_new", ctypes.c_void_p),
+        ("v_new", ctypes.c_void_p),
+        ("k_pool", ctypes.c_void_p),
+        ("v_pool", ctypes.c_void_p),
+        ("k_scale", ctypes.c_void_p),
+        ("v_scale", ctypes.c_void_p),
+        ("block_table", ctypes.c_void_p),
+        ("seq_lens", ctypes.c_void_p),
+    ]
+
+
 class _Problem(ctypes.Structure):
     _fields_ = [
         ("batch", ctypes.c_int32),
@@ -90,6 +110,10 @@ def _load():
         lib.rl_oracle_e4m3_to_double.restype = ctypes.c_double
         lib.rl_oracle_bf16_to_double.argtypes = [ctypes.c_uint16]
         lib.rl_oracle_bf16_to_double.restype = ctypes.c_double
+        lib.rl_oracle_kv_append.argtypes = [ctypes.POINTER(_Append)]
+        lib.rl_oracle_kv_append.restype = ctypes.c_int
+        lib.rl_oracle_e4m3_encode.argtypes = [ctypes.c_float]
+        lib.rl_oracle_e4m3_encode.restype = ctypes.c_uint8
         lib.rl_oracle_max_threads.argtypes = []
         lib.rl_oracle_max_threads.restype = ctypes.c_int
         _lib = lib
@@ -152,6 +176,44 @@ def decode_attention(q_bits, k_pool, v_pool, block_table, seq_lens, *,
     if rc != OK:
         raise OracleError("oracle failed with code %d" % rc)
     return out
+
+
+def kv_append(k_new_bits, v_new_bits, k_pool, v_pool, block_table, seq_lens, *,
+              kv_dtype=KV_BF16, k_scale=None, v_scale=None):
+    """Appends one token per (sequence, kv head); returns updated copies of
+    (k_pool, v_pool, k_scale, v_scale).  k_new/v_new: uint16 bf16 bits
+    [B, Hkv, D]; pools as in decode_attention; seq_lens = lengths before the
+    append."""
+    lib = _load()
+    k_new_bits = _c(k_new_bits, np.uint16)
+    v_new_bits = _c(v_new_bits, np.uint16)
+    pool_dtype = np.uint16 if kv_dtype == KV_BF16 else np.uint8
+    k_pool = _c(k_pool, pool_dtype).copy()
+    v_pool = _c(v_pool, pool_dtype).copy()
+    block_table = _c(block_table, np.int32)
+    seq_lens = _c(seq_lens, np.int32)
+    B, Hkv, D = k_new_bits.shape
+    P, Hkv2, page, D2 = k_pool.shape
+    if (Hkv2, D2) != (Hkv, D) or v_new_bits.shape != k_new_bits.shape:
+        raise ValueError("shape mismatch")
+    if kv_dtype == KV_FP8_E4M3:
+        k_scale = _c(k_scale, np.float32).copy()
+        v_scale = _c(v_scale, np.float32).copy()
+    prob = _Append(
+        batch=B, num_kv_heads=Hkv, head_dim=D, page_size=page, kv_dtype=kv_dtype,
+        max_pages=block_table.shape[1], num_pages=P, k_new=k_new_bits.ctypes.data,
+        v_new=v_new_bits.ctypes.data, k_pool=k_pool.ctypes.data, v_pool=v_pool.ctypes.data,
+        k_scale=k_scale.ctypes.data if kv_dtype == KV_FP8_E4M3 else None,
+        v_scale=v_scale.ctypes.data if kv_dtype == KV_FP8_E4M3 else None,
+        block_table=block_table.ctypes.data, seq_lens=seq_lens.ctypes.data)
+    rc = lib.rl_oracle_kv_append(ctypes.byref(prob))
+    if rc != OK:
+        raise OracleError("oracle append failed with code %d" % rc)
+    return k_pool, v_pool, k_scale, v_scale
+
+
+def e4m3_encode(x: float) -> int:
+    return _load().rl_oracle_e4m3_encode(float(x))
 
 
 def e4m3_to_double(code: int) -> float:

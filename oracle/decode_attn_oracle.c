@@ -211,6 +211,132 @@ int rl_oracle_decode_attn(const rl_oracle_problem* p, const int32_t* rows,
     return failed ? RL_ORACLE_ERR_NOMEM : RL_ORACLE_OK;
 }
 
+/*
+ * Round-to-nearest-even onto the OCP E4M3FN grid, from the format's
+ * definition: 4 exponent bits with bias 7, 3 mantissa bits, subnormals
+ * m/8 * 2^-6, largest finite 448.  Inputs are finite with |x| <= 448 (callers
+ * clamp first); NaN encodes as 0x7F.  The sign of zero is kept.
+ */
+uint8_t rl_oracle_e4m3_encode(float x)
+{
+    if (x != x)
+        return 0x7F;
+    const uint8_t sign = signbit(x) ? 0x80 : 0x00;
+    const double a = fabs((double)x);
+    if (a < ldexp(1.0, -6)) {
+        /* subnormal step 2^-9; rounding up to 8 steps yields code 0x08 = 2^-6 */
+        const double steps = rint(a * 512.0);
+        return sign | (uint8_t)steps;
+    }
+    int e = (int)floor(log2(a));
+    if (ldexp(1.0, e) > a)  /* guard log2 rounding at exact powers of two */
+        e -= 1;
+    if (ldexp(1.0, e + 1) <= a)
+        e += 1;
+    double q = rint((a / ldexp(1.0, e) - 1.0) * 8.0);
+    if (q == 8.0) {
+        q = 0.0;
+        e += 1;
+    }
+    return sign | (uint8_t)(((e + 7) << 3) | (int)q);
+}
+
+/* fp32 slab scale for a maximum magnitude: absmax / 448, or 1 for zero. */
+static float slab_scale_for(float absmax)
+{
+    return absmax > 0.0f ? absmax / 448.0f : 1.0f;
+}
+
+static float clamp448(float v)
+{
+    return v > 448.0f ? 448.0f : (v < -448.0f ? -448.0f : v);
+}
+
+/*
+ * Appends one token per (sequence, kv head) to a pool.  For bf16 pools the
+ * token's bits are copied into page block_table[b][L/16], slot L%16
+ * (L = seq_lens[b], the length before the append).  For e4m3 pools, in fp32:
+ *   slot 0 (the page starts empty):  scale = absmax(token)/448 (1 if zero)
+ *   later slots:  scale' = max(scale, absmax(token)/448); when it grows, every
+ *     stored code c of the slab's earlier slots becomes
+ *     e4m3(e4m3value(c) * (scale / scale'))
+ *   the token:  e4m3(clamp(x / scale', +-448))
+ * with e4m3() rounding to nearest even.  Sequences with L < 0 are skipped.
+ */
+int rl_oracle_kv_append(const rl_oracle_append* p)
+{
+    if (p == NULL || p->k_new == NULL || p->v_new == NULL || p->k_pool == NULL ||
+        p->v_pool == NULL || p->block_table == NULL || p->seq_lens == NULL ||
+        p->batch < 0 || p->num_kv_heads <= 0 || p->head_dim <= 0 || p->page_size <= 0 ||
+        p->max_pages <= 0 || p->num_pages <= 0)
+        return RL_ORACLE_ERR_ARG;
+    const int fp8 = p->kv_dtype == RL_ORACLE_KV_FP8_E4M3;
+    if (!fp8 && p->kv_dtype != RL_ORACLE_KV_BF16)
+        return RL_ORACLE_ERR_ARG;
+    if (fp8 && (p->k_scale == NULL || p->v_scale == NULL))
+        return RL_ORACLE_ERR_ARG;
+    for (int b = 0; b < p->batch; ++b) {
+        const int L = p->seq_lens[b];
+        if (L < 0)
+            continue;
+        if ((int64_t)L >= (int64_t)p->max_pages * p->page_size)
+            return RL_ORACLE_ERR_PRECONDITION;
+        const int32_t page = p->block_table[(int64_t)b * p->max_pages + L / p->page_size];
+        if (page < 0 || (int64_t)page >= p->num_pages)
+            return RL_ORACLE_ERR_PRECONDITION;
+    }
+    const int D = p->head_dim, P = p->page_size, H = p->num_kv_heads;
+    for (int b = 0; b < p->batch; ++b) {
+        const int L = p->seq_lens[b];
+        if (L < 0)
+            continue;
+        const int64_t page = p->block_table[(int64_t)b * p->max_pages + L / P];
+        const int slot = L % P;
+        for (int kvh = 0; kvh < H; ++kvh) {
+            for (int which = 0; which < 2; ++which) {
+                const uint16_t* src = (const uint16_t*)(which ? p->v_new : p->k_new) +
+                                      ((int64_t)b * H + kvh) * D;
+                const int64_t slab = page * H + kvh;
+                if (!fp8) {
+                    uint16_t* dst = (uint16_t*)(which ? p->v_pool : p->k_pool) +
+                                    (slab * P + slot) * D;
+                    memcpy(dst, src, sizeof(uint16_t) * (size_t)D);
+                    continue;
+                }
+                uint8_t* codes = (uint8_t*)(which ? p->v_pool : p->k_pool) + slab * P * D;
+                float* scale = (which ? p->v_scale : p->k_scale) + slab;
+                float absmax = 0.0f;
+                for (int d = 0; d < D; ++d) {
+                    const float v = fabsf((float)rl_oracle_bf16_to_double(src[d]));
+                    if (v > absmax)
+                        absmax = v;
+                }
+                const float wanted = slab_scale_for(absmax);
+                float s_new;
+                if (slot == 0) {
+                    s_new = wanted;
+                } else {
+                    const float s_old = *scale;
+                    s_new = wanted > s_old ? wanted : s_old;
+                    if (s_new != s_old) {
+                        const float ratio = s_old / s_new;
+                        for (int i = 0; i < slot * D; ++i) {
+                            const float old = (float)rl_oracle_e4m3_to_double(codes[i]);
+                            codes[i] = rl_oracle_e4m3_encode(old * ratio);
+                        }
+                    }
+                }
+                *scale = s_new;
+                for (int d = 0; d < D; ++d) {
+                    const float x = (float)rl_oracle_bf16_to_double(src[d]);
+                    codes[slot * D + d] = rl_oracle_e4m3_encode(clamp448(x / s_new));
+                }
+            }
+        }
+    }
+    return RL_ORACLE_OK;
+}
+
 int rl_oracle_max_threads(void)
 {
 #ifdef _OPENMP

@@ -57,6 +57,34 @@ typedef struct {
 int rl_oracle_decode_attn(const rl_oracle_problem* p, const int32_t* rows,
                           int64_t num_rows, double* out);
 
+/*
+ * One decode step's K/V cache append (the step before attention): the new
+ * token of every sequence b (k_new/v_new [batch][num_kv_heads][head_dim] bf16
+ * bits) is written to page block_table[b][L/page_size], slot L%page_size,
+ * L = seq_lens[b] (length before the append; L < 0 skips b).  e4m3 pools keep
+ * one fp32 scale per (page, kv head) that only grows; see the .c file for the
+ * exact fp32 rules.  Pools and scales are updated in place.
+ */
+typedef struct {
+    int32_t batch, num_kv_heads, head_dim, page_size;
+    int32_t kv_dtype;
+    int32_t max_pages;
+    int64_t num_pages;
+    const void* k_new;
+    const void* v_new;
+    void* k_pool;
+    void* v_pool;
+    float* k_scale;
+    float* v_scale;
+    const int32_t* block_table;
+    const int32_t* seq_lens;
+} rl_oracle_append;
+
+int rl_oracle_kv_append(const rl_oracle_append* p);
+
+/* Round-to-nearest-even e4m3 code of x, |x| <= 448 (NaN -> 0x7F). */
+uint8_t rl_oracle_e4m3_encode(float x);
+
 /* Exact value of one OCP E4M3FN code (NaN for S.1111.111). */
 double rl_oracle_e4m3_to_double(uint8_t code);
 

@@ -1,8 +1,8 @@
 """The oracle's pins must catch plausible mistakes (CPU only).
 
 Each case below plants one slip in a private copy of the oracle's C source,
-builds it, and runs the pin suite (test_oracle.py) against that build in a
-fresh process.  The suite must fail for every mutant and pass for the
+builds it, and runs the pin suites (attention, append, codecs) against that
+build in a fresh process.  The suite must fail for every mutant and pass for the
 unmodified source built the same way.
 """
 import concurrent.futures
@@ -49,6 +49,17 @@ MUTANTS = [
      "dst[d] += w * pool_element(p, p->v_pool, p->k_scale,"),
     ("bf16 read as low half", "uint32_t u = (uint32_t)bits << 16;",
      "uint32_t u = (uint32_t)bits << 15;"),
+    ("append to the next slot", "codes[slot * D + d] = rl_oracle_e4m3_encode(",
+     "codes[((slot + 1) % P) * D + d] = rl_oracle_e4m3_encode("),
+    ("append scale never grows", "s_new = wanted > s_old ? wanted : s_old;",
+     "s_new = s_old;"),
+    ("append rescale ratio inverted", "const float ratio = s_old / s_new;",
+     "const float ratio = s_new / s_old;"),
+    ("append reads kv head 0", "((int64_t)b * H + kvh) * D;", "((int64_t)b * H) * D;"),
+    ("encoder ties away from zero", "double q = rint((a / ldexp(1.0, e) - 1.0) * 8.0);",
+     "double q = round((a / ldexp(1.0, e) - 1.0) * 8.0);"),
+    ("encoder subnormal step", "const double steps = rint(a * 512.0);",
+     "const double steps = rint(a * 256.0);"),
 ]
 
 
@@ -63,11 +74,14 @@ def _build(src_text, workdir, name):
     return so_path
 
 
+PIN_FILES = ["test_oracle.py", "test_oracle_append.py", "test_codecs.py"]
+
+
 def _run_pins(so_path):
     env = dict(os.environ, RL_ORACLE_LIB=so_path, OMP_NUM_THREADS="2")
     r = subprocess.run(
-        [sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
-         os.path.join(ROOT, "tests", "test_oracle.py")],
+        [sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider"] +
+        [os.path.join(ROOT, "tests", f) for f in PIN_FILES],
         cwd=ROOT, env=env, stdout=subprocess.PIPE, stderr=subprocess.STDOUT,
         timeout=600)
     return r.returncode, r.stdout.decode(errors="replace")[-2000:]
