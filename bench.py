@@ -101,6 +101,9 @@ def parse_args():
     ap.add_argument("--pmc-calibrate", action="store_true",
                     help="launch one plain copy of %d bytes first, so that a counter "
                          "run can scale FETCH_SIZE/WRITE_SIZE" % COPY_CALIBRATION_BYTES)
+    ap.add_argument("--op", choices=["attention", "append"], default="attention",
+                    help="attention (the decode step, default) or the KV-cache append "
+                         "that precedes it (a separate JSON line with its own metric)")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="turn two rocprofv3 --pmc counter_collection.csv files (FETCH_SIZE, "
                          "WRITE_SIZE) of a --pmc-calibrate run into profiles/traffic.json")
@@ -218,6 +221,49 @@ def cpu_baseline(p, rows_per_call=None):
     }
 
 
+def bench_append(args, base, stream):
+    """Times K KV-cache appends (one new token per sequence and kv head) on the
+    workload's shapes; every sequence appends at its current length."""
+    import numpy as np
+    import torch
+    from paper_2512_22492_amd import binding
+    L = base.lengths()
+    room = L < base.max_pages * base.page_size
+    if not room.all():
+        # append at the last slot of the last page instead of past the table
+        base.seq_lens.copy_(torch.from_numpy(np.minimum(L, base.max_pages * base.page_size - 1)
+                                             .astype(np.int32)).to(base.seq_lens.device))
+    gen = torch.Generator(device=base.q.device).manual_seed(1)
+    shape = (base.batch, base.num_kv_heads, base.head_dim)
+    k = torch.randn(shape, generator=gen, device=base.q.device).to(torch.bfloat16)
+    v = torch.randn(shape, generator=gen, device=base.q.device).to(torch.bfloat16)
+    for _ in range(args.warmup):
+        binding.kv_append(base, k, v, stream=stream)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        binding.kv_append(base, k, v, stream=stream)
+    torch.cuda.synchronize()
+    us = (time.perf_counter() - t0) * 1e6 / args.steps
+    elt = 2 if base.kv_dtype == "bf16" else 1
+    tok = base.batch * base.num_kv_heads * base.head_dim
+    moved = 2 * (tok * 2 + tok * elt) + base.batch * 8   # read new K/V, write slots, table
+    return {
+        "metric": "KV-cache append (one token per sequence) us per call, 1 GPU",
+        "value": round(us, 3), "unit": "us", "higher_is_better": False,
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "dtype": base.kv_dtype, "data": "synthetic",
+        "config": {"workload": "%s: %s" % (args.config, _describe(args.config)),
+                   "batch": base.batch, "num_kv_heads": base.num_kv_heads},
+        "bytes_per_call": moved, "GBs": round(moved / us / 1e3, 2),
+    }
+
+
+def _describe(name):
+    from paper_2512_22492_amd import workloads
+    return workloads.describe(name)
+
+
 def main():
     args = parse_args()
     if args.summarize_pmc:
@@ -248,6 +294,9 @@ def main():
             **base.__dict__, "k_pool": base.k_pool.clone(), "v_pool": base.v_pool.clone(),
             "k_scale": None if base.k_scale is None else base.k_scale.clone(),
             "v_scale": None if base.v_scale is None else base.v_scale.clone()}))
+    if args.op == "append":
+        print(json.dumps(bench_append(args, base, torch.cuda.current_stream())), flush=True)
+        return
     out = torch.empty_like(base.q)
     flags = binding.RL_DA_SCORES_ON_VALU if args.scores == "valu" else 0
     attn = binding.DecodeAttention.for_problem(base, flags=flags,

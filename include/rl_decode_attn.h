@@ -143,6 +143,42 @@ rl_da_status rl_decode_attn_split_info(const rl_decode_attn* h, int32_t max_page
                                        int32_t* split_tokens, int32_t* num_splits);
 
 /*
+ * KV-cache append: the step before attention in every decode step (the
+ * rollout engine generates one token per sequence per step, Sec. 2.1; the
+ * new token's key and value join the paged cache the attention then reads).
+ * For every sequence b with L = seq_lens[b] >= 0 (its length BEFORE the
+ * append) and every kv head, the new token k_new[b][kvh][:], v_new[b][kvh][:]
+ * (bf16, [batch][num_kv_heads][head_dim]) is written to page
+ * block_table[b][L / page_size], slot L % page_size of k_pool / v_pool.  The
+ * caller has already placed that page in the table and increments seq_lens
+ * afterwards.
+ *
+ * bf16 pools: the token's bits are copied.  e4m3 pools keep one fp32 scale
+ * per (page, kv head) that only grows (the paper is silent on re-scaling; this
+ * is the build's reading), computed in fp32 and rounded to nearest even:
+ *   slot 0 (fresh page):  scale = absmax(token) / 448, or 1 if zero
+ *   other slots:  scale' = max(scale, absmax(token) / 448); when it grows,
+ *     each earlier code c of the slab becomes e4m3(value(c) * (scale/scale'))
+ *   the token:  e4m3(clamp(x / scale', -448, 448))
+ * Different sequences must append into different (page, kv head) slabs.
+ *
+ * Bounds are checked on the device: a sequence whose L is at least
+ * max_pages * page_size, or whose target page is outside [0, num_pages), is
+ * skipped (nothing written) and, when device_error is non-NULL, reported in
+ * that int32 device word with RL_DA_DEVERR_LENGTH_TOO_LONG /
+ * RL_DA_DEVERR_PAGE_OUT_OF_RANGE (bits are only ever set).  Needs no handle;
+ * enqueues one kernel on `stream`.  head_dim 128 and page_size 16 only
+ * (else UNSUPPORTED); k_new, v_new and the pools 16-byte aligned; k_scale and
+ * v_scale non-NULL exactly for e4m3.
+ */
+rl_da_status rl_kv_append(const void* k_new, const void* v_new, void* k_pool, void* v_pool,
+                          float* k_scale, float* v_scale, int64_t num_pages,
+                          const int32_t* block_table, int32_t max_pages,
+                          const int32_t* seq_lens, int32_t batch, int32_t num_kv_heads,
+                          int32_t head_dim, int32_t page_size, int32_t kv_dtype,
+                          int32_t* device_error, void* stream);
+
+/*
  * Measurement hook (no counterpart in the paper): with both events non-NULL,
  * every later run() records split_begin on its stream just before the split-K
  * kernel and split_end just after it, so hipEventElapsedTime gives that
