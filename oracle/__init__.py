@@ -110,6 +110,9 @@ def _load():
         lib.rl_oracle_e4m3_to_double.restype = ctypes.c_double
         lib.rl_oracle_bf16_to_double.argtypes = [ctypes.c_uint16]
         lib.rl_oracle_bf16_to_double.restype = ctypes.c_double
+        lib.rl_oracle_extend_attn.argtypes = [ctypes.POINTER(_Problem), ctypes.c_void_p,
+                                              ctypes.c_void_p]
+        lib.rl_oracle_extend_attn.restype = ctypes.c_int
         lib.rl_oracle_kv_append.argtypes = [ctypes.POINTER(_Append)]
         lib.rl_oracle_kv_append.restype = ctypes.c_int
         lib.rl_oracle_e4m3_encode.argtypes = [ctypes.c_float]
@@ -175,6 +178,42 @@ def decode_attention(q_bits, k_pool, v_pool, block_table, seq_lens, *,
                                        rows.shape[0], out.ctypes.data)
     if rc != OK:
         raise OracleError("oracle failed with code %d" % rc)
+    return out
+
+
+def extend_attention(q_bits, q_start, k_pool, v_pool, block_table, seq_lens, *,
+                     num_kv_heads, scale, kv_dtype=KV_BF16, k_scale=None, v_scale=None):
+    """Causal attention of each sequence's new tokens (q rows q_start[b] ..
+    q_start[b+1]-1, the last n_b cached tokens) over its cache.  q_bits uint16
+    [T, Hq, D]; returns fp64 [T, Hq, D]."""
+    lib = _load()
+    q_bits = _c(q_bits, np.uint16)
+    q_start = _c(q_start, np.int32)
+    pool_dtype = np.uint16 if kv_dtype == KV_BF16 else np.uint8
+    k_pool = _c(k_pool, pool_dtype)
+    v_pool = _c(v_pool, pool_dtype)
+    block_table = _c(block_table, np.int32)
+    seq_lens = _c(seq_lens, np.int32)
+    T, Hq, D = q_bits.shape
+    B = seq_lens.shape[0]
+    P, Hkv, page, _ = k_pool.shape
+    if q_start.shape != (B + 1,) or q_start[-1] != T:
+        raise ValueError("q_start must have batch+1 entries ending at T")
+    if kv_dtype == KV_FP8_E4M3:
+        k_scale = _c(k_scale, np.float32)
+        v_scale = _c(v_scale, np.float32)
+    prob = _Problem(
+        batch=B, num_q_heads=Hq, num_kv_heads=Hkv, head_dim=D, page_size=page,
+        kv_dtype=kv_dtype, max_pages=block_table.shape[1], num_pages=P,
+        scale=float(scale), q=q_bits.ctypes.data, k_pool=k_pool.ctypes.data,
+        v_pool=v_pool.ctypes.data,
+        k_scale=k_scale.ctypes.data if kv_dtype == KV_FP8_E4M3 else None,
+        v_scale=v_scale.ctypes.data if kv_dtype == KV_FP8_E4M3 else None,
+        block_table=block_table.ctypes.data, seq_lens=seq_lens.ctypes.data)
+    out = np.empty((T, Hq, D), dtype=np.float64)
+    rc = lib.rl_oracle_extend_attn(ctypes.byref(prob), q_start.ctypes.data, out.ctypes.data)
+    if rc != OK:
+        raise OracleError("oracle extend failed with code %d" % rc)
     return out
 
 

@@ -104,28 +104,18 @@ static int row_is_valid(const rl_oracle_problem* p, int b, int h)
 }
 
 /*
- * One output row out[b,h,:], written to dst[0..D-1].  `scores` is caller
- * scratch of at least seq_lens[b] doubles.
+ * Attention of one query row qrow (head_dim bf16 values) over the first
+ * `visible` cached tokens of sequence b, kv head kvh, written to dst[0..D-1].
+ * `scores` is caller scratch of at least `visible` doubles; visible >= 1.
  */
-static void attend_one_row(const rl_oracle_problem* p, int b, int h,
-                           double* scores, double* dst)
+static void attend_prefix(const rl_oracle_problem* p, const uint16_t* qrow, int b, int kvh,
+                          int visible, double* scores, double* dst)
 {
     const int D = p->head_dim;
-    const int G = p->num_q_heads / p->num_kv_heads;
-    const int kvh = h / G;
-    const int L = p->seq_lens[b];
     const int32_t* pages = p->block_table + (int64_t)b * p->max_pages;
-    const uint16_t* qrow =
-        (const uint16_t*)p->q + ((int64_t)b * p->num_q_heads + h) * D;
-
-    if (L <= 0) {
-        for (int d = 0; d < D; ++d)
-            dst[d] = 0.0;
-        return;
-    }
 
     /* Scores s_t = scale * sum_d q[d] * k_t[d]. */
-    for (int t = 0; t < L; ++t) {
+    for (int t = 0; t < visible; ++t) {
         const int64_t page = pages[t / p->page_size];
         const int slot = t % p->page_size;
         double dot = 0.0;
@@ -137,11 +127,11 @@ static void attend_one_row(const rl_oracle_problem* p, int b, int h,
 
     /* Softmax weights w_t = exp(s_t - max_s) / sum_u exp(s_u - max_s). */
     double smax = scores[0];
-    for (int t = 1; t < L; ++t)
+    for (int t = 1; t < visible; ++t)
         if (scores[t] > smax)
             smax = scores[t];
     double z = 0.0;
-    for (int t = 0; t < L; ++t) {
+    for (int t = 0; t < visible; ++t) {
         scores[t] = exp(scores[t] - smax);
         z += scores[t];
     }
@@ -149,7 +139,7 @@ static void attend_one_row(const rl_oracle_problem* p, int b, int h,
     /* out[d] = sum_t w_t * v_t[d]. */
     for (int d = 0; d < D; ++d)
         dst[d] = 0.0;
-    for (int t = 0; t < L; ++t) {
+    for (int t = 0; t < visible; ++t) {
         const int64_t page = pages[t / p->page_size];
         const int slot = t % p->page_size;
         const double w = scores[t] / z;
@@ -157,6 +147,22 @@ static void attend_one_row(const rl_oracle_problem* p, int b, int h,
             dst[d] += w * pool_element(p, p->v_pool, p->v_scale, page, kvh,
                                        slot, d);
     }
+}
+
+/* Decode row out[b,h,:]: query q[b,h,:] over all seq_lens[b] tokens. */
+static void attend_one_row(const rl_oracle_problem* p, int b, int h,
+                           double* scores, double* dst)
+{
+    const int G = p->num_q_heads / p->num_kv_heads;
+    const int L = p->seq_lens[b];
+    if (L <= 0) {
+        for (int d = 0; d < p->head_dim; ++d)
+            dst[d] = 0.0;
+        return;
+    }
+    const uint16_t* qrow =
+        (const uint16_t*)p->q + ((int64_t)b * p->num_q_heads + h) * p->head_dim;
+    attend_prefix(p, qrow, b, h / G, L, scores, dst);
 }
 
 int rl_oracle_decode_attn(const rl_oracle_problem* p, const int32_t* rows,
@@ -205,6 +211,72 @@ int rl_oracle_decode_attn(const rl_oracle_problem* p, const int32_t* rows,
             const int b = rows ? rows[2 * r] : (int)(r / p->num_q_heads);
             const int h = rows ? rows[2 * r + 1] : (int)(r % p->num_q_heads);
             attend_one_row(p, b, h, scores, out + r * p->head_dim);
+        }
+        free(scores);
+    }
+    return failed ? RL_ORACLE_ERR_NOMEM : RL_ORACLE_OK;
+}
+
+/*
+ * Extend (prefill) attention: n_b new query tokens per sequence whose keys and
+ * values are already in the cache, i.e. the last n_b of its L_b = seq_lens[b]
+ * cached tokens.  Query token i of sequence b (row q_start[b] + i of q/out)
+ * sits at position L_b - n_b + i and attends causally to cache tokens
+ * t <= L_b - n_b + i.  A decode step is the case n_b = 1.
+ */
+static void extend_one_row(const rl_oracle_problem* p, const int32_t* q_start, int64_t row,
+                           int b, int h, double* scores, double* dst)
+{
+    const int G = p->num_q_heads / p->num_kv_heads;
+    const int n_new = q_start[b + 1] - q_start[b];
+    const int L = p->seq_lens[b];
+    const int i = (int)(row - q_start[b]);
+    const int visible = L - n_new + i + 1;  /* tokens 0 .. L-n_new+i */
+    const uint16_t* qrow = (const uint16_t*)p->q + (row * p->num_q_heads + h) * p->head_dim;
+    attend_prefix(p, qrow, b, h / G, visible, scores, dst);
+}
+
+int rl_oracle_extend_attn(const rl_oracle_problem* p, const int32_t* q_start, double* out)
+{
+    if (p == NULL || q_start == NULL || out == NULL || p->q == NULL || p->k_pool == NULL ||
+        p->v_pool == NULL || p->block_table == NULL || p->seq_lens == NULL)
+        return RL_ORACLE_ERR_ARG;
+    if (p->batch < 0 || p->num_q_heads <= 0 || p->num_kv_heads <= 0 ||
+        p->num_q_heads % p->num_kv_heads != 0 || p->head_dim <= 0 || p->page_size <= 0)
+        return RL_ORACLE_ERR_ARG;
+    if (p->kv_dtype == RL_ORACLE_KV_FP8_E4M3 && (p->k_scale == NULL || p->v_scale == NULL))
+        return RL_ORACLE_ERR_ARG;
+    if (q_start[0] != 0)
+        return RL_ORACLE_ERR_ARG;
+    int max_len = 1;
+    for (int b = 0; b < p->batch; ++b) {
+        const int n = q_start[b + 1] - q_start[b];
+        if (n < 0 || n > p->seq_lens[b])
+            return RL_ORACLE_ERR_PRECONDITION;
+        if (n > 0 && !row_is_valid(p, b, 0))
+            return RL_ORACLE_ERR_PRECONDITION;
+        if (p->seq_lens[b] > max_len)
+            max_len = p->seq_lens[b];
+    }
+    const int64_t T = q_start[p->batch];
+    int failed = 0;
+#pragma omp parallel
+    {
+        double* scores = (double*)malloc(sizeof(double) * (size_t)max_len);
+        if (scores == NULL) {
+#pragma omp atomic write
+            failed = 1;
+        }
+#pragma omp for schedule(dynamic, 1)
+        for (int64_t r = 0; r < T * p->num_q_heads; ++r) {
+            if (scores == NULL)
+                continue;
+            const int64_t row = r / p->num_q_heads;
+            const int h = (int)(r % p->num_q_heads);
+            int b = 0;
+            while (q_start[b + 1] <= row)
+                ++b;
+            extend_one_row(p, q_start, row, b, h, scores, out + r * p->head_dim);
         }
         free(scores);
     }

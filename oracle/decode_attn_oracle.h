@@ -58,6 +58,17 @@ int rl_oracle_decode_attn(const rl_oracle_problem* p, const int32_t* rows,
                           int64_t num_rows, double* out);
 
 /*
+ * Extend (prefill) attention over the paged cache.  q is [T][num_q_heads]
+ * [head_dim] bf16 bits with T = q_start[batch]; rows q_start[b] ..
+ * q_start[b+1]-1 are sequence b's n_b new tokens, whose keys/values are the
+ * last n_b of its seq_lens[b] cached tokens.  Row q_start[b] + i attends
+ * causally to cache tokens 0 .. seq_lens[b] - n_b + i.  out is [T][Hq][D]
+ * fp64.  p->batch, seq_lens, block_table, pools as for decode (p->q is the
+ * [T][Hq][D] array).
+ */
+int rl_oracle_extend_attn(const rl_oracle_problem* p, const int32_t* q_start, double* out);
+
+/*
  * One decode step's K/V cache append (the step before attention): the new
  * token of every sequence b (k_new/v_new [batch][num_kv_heads][head_dim] bf16
  * bits) is written to page block_table[b][L/page_size], slot L%page_size,

@@ -21,10 +21,11 @@ MUTANTS = [
     ("dropped scale", "scores[t] = p->scale * dot;", "scores[t] = dot;"),
     ("flipped score sign", "scores[t] = p->scale * dot;",
      "scores[t] = -p->scale * dot;"),
-    ("interleaved head grouping", "const int kvh = h / G;",
-     "const int kvh = h % p->num_kv_heads;"),
+    ("interleaved head grouping", "attend_prefix(p, qrow, b, h / G, L, scores, dst);",
+     "attend_prefix(p, qrow, b, h % p->num_kv_heads, L, scores, dst);"),
     ("query row of the kv head",
-     "((int64_t)b * p->num_q_heads + h) * D", "((int64_t)b * p->num_q_heads + kvh) * D"),
+     "((int64_t)b * p->num_q_heads + h) * p->head_dim;",
+     "((int64_t)b * p->num_q_heads + h / G) * p->head_dim;"),
     ("slot off by one", "const int slot = t % p->page_size;\n        double dot",
      "const int slot = (t + 1) % p->page_size;\n        double dot"),
     ("every token from logical page 0",
@@ -38,8 +39,8 @@ MUTANTS = [
     ("no normalisation", "const double w = scores[t] / z;",
      "const double w = scores[t];"),
     ("last token dropped from values",
-     "for (int t = 0; t < L; ++t) {\n        const int64_t page = pages[t / p->page_size];\n        const int slot = t % p->page_size;\n        const double w",
-     "for (int t = 0; t < L - 1; ++t) {\n        const int64_t page = pages[t / p->page_size];\n        const int slot = t % p->page_size;\n        const double w"),
+     "for (int t = 0; t < visible; ++t) {\n        const int64_t page = pages[t / p->page_size];\n        const int slot = t % p->page_size;\n        const double w",
+     "for (int t = 0; t < visible - 1; ++t) {\n        const int64_t page = pages[t / p->page_size];\n        const int slot = t % p->page_size;\n        const double w"),
     ("e4m3 exponent bias 8", "mag = ldexp(1.0 + (double)m / 8.0, e - 7);",
      "mag = ldexp(1.0 + (double)m / 8.0, e - 8);"),
     ("e4m3 subnormal scale", "mag = ldexp((double)m / 8.0, -6);",
@@ -60,6 +61,16 @@ MUTANTS = [
      "double q = round((a / ldexp(1.0, e) - 1.0) * 8.0);"),
     ("encoder subnormal step", "const double steps = rint(a * 512.0);",
      "const double steps = rint(a * 256.0);"),
+    ("extend sees its own next token", "const int visible = L - n_new + i + 1;",
+     "const int visible = L - n_new + i + 2 <= L ? L - n_new + i + 2 : L;"),
+    ("extend without causal mask", "const int visible = L - n_new + i + 1;",
+     "const int visible = L;"),
+    ("extend query row of the first new token",
+     "(const uint16_t*)p->q + (row * p->num_q_heads + h) * p->head_dim;",
+     "(const uint16_t*)p->q + ((int64_t)q_start[b] * p->num_q_heads + h) * p->head_dim;"),
+    ("extend kv head of the query head",
+     "attend_prefix(p, qrow, b, h / G, visible, scores, dst);",
+     "attend_prefix(p, qrow, b, h % p->num_kv_heads, visible, scores, dst);"),
 ]
 
 
@@ -74,7 +85,8 @@ def _build(src_text, workdir, name):
     return so_path
 
 
-PIN_FILES = ["test_oracle.py", "test_oracle_append.py", "test_codecs.py"]
+PIN_FILES = ["test_oracle.py", "test_oracle_append.py", "test_oracle_extend.py",
+             "test_codecs.py"]
 
 
 def _run_pins(so_path):
