@@ -101,9 +101,13 @@ def parse_args():
     ap.add_argument("--pmc-calibrate", action="store_true",
                     help="launch one plain copy of %d bytes first, so that a counter "
                          "run can scale FETCH_SIZE/WRITE_SIZE" % COPY_CALIBRATION_BYTES)
-    ap.add_argument("--op", choices=["attention", "append"], default="attention",
-                    help="attention (the decode step, default) or the KV-cache append "
-                         "that precedes it (a separate JSON line with its own metric)")
+    ap.add_argument("--op", choices=["attention", "append", "extend"], default="attention",
+                    help="attention (the decode step, default), the KV-cache append that "
+                         "precedes it, or extend (prefill) attention of --new-tokens per "
+                         "sequence after the workload's cached lengths (separate JSON lines "
+                         "with their own metrics)")
+    ap.add_argument("--new-tokens", type=int, default=512,
+                    help="new tokens per sequence for --op extend")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="turn two rocprofv3 --pmc counter_collection.csv files (FETCH_SIZE, "
                          "WRITE_SIZE) of a --pmc-calibrate run into profiles/traffic.json")
@@ -259,6 +263,48 @@ def bench_append(args, base, stream):
     }
 
 
+def bench_extend(args, dev):
+    """Times K extend-attention launches: every sequence of the workload gets
+    --new-tokens new tokens after its cached length; FLOPs are the causal
+    count 4 * D * Hq * sum over new tokens of the keys they see."""
+    import numpy as np
+    import torch
+    from paper_2512_22492_amd import binding, workloads
+    cfg = dict(workloads.CONFIGS[args.config])
+    seed = cfg.pop("seed")
+    n = args.new_tokens
+    prior = workloads.draw_lengths(np.random.default_rng(seed), cfg["batch"], cfg["lengths"])
+    cfg["lengths"] = [int(x) + n for x in prior]
+    p = workloads.make_problem(args.config + "+extend", seed=seed, device=dev, **cfg)
+    T = n * p.batch
+    gen = torch.Generator(device=dev).manual_seed(seed + 1)
+    q = torch.randn((T, p.num_q_heads, p.head_dim), generator=gen, device=dev).to(torch.bfloat16)
+    q_start = torch.arange(0, T + 1, n, dtype=torch.int32, device=dev)
+    out = torch.empty_like(q)
+    for _ in range(args.warmup):
+        binding.extend_attention(p, q, q_start, n, out)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        binding.extend_attention(p, q, q_start, n, out)
+    torch.cuda.synchronize()
+    s = (time.perf_counter() - t0) / args.steps
+    visible = sum(int(L) * n + n * (n + 1) // 2 for L in prior)
+    flops = 4.0 * p.head_dim * p.num_q_heads * visible
+    tf = flops / s / 1e12
+    return {
+        "metric": "extend (prefill) attention TFLOP/s, causal, 1 GPU",
+        "value": round(tf, 2), "unit": "TFLOP/s", "higher_is_better": True,
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(s * 1e3, 4),
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "%s cached prefixes + %d new tokens per sequence" % (args.config, n),
+                   "batch": p.batch, "num_q_heads": p.num_q_heads,
+                   "num_kv_heads": p.num_kv_heads, "new_tokens": T},
+        "roofline": {"bound": "mfma", "achieved": round(tf, 2), "peak": 2500.0,
+                     "unit": "TFLOP/s", "frac": round(tf / 2500.0, 4)},
+    }
+
+
 def _describe(name):
     from paper_2512_22492_amd import workloads
     return workloads.describe(name)
@@ -287,6 +333,9 @@ def main():
     dev = torch.device("cuda:0")
     print("bench: generating %s (%s)" % (args.config, workloads.describe(args.config)),
           file=sys.stderr, flush=True)
+    if args.op == "extend":
+        print(json.dumps(bench_extend(args, dev)), flush=True)
+        return
     base = workloads.make_config(args.config, device=dev)
     replicas = [base]
     for _ in range(1, max(1, args.replicas)):

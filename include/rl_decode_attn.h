@@ -143,6 +143,34 @@ rl_da_status rl_decode_attn_split_info(const rl_decode_attn* h, int32_t max_page
                                        int32_t* split_tokens, int32_t* num_splits);
 
 /*
+ * Extend (prefill) attention: causal attention of several new tokens per
+ * sequence over the paged cache, for multi-turn continuations and re-prefill
+ * of trajectories (the rollout's multi-turn tool interactions, Sec. 2.1, and
+ * the reassignment of a failed rollout's trajectories, Sec. 5.2.2).  The new
+ * tokens' keys and values must already be in the cache (rl_kv_append or the
+ * caller's own writes): sequence b's n_b = q_start[b+1] - q_start[b] new
+ * tokens are the last n_b of its L_b = seq_lens[b] cached tokens.  Row
+ * q_start[b] + i of q / out (new token i of b) attends to cached tokens
+ * 0 .. L_b - n_b + i:
+ *     out[r,h,:] = sum_t softmax_t(scale * <q[r,h,:], K_b[t,kvh,:]>) V_b[t,kvh,:]
+ * q, out: [T][num_q_heads][head_dim] bf16 with T = q_start[batch]; q_start:
+ * [batch+1] int32 device array, non-decreasing from 0; pools, block_table and
+ * seq_lens as for rl_decode_attn_run.  max_q_per_seq >= every n_b (sizes the
+ * grid).  Preconditions: n_b <= L_b <= max_pages * page_size and the table
+ * entries of pages 0 .. (L_b-1)/page_size in [0, num_pages).  Needs no
+ * handle and no workspace; enqueues one kernel on `stream`.  bf16 pools,
+ * head_dim 128, page_size 16 and Hq/Hkv in {1, 2, 4, 8, 16} only (else
+ * UNSUPPORTED); q, the pools and out 16-byte aligned.
+ */
+rl_da_status rl_extend_attn(const void* q, const int32_t* q_start, int32_t max_q_per_seq,
+                            const void* k_pool, const void* v_pool, const float* k_scale,
+                            const float* v_scale, int64_t num_pages, const int32_t* block_table,
+                            int32_t max_pages, const int32_t* seq_lens, int32_t batch,
+                            int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                            int32_t page_size, int32_t kv_dtype, float scale, void* out,
+                            void* stream);
+
+/*
  * KV-cache append: the step before attention in every decode step (the
  * rollout engine generates one token per sequence per step, Sec. 2.1; the
  * new token's key and value join the paged cache the attention then reads).

@@ -37,6 +37,7 @@ EXPORTED = [
     "rl_decode_attn_workspace_size",
     "rl_decode_attn_check_error",
     "rl_decode_attn_split_info",
+    "rl_extend_attn",
     "rl_kv_append",
     "rl_decode_attn_set_timing_events",
 ]
@@ -101,6 +102,9 @@ def load_library():
     lib.rl_decode_attn_check_error.restype = ctypes.c_int
     lib.rl_decode_attn_split_info.argtypes = [vp, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)]
     lib.rl_decode_attn_split_info.restype = ctypes.c_int
+    lib.rl_extend_attn.argtypes = [vp, vp, i32, vp, vp, vp, vp, i64, vp, i32, vp, i32, i32, i32,
+                                   i32, i32, i32, ctypes.c_float, vp, vp]
+    lib.rl_extend_attn.restype = ctypes.c_int
     lib.rl_kv_append.argtypes = [vp, vp, vp, vp, vp, vp, i64, vp, i32, vp, i32, i32, i32, i32,
                                  i32, vp, vp]
     lib.rl_kv_append.restype = ctypes.c_int
@@ -182,6 +186,29 @@ def rl_decode_attn_split_info(h, max_pages):
     rc = load_library().rl_decode_attn_split_info(h, int(max_pages), ctypes.byref(st),
                                                   ctypes.byref(ns))
     return rc, st.value, ns.value
+
+
+def rl_extend_attn(q, q_start, max_q_per_seq, k_pool, v_pool, k_scale, v_scale, num_pages,
+                   block_table, max_pages, seq_lens, batch, num_q_heads, num_kv_heads,
+                   head_dim=128, page_size=16, kv_dtype=RL_DA_KV_BF16, scale=1.0, out=None,
+                   stream=None) -> int:
+    return load_library().rl_extend_attn(
+        _ptr(q), _ptr(q_start), int(max_q_per_seq), _ptr(k_pool), _ptr(v_pool), _ptr(k_scale),
+        _ptr(v_scale), int(num_pages), _ptr(block_table), int(max_pages), _ptr(seq_lens),
+        int(batch), int(num_q_heads), int(num_kv_heads), int(head_dim), int(page_size),
+        int(kv_dtype), float(scale), _ptr(out), _stream(stream))
+
+
+def extend_attention(p, q, q_start, max_q_per_seq, out, stream=None):
+    """Extend attention of new tokens q [T, Hq, D] (rows q_start[b]..) over
+    problem p's cache (p.seq_lens include the new tokens); raises on error."""
+    dt = RL_DA_KV_BF16 if p.kv_dtype == "bf16" else RL_DA_KV_FP8_E4M3
+    rc = rl_extend_attn(q, q_start, max_q_per_seq, p.k_pool, p.v_pool, p.k_scale, p.v_scale,
+                        p.num_pages, p.block_table, p.max_pages, p.seq_lens, p.batch,
+                        p.num_q_heads, p.num_kv_heads, p.head_dim, p.page_size, dt, p.scale,
+                        out, stream)
+    if rc != RL_DA_OK:
+        raise RLDecodeAttnError(rc, "rl_extend_attn")
 
 
 def rl_kv_append(k_new, v_new, k_pool, v_pool, k_scale, v_scale, num_pages, block_table,

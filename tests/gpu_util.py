@@ -57,11 +57,13 @@ def rne_bf16(x):
         torch.bfloat16).double().numpy()
 
 
-def check_close(got, ref, what=""):
+def check_close(got, ref, what="", extra_abs=0.0):
     """Asserts the official tolerance |err| <= 1e-2 + 1e-2 |ref| and the tight
     one: the bf16 output is within one bf16 ulp of the fp64 reference (plus
     1e-6 absolute for fp32 accumulation), which rounding an fp32 result that
-    carries ~1e-6 relative error guarantees.  Returns error statistics."""
+    carries ~1e-6 relative error guarantees; extra_abs widens the tight bound
+    for paths whose arithmetic carries a known extra error.  Returns error
+    statistics."""
     got = np.asarray(got, dtype=np.float64)
     ref = np.asarray(ref, dtype=np.float64)
     assert got.shape == ref.shape, (got.shape, ref.shape)
@@ -73,7 +75,7 @@ def check_close(got, ref, what=""):
         "%s: |err| %.3g > tolerance at %s (ref %.6g got %.6g)"
         % (what, err[worst], worst, ref[worst], got[worst]))
     ulp = bf16_ulp(ref)
-    tight = ulp + TIGHT_ABS
+    tight = ulp + TIGHT_ABS + extra_abs
     worst = np.unravel_index(np.argmax(err - tight), err.shape)
     assert np.all(err <= tight), (
         "%s: |err| %.3g exceeds one bf16 ulp (%.3g) at %s (ref %.8g got %.8g)"

@@ -1,0 +1,132 @@
+"""GPU extend (prefill) attention against the fp64 oracle: ragged new-token
+counts over ragged cached prefixes for every supported group size, poisoned
+unread memory, causality, and argument checks."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2512_22492_amd import binding as B
+from paper_2512_22492_amd import workloads
+
+from gpu_util import bf16_to_f64, check_close, device
+
+pytestmark = pytest.mark.gpu
+
+
+def extend_problem(new, prior, seed, hq=8, hkv=2):
+    lengths = [a + b for a, b in zip(new, prior)]
+    p = workloads.make_problem("ext", batch=len(new), num_q_heads=hq, num_kv_heads=hkv,
+                               lengths=lengths, seed=seed, pool_factor=1.25).to(device())
+    gen = torch.Generator().manual_seed(seed + 3)
+    q = torch.randn((int(sum(new)), hq, 128), generator=gen).to(torch.bfloat16).to(device())
+    q_start = torch.tensor(np.concatenate([[0], np.cumsum(new)]), dtype=torch.int32,
+                           device=device())
+    return p, q, q_start
+
+
+def run_extend(p, q, q_start, max_new):
+    out = torch.full_like(q, float("nan"))
+    B.extend_attention(p, q, q_start, max_new, out)
+    torch.cuda.synchronize()
+    return out
+
+
+def p_split_bound(p):
+    """The PV MFMA takes each probability as two bf16 terms, so every weight
+    carries up to 2^-18 relative error and the normalisation up to another
+    2^-18: the output may move by 2^-17 * max|V| beyond the bf16 rounding."""
+    return 2.0 ** -17 * float(p.v_pool.float().abs().max())
+
+
+def oracle_extend(p, q, q_start):
+    h = p.host_arrays()
+    return oracle.extend_attention(q.cpu().view(torch.int16).numpy().view(np.uint16),
+                                   q_start.cpu().numpy(), h["k_pool"], h["v_pool"],
+                                   h["block_table"], h["seq_lens"],
+                                   num_kv_heads=p.num_kv_heads, scale=p.scale)
+
+
+CASES = [
+    ([1, 3, 5, 16, 17, 33], [0, 7, 100, 4000, 15, 1]),
+    ([64, 1, 100, 0, 2], [0, 63, 1000, 5, 9]),
+    ([200], [3000]),
+]
+
+
+@pytest.mark.parametrize("hq,hkv", [(8, 2), (4, 4), (8, 4), (16, 2), (32, 2)])
+@pytest.mark.parametrize("case", range(len(CASES)))
+def test_extend_matches_oracle(hq, hkv, case):
+    new, prior = CASES[case]
+    p, q, q_start = extend_problem(new, prior, seed=31 + case, hq=hq, hkv=hkv)
+    got = bf16_to_f64(run_extend(p, q, q_start, max(new)))
+    print(check_close(got, oracle_extend(p, q, q_start), "extend G=%d case %d" % (hq // hkv, case),
+                      extra_abs=p_split_bound(p)))
+
+
+def test_extend_qwen3_8b_shapes_sampled():
+    new, prior = [512, 300, 77, 1], [4096, 8000, 20, 12000]
+    p, q, q_start = extend_problem(new, prior, seed=40, hq=32, hkv=8)
+    got = run_extend(p, q, q_start, max(new))
+    # oracle on a sample of rows: the oracle takes whole sequences, so restrict
+    # each sequence's rows by passing a sub-problem of 4 chosen tokens each
+    h = p.host_arrays()
+    qs = q_start.cpu().numpy()
+    pick = []
+    for b in range(4):
+        n = new[b]
+        for i in sorted({0, n // 2, n - 1}):
+            pick.append((b, i))
+    for b, i in pick:
+        lens = h["seq_lens"].copy()
+        lens[b] = prior[b] + i + 1
+        qrow = q[qs[b] + i:qs[b] + i + 1].cpu().view(torch.int16).numpy().view(np.uint16)
+        ref = oracle.decode_attention(np.repeat(qrow, 4, axis=0), h["k_pool"], h["v_pool"],
+                                      h["block_table"], lens, num_kv_heads=8, scale=p.scale,
+                                      rows=[[b, hh] for hh in range(32)])
+        check_close(bf16_to_f64(got[qs[b] + i]), ref, "row b=%d i=%d" % (b, i),
+                    extra_abs=p_split_bound(p))
+
+
+def test_extend_ignores_unread_memory_and_is_causal():
+    new, prior = [20, 5], [13, 40]
+    p, q, q_start = extend_problem(new, prior, seed=41)
+    base = run_extend(p, q, q_start, 20)
+    bt = p.block_table.cpu().numpy()
+    nan = float("nan")
+    for b, L in enumerate([33, 45]):
+        last, tail = int(bt[b, (L - 1) // 16]), L % 16
+        if tail:
+            p.k_pool[last, :, tail:, :] = nan
+            p.v_pool[last, :, tail:, :] = nan
+    assert torch.equal(run_extend(p, q, q_start, 20).view(torch.int16), base.view(torch.int16))
+    # the last cached token of sequence 0 is visible only to its last new token
+    last, slot = int(bt[0, 32 // 16]), 32 % 16
+    p.k_pool[last, :, slot, :] *= -3.0
+    moved = run_extend(p, q, q_start, 20)
+    assert torch.equal(moved[:19].view(torch.int16), base[:19].view(torch.int16))
+    assert not torch.equal(moved[19].view(torch.int16), base[19].view(torch.int16))
+    assert torch.equal(moved[20:].view(torch.int16), base[20:].view(torch.int16))
+
+
+def test_extend_argument_validation():
+    p, q, q_start = extend_problem([3, 2], [4, 4], seed=42)
+    out = torch.empty_like(q)
+
+    def call(**kw):
+        args = dict(q=q, q_start=q_start, max_q_per_seq=3, k_pool=p.k_pool, v_pool=p.v_pool,
+                    k_scale=None, v_scale=None, num_pages=p.num_pages,
+                    block_table=p.block_table, max_pages=p.max_pages, seq_lens=p.seq_lens,
+                    batch=2, num_q_heads=8, num_kv_heads=2, scale=p.scale, out=out)
+        args.update(kw)
+        return B.rl_extend_attn(**args)
+
+    assert call() == B.RL_DA_OK
+    assert call(q=None) == B.RL_DA_ERR_INVALID_ARG
+    assert call(num_q_heads=7) == B.RL_DA_ERR_INVALID_ARG
+    assert call(out=out.data_ptr() + 2) == B.RL_DA_ERR_INVALID_ARG
+    assert call(k_scale=p.seq_lens) == B.RL_DA_ERR_INVALID_ARG
+    assert call(head_dim=64) == B.RL_DA_ERR_UNSUPPORTED
+    assert call(num_q_heads=6) == B.RL_DA_ERR_UNSUPPORTED
+    assert call(max_q_per_seq=0) == B.RL_DA_OK
+    torch.cuda.synchronize()
