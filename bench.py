@@ -189,10 +189,13 @@ def load_traffic(config, kernel_source_sha):
 
 
 def kernel_source_sha():
+    """sha256 over the sources of the decode kernels (shared header first)."""
     import hashlib
-    path = os.path.join(ROOT, "paper_2512_22492_amd", "csrc", "rl_decode_attn.hip")
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    h = hashlib.sha256()
+    for name in ("rl_common.h", "rl_decode.hip"):
+        with open(os.path.join(ROOT, "paper_2512_22492_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def cpu_baseline(p, rows_per_call=None):

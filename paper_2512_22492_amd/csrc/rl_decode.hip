@@ -1,4 +1,4 @@
-// rl_decode_attn.hip -- paged grouped-query decode attention for gfx950.
+// rl_decode.hip -- decode-step kernels and the handle-based C interface.
 //
 // One decode step of one attention layer (the rollout inner loop of
 // arXiv 2512.22492, Sec. 2.1): out[b,h] = softmax(scale * q[b,h] K_b^T) V_b
@@ -28,33 +28,18 @@
 // All arithmetic is fp32; scores are kept in the log2 domain (scale folded
 // with log2(e)) so that every exponential is one v_exp_f32.
 
-#include <hip/hip_runtime.h>
-
-#include <math.h>
-#include <stdint.h>
 #include <stdlib.h>
 
-#include "rl_decode_attn.h"
+#include "rl_common.h"
+
+using namespace rl_da;
 
 namespace {
 
-constexpr int kHeadDim = 128;
-constexpr int kPageSize = 16;
-constexpr int kWave = 64;
-constexpr int kUnitWaves = 4;                       // wavefronts per work unit
 constexpr int kDefaultSplitTokens = 4096;
 // each wavefront holds its pages' block-table entries one per lane
 constexpr int kMaxSplitTokens = kWave * kUnitWaves * kPageSize;
-constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kSlabBytesBf16 = kPageSize * kHeadDim * 2;
-
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
-typedef float floatx4_t __attribute__((ext_vector_type(4)));
-typedef float floatx2_t __attribute__((ext_vector_type(2)));
-typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
-typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
 
 struct SplitArgs {
     const uint16_t* q;          // bf16 bits [B][Hq][D]
@@ -76,94 +61,6 @@ struct SplitArgs {
     int32_t num_splits;         // ceil(max_pages / split_pages)
     float scale_log2;           // scale * log2(e)
 };
-
-// ------------------------------------------------------------ helpers ---
-
-__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
-__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
-
-// fp32 -> bf16 bits, round to nearest even (quiet NaN kept NaN).
-__device__ __forceinline__ uint32_t f32_to_bf16(float f)
-{
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u)
-        return 0x7fc0u;
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return u >> 16;
-}
-
-__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c)
-{
-    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a),
-                                           __builtin_bit_cast(bf16x2_t, b), c, false);
-}
-
-// DPP lane permutations inside a 16-lane row.  quad_perm [1,0,3,2] and
-// [2,3,0,1] pair lanes within a quad; row_half_mirror pairs the two quads of
-// each 8-lane half; row_mirror pairs the two halves.  Applied in turn they
-// combine all 16 lanes of a row.
-constexpr int kDppQuadXor1 = 0xB1;
-constexpr int kDppQuadXor2 = 0x4E;
-constexpr int kDppRowHalfMirror = 0x141;
-constexpr int kDppRowMirror = 0x140;
-
-template <int CTRL>
-__device__ __forceinline__ float dpp_f32(float v)
-{
-    return __int_as_float(
-        __builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xf, 0xf, false));
-}
-
-__device__ __forceinline__ float row16_sum(float v)
-{
-    v += dpp_f32<kDppQuadXor1>(v);
-    v += dpp_f32<kDppQuadXor2>(v);
-    v += dpp_f32<kDppRowHalfMirror>(v);
-    v += dpp_f32<kDppRowMirror>(v);
-    return v;
-}
-
-__device__ __forceinline__ float row16_max(float v)
-{
-    v = fmaxf(v, dpp_f32<kDppQuadXor1>(v));
-    v = fmaxf(v, dpp_f32<kDppQuadXor2>(v));
-    v = fmaxf(v, dpp_f32<kDppRowHalfMirror>(v));
-    v = fmaxf(v, dpp_f32<kDppRowMirror>(v));
-    return v;
-}
-
-__device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
-
-// Loads with the non-temporal hint: K/V bytes are read exactly once, so they
-// are streamed past the caches rather than kept.
-__device__ __forceinline__ uint4 load_stream16(const uint8_t* p)
-{
-    const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
-    return make_uint4(v.x, v.y, v.z, v.w);
-}
-
-__device__ __forceinline__ uint2 load_stream8(const uint8_t* p)
-{
-    const u32x2_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x2_t*>(p));
-    return make_uint2(v.x, v.y);
-}
-
-// Orders LDS traffic between the lanes of one wavefront (the work-group is
-// a single wavefront, so no s_barrier and no wait on global loads is needed).
-__device__ __forceinline__ void wave_lds_sync()
-{
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
-__device__ __forceinline__ void unpack8(const uint4& w, float (&v)[8])
-{
-    v[0] = bf16_lo(w.x); v[1] = bf16_hi(w.x);
-    v[2] = bf16_lo(w.y); v[3] = bf16_hi(w.y);
-    v[4] = bf16_lo(w.z); v[5] = bf16_hi(w.z);
-    v[6] = bf16_lo(w.w); v[7] = bf16_hi(w.w);
-}
 
 // One wavefront's share of a work unit: pages p0 + wave + 4i, i < count.
 struct WaveTask {
@@ -436,8 +333,6 @@ struct KvFp8 {
 // rescaling, so the rescale and its LDS exchange run only on the rare pages
 // where some head's max moves.  Results are the same up to fp32 rounding: m
 // cancels in acc / l.
-
-constexpr float kMaxSlack = 8.0f;
 
 // Three wavefronts per SIMD: the register budget (168) fits both page buffers
 // and the accumulators without spilling.
@@ -797,311 +692,6 @@ __global__ __launch_bounds__(kWave * kMergeWaves) void merge_splits(MergeArgs a)
         f32_to_bf16(x0 * inv) | (f32_to_bf16(x1 * inv) << 16);
 }
 
-// ---------------------------------------------------- extend attention ---
-//
-// Causal attention of each sequence's n_b new tokens (already appended: the
-// last n_b of its L_b cached tokens).  A work unit is one work-group of four
-// wavefronts for (sequence b, kv head, tile of 64/G new tokens); wavefront w
-// owns 16/G of the tile's tokens and all G query heads of the kv head: 16
-// query rows, row m = (token m / G, head m % G).  Every K/V page the tile can
-// see is loaded once into LDS for the four wavefronts (K as [token][dim], V
-// transposed to [dim][token]); each wavefront then forms its 16x16 score tile
-// with four v_mfma_f32_16x16x32_bf16 (as the decode kernel), applies the
-// causal mask where a page crosses a query position, keeps an online softmax
-// per row, and accumulates O += P V with v_mfma_f32_16x16x16_bf16 over eight
-// 16-dim blocks.  P goes to the PV MFMA as two bf16 terms (hi + lo), so the
-// value sum keeps fp32-level accuracy; l sums the same fp32 probabilities.
-
-constexpr int kExtendRows = 16;                   // query rows per wavefront
-constexpr int kKRowPad = 8;                       // bf16 elements of row padding
-constexpr int kVtRow = kPageSize + 4;             // [dim][token] row, padded
-
-struct ExtendArgs {
-    const uint16_t* q;          // bf16 [T][Hq][D]
-    const int32_t* q_start;     // [B+1]
-    const uint8_t* k_pool;
-    const uint8_t* v_pool;
-    const int32_t* block_table;
-    const int32_t* seq_lens;
-    uint16_t* out;              // bf16 [T][Hq][D]
-    int32_t num_q_heads;
-    int32_t num_kv_heads;
-    int32_t max_pages;
-    int32_t num_tiles;          // ceil(max_q_per_seq / tile tokens)
-    float scale_log2;
-};
-
-template <int G>
-__global__ __launch_bounds__(kWave * kUnitWaves) void extend_bf16(ExtendArgs a)
-{
-    static_assert(G >= 1 && G <= 16 && 16 % G == 0, "16 rows per wavefront hold whole groups");
-    constexpr int kTokPerWave = kExtendRows / G;
-    constexpr int kTileTok = kUnitWaves * kTokPerWave;
-    __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][kPageSize][kHeadDim + kKRowPad];
-    __shared__ __attribute__((aligned(16))) uint16_t vt_lds[2][kHeadDim][kVtRow];
-    __shared__ __attribute__((aligned(16))) uint16_t p_lds[kUnitWaves][2][kExtendRows][kVtRow];
-
-    const int tile = blockIdx.x % a.num_tiles;
-    const int bk = blockIdx.x / a.num_tiles;
-    const int kvh = bk % a.num_kv_heads;
-    const int b = bk / a.num_kv_heads;
-    const int q0 = a.q_start[b];
-    // lengths clamped to what the table row can hold, new tokens to the length
-    const int L = min(a.seq_lens[b], a.max_pages * kPageSize);
-    const int n_new = min(a.q_start[b + 1] - q0, L);
-    const int tok0 = tile * kTileTok;
-    if (tok0 >= n_new)
-        return;
-    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-    const int n = lane & 15, kg = lane >> 4;
-    const int h0 = kvh * G;
-    const int base_pos = L - n_new;  // position of new token 0
-
-    // Query operand rows: lane holds row m = lane % 16 for the MFMA A operand.
-    uint4 qa[4];
-    {
-        const int m = lane & 15;
-        const int qi = tok0 + wave * kTokPerWave + m / G;
-        const bool real = qi < n_new;
-        const uint16_t* qrow =
-            a.q + ((int64_t)(q0 + (real ? qi : 0)) * a.num_q_heads + h0 + m % G) * kHeadDim;
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-            qa[i] = real ? *reinterpret_cast<const uint4*>(qrow + 32 * i + 8 * kg)
-                         : make_uint4(0, 0, 0, 0);
-    }
-    // Rows this lane holds in the C layout: m = 4kg + j.
-    int row_pos[4];
-    bool row_real[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int m = 4 * kg + j;
-        const int qi = tok0 + wave * kTokPerWave + m / G;
-        row_real[j] = qi < n_new;
-        row_pos[j] = base_pos + qi;
-    }
-    const int tile_last = min(tok0 + kTileTok, n_new) - 1;
-    const int npages = (base_pos + tile_last) / kPageSize + 1;  // pages the tile sees
-    const int first_masked_page = (base_pos + tok0) / kPageSize;
-
-    float m_run[4], lsum[4];
-    floatx4_t o[8];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        m_run[j] = -INFINITY;
-        lsum[j] = 0.0f;
-    }
-#pragma unroll
-    for (int nb = 0; nb < 8; ++nb)
-        o[nb] = floatx4_t{0.0f, 0.0f, 0.0f, 0.0f};
-
-    // Staging: thread t moves 16 bytes of K and of V: token t/16, dims 8(t%16)..+8.
-    const int st_tok = threadIdx.x / 16, st_dim = (threadIdx.x % 16) * 8;
-    const int32_t* bt = a.block_table + (int64_t)b * a.max_pages;
-    auto fetch = [&](int j, uint4& kr, uint4& vr) {
-        const int64_t page = bt[j];
-        const int64_t off = ((page * a.num_kv_heads + kvh) * kPageSize + st_tok) * kHeadDim + st_dim;
-        kr = load_stream16(a.k_pool + 2 * off);
-        vr = load_stream16(a.v_pool + 2 * off);
-    };
-    uint4 kr, vr;
-    fetch(0, kr, vr);
-
-    for (int j = 0; j < npages; ++j) {
-        const int buf = j & 1;
-        // slots past the sequence end may hold NaN: they must not reach P.V
-        if (j * kPageSize + st_tok >= L) {
-            kr = make_uint4(0, 0, 0, 0);
-            vr = make_uint4(0, 0, 0, 0);
-        }
-        *reinterpret_cast<uint4*>(&k_lds[buf][st_tok][st_dim]) = kr;
-        {
-            const uint32_t w[4] = {vr.x, vr.y, vr.z, vr.w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                vt_lds[buf][st_dim + 2 * e][st_tok] = (uint16_t)(w[e] & 0xffffu);
-                vt_lds[buf][st_dim + 2 * e + 1][st_tok] = (uint16_t)(w[e] >> 16);
-            }
-        }
-        if (j + 1 < npages)
-            fetch(j + 1, kr, vr);
-        __syncthreads();
-
-        // scores S[row 4kg+jj][token n]
-        floatx4_t sacc = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const uint4 kb = *reinterpret_cast<const uint4*>(&k_lds[buf][n][32 * i + 8 * kg]);
-            sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                __builtin_bit_cast(bf16x8_t, qa[i]), __builtin_bit_cast(bf16x8_t, kb), sacc,
-                0, 0, 0);
-        }
-        const int key = j * kPageSize + n;
-        float s[4];
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj) {
-            float x = sacc[jj] * a.scale_log2;
-            if (j >= first_masked_page)
-                x = key <= row_pos[jj] ? x : -INFINITY;
-            s[jj] = row_real[jj] ? x : 0.0f;  // rows past the tile's tokens stay finite
-        }
-        float mx[4];
-        bool grow_any = false;
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj) {
-            mx[jj] = row16_max(s[jj]);   // finite: key 0 is visible to every row
-            grow_any |= mx[jj] > m_run[jj] + kMaxSlack;
-        }
-        if (__any(grow_any)) {
-#pragma unroll
-            for (int jj = 0; jj < 4; ++jj) {
-                const float m_new = mx[jj] > m_run[jj] + kMaxSlack ? mx[jj] : m_run[jj];
-                const float alpha = exp2_fast(m_run[jj] - m_new);
-                m_run[jj] = m_new;
-                lsum[jj] *= alpha;
-#pragma unroll
-                for (int nb = 0; nb < 8; ++nb)
-                    o[nb][jj] *= alpha;
-            }
-        }
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj) {
-            const float p = exp2_fast(s[jj] - m_run[jj]);
-            lsum[jj] += p;
-            const uint32_t hi = f32_to_bf16(p);
-            const float rest = p - __uint_as_float(hi << 16);
-            p_lds[wave][0][4 * kg + jj][n] = (uint16_t)hi;
-            p_lds[wave][1][4 * kg + jj][n] = (uint16_t)f32_to_bf16(rest);
-        }
-        wave_lds_sync();
-        const uint2 ph = *reinterpret_cast<const uint2*>(&p_lds[wave][0][n][4 * kg]);
-        const uint2 pl = *reinterpret_cast<const uint2*>(&p_lds[wave][1][n][4 * kg]);
-        wave_lds_sync();
-#pragma unroll
-        for (int nb = 0; nb < 8; ++nb) {
-            const uint2 vb = *reinterpret_cast<const uint2*>(&vt_lds[buf][16 * nb + n][4 * kg]);
-            o[nb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(
-                __builtin_bit_cast(bf16x4_t, ph), __builtin_bit_cast(bf16x4_t, vb), o[nb], 0, 0, 0);
-            o[nb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(
-                __builtin_bit_cast(bf16x4_t, pl), __builtin_bit_cast(bf16x4_t, vb), o[nb], 0, 0, 0);
-        }
-    }
-
-    // out[row] = O[row] / l[row]; lane holds rows 4kg+jj, dims 16nb + n.
-#pragma unroll
-    for (int jj = 0; jj < 4; ++jj) {
-        const float l = row16_sum(lsum[jj]);
-        if (!row_real[jj])
-            continue;
-        const int m = 4 * kg + jj;
-        const int qi = tok0 + wave * kTokPerWave + m / G;
-        uint16_t* orow = a.out + ((int64_t)(q0 + qi) * a.num_q_heads + h0 + m % G) * kHeadDim;
-        const float inv = 1.0f / l;
-#pragma unroll
-        for (int nb = 0; nb < 8; ++nb)
-            orow[16 * nb + n] = (uint16_t)f32_to_bf16(o[nb][jj] * inv);
-    }
-}
-
-// --------------------------------------------------------- KV append ---
-//
-// One work-group of two wavefronts per (sequence, kv head): wavefront 0 appends
-// the key, wavefront 1 the value.  Lane l owns dims 2l and 2l+1.
-
-struct AppendArgs {
-    const uint16_t* k_new;      // bf16 bits [B][Hkv][D]
-    const uint16_t* v_new;
-    uint8_t* k_pool;
-    uint8_t* v_pool;
-    float* k_scale;
-    float* v_scale;
-    const int32_t* block_table;
-    const int32_t* seq_lens;
-    int32_t* dev_error;         // may be null
-    int64_t num_pages;
-    int32_t num_kv_heads;
-    int32_t max_pages;
-};
-
-__device__ __forceinline__ float wave_max(float v)
-{
-    v = row16_max(v);
-    v = fmaxf(v, __shfl_xor(v, 16));
-    v = fmaxf(v, __shfl_xor(v, 32));
-    return v;
-}
-
-// Two fp32 values to two e4m3 codes (round to nearest even) in the low 16 bits.
-__device__ __forceinline__ uint32_t e4m3_pair(float a, float b)
-{
-    return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false) & 0xffffu;
-}
-
-__device__ __forceinline__ float clamp448(float v)
-{
-    // comparisons, not fminf/fmaxf, so that a NaN passes through unchanged
-    return v > 448.0f ? 448.0f : (v < -448.0f ? -448.0f : v);
-}
-
-template <bool FP8>
-__global__ __launch_bounds__(2 * kWave) void kv_append_kernel(AppendArgs a)
-{
-    const int b = blockIdx.x / a.num_kv_heads;
-    const int kvh = blockIdx.x % a.num_kv_heads;
-    const int which = threadIdx.x / kWave;  // 0: key, 1: value
-    const int lane = threadIdx.x % kWave;
-    const int L = a.seq_lens[b];
-    if (L < 0)
-        return;
-    if (L >= a.max_pages * kPageSize) {
-        if (a.dev_error != nullptr && threadIdx.x == 0 && kvh == 0)
-            atomicOr(a.dev_error, RL_DA_DEVERR_LENGTH_TOO_LONG);
-        return;
-    }
-    const int32_t page = a.block_table[(int64_t)b * a.max_pages + L / kPageSize];
-    if (page < 0 || (int64_t)page >= a.num_pages) {
-        if (a.dev_error != nullptr && threadIdx.x == 0)
-            atomicOr(a.dev_error, RL_DA_DEVERR_PAGE_OUT_OF_RANGE);
-        return;
-    }
-    const int slot = L % kPageSize;
-    const int64_t slab = (int64_t)page * a.num_kv_heads + kvh;
-    const uint16_t* src = (which ? a.v_new : a.k_new) + ((int64_t)b * a.num_kv_heads + kvh) * kHeadDim;
-    const uint32_t bits = *reinterpret_cast<const uint32_t*>(src + 2 * lane);
-    uint8_t* pool = which ? a.v_pool : a.k_pool;
-    if (!FP8) {
-        *reinterpret_cast<uint32_t*>(pool + (slab * kPageSize + slot) * kHeadDim * 2 + 4 * lane) =
-            bits;
-        return;
-    }
-    const float x0 = bf16_lo(bits), x1 = bf16_hi(bits);
-    const float absmax = wave_max(fmaxf(fabsf(x0), fabsf(x1)));
-    const float wanted = absmax > 0.0f ? absmax / 448.0f : 1.0f;
-    float* scale = (which ? a.v_scale : a.k_scale) + slab;
-    uint8_t* codes = pool + slab * kPageSize * kHeadDim;
-    float s_new = wanted;
-    if (slot != 0) {
-        const float s_old = *scale;
-        s_new = wanted > s_old ? wanted : s_old;
-        if (s_new != s_old) {
-            // re-encode the slab's earlier slots at the grown scale
-            const float ratio = s_old / s_new;
-            uint32_t* words = reinterpret_cast<uint32_t*>(codes);
-            for (int w = lane; w < slot * kHeadDim / 4; w += kWave) {
-                const uint32_t c = words[w];
-                const floatx2_t lo = __builtin_amdgcn_cvt_pk_f32_fp8(c, false);
-                const floatx2_t hi = __builtin_amdgcn_cvt_pk_f32_fp8(c, true);
-                words[w] = e4m3_pair(lo.x * ratio, lo.y * ratio) |
-                           (e4m3_pair(hi.x * ratio, hi.y * ratio) << 16);
-            }
-        }
-    }
-    const uint32_t pair = e4m3_pair(clamp448(x0 / s_new), clamp448(x1 / s_new));
-    *reinterpret_cast<uint16_t*>(codes + slot * kHeadDim + 2 * lane) = (uint16_t)pair;
-    if (lane == 0)
-        *scale = s_new;
-}
-
 // ------------------------------------------------------------ dispatch ---
 
 typedef void (*SplitKernel)(SplitArgs);
@@ -1207,8 +797,6 @@ size_t workspace_bytes_for(const rl_da_config* cfg, int max_splits)
 {
     return partials_bytes(cfg, max_splits) + 256;
 }
-
-bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 }  // namespace
 
@@ -1378,111 +966,6 @@ rl_da_status rl_decode_attn_run(rl_decode_attn* h, const void* q, const void* k_
             return RL_DA_ERR_HIP;
     }
     return RL_DA_OK;
-}
-
-rl_da_status rl_kv_append(const void* k_new, const void* v_new, void* k_pool, void* v_pool,
-                          float* k_scale, float* v_scale, int64_t num_pages,
-                          const int32_t* block_table, int32_t max_pages,
-                          const int32_t* seq_lens, int32_t batch, int32_t num_kv_heads,
-                          int32_t head_dim, int32_t page_size, int32_t kv_dtype,
-                          int32_t* device_error, void* stream)
-{
-    if (k_new == nullptr || v_new == nullptr || k_pool == nullptr || v_pool == nullptr ||
-        block_table == nullptr || seq_lens == nullptr)
-        return RL_DA_ERR_INVALID_ARG;
-    if (batch < 0 || num_kv_heads <= 0 || max_pages < 1 || num_pages < 1)
-        return RL_DA_ERR_INVALID_ARG;
-    if (kv_dtype != RL_DA_KV_BF16 && kv_dtype != RL_DA_KV_FP8_E4M3)
-        return RL_DA_ERR_INVALID_ARG;
-    if (head_dim != kHeadDim || page_size != kPageSize)
-        return RL_DA_ERR_UNSUPPORTED;
-    if (!aligned16(k_new) || !aligned16(v_new) || !aligned16(k_pool) || !aligned16(v_pool))
-        return RL_DA_ERR_INVALID_ARG;
-    const bool fp8 = kv_dtype == RL_DA_KV_FP8_E4M3;
-    if (fp8 != (k_scale != nullptr) || fp8 != (v_scale != nullptr))
-        return RL_DA_ERR_INVALID_ARG;
-    if (batch == 0)
-        return RL_DA_OK;
-    const int64_t blocks = (int64_t)batch * num_kv_heads;
-    if (blocks > INT32_MAX)
-        return RL_DA_ERR_UNSUPPORTED;
-    AppendArgs aa;
-    aa.k_new = (const uint16_t*)k_new;
-    aa.v_new = (const uint16_t*)v_new;
-    aa.k_pool = (uint8_t*)k_pool;
-    aa.v_pool = (uint8_t*)v_pool;
-    aa.k_scale = k_scale;
-    aa.v_scale = v_scale;
-    aa.block_table = block_table;
-    aa.seq_lens = seq_lens;
-    aa.dev_error = device_error;
-    aa.num_pages = num_pages;
-    aa.num_kv_heads = num_kv_heads;
-    aa.max_pages = max_pages;
-    hipStream_t st = (hipStream_t)stream;
-    if (fp8)
-        hipLaunchKernelGGL(kv_append_kernel<true>, dim3((unsigned)blocks), dim3(2 * kWave), 0,
-                           st, aa);
-    else
-        hipLaunchKernelGGL(kv_append_kernel<false>, dim3((unsigned)blocks), dim3(2 * kWave), 0,
-                           st, aa);
-    return hipGetLastError() == hipSuccess ? RL_DA_OK : RL_DA_ERR_HIP;
-}
-
-rl_da_status rl_extend_attn(const void* q, const int32_t* q_start, int32_t max_q_per_seq,
-                            const void* k_pool, const void* v_pool, const float* k_scale,
-                            const float* v_scale, int64_t num_pages, const int32_t* block_table,
-                            int32_t max_pages, const int32_t* seq_lens, int32_t batch,
-                            int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
-                            int32_t page_size, int32_t kv_dtype, float scale, void* out,
-                            void* stream)
-{
-    if (q == nullptr || q_start == nullptr || k_pool == nullptr || v_pool == nullptr ||
-        block_table == nullptr || seq_lens == nullptr || out == nullptr)
-        return RL_DA_ERR_INVALID_ARG;
-    if (batch < 0 || max_q_per_seq < 0 || num_q_heads <= 0 || num_kv_heads <= 0 ||
-        num_q_heads % num_kv_heads != 0 || max_pages < 1 || num_pages < 1 || !isfinite(scale))
-        return RL_DA_ERR_INVALID_ARG;
-    if (kv_dtype != RL_DA_KV_BF16 && kv_dtype != RL_DA_KV_FP8_E4M3)
-        return RL_DA_ERR_INVALID_ARG;
-    if ((k_scale != nullptr) != (kv_dtype == RL_DA_KV_FP8_E4M3) ||
-        (v_scale != nullptr) != (kv_dtype == RL_DA_KV_FP8_E4M3))
-        return RL_DA_ERR_INVALID_ARG;
-    if (!aligned16(q) || !aligned16(k_pool) || !aligned16(v_pool) || !aligned16(out))
-        return RL_DA_ERR_INVALID_ARG;
-    const int G = num_q_heads / num_kv_heads;
-    if (head_dim != kHeadDim || page_size != kPageSize || kv_dtype != RL_DA_KV_BF16 ||
-        (G != 1 && G != 2 && G != 4 && G != 8 && G != 16))
-        return RL_DA_ERR_UNSUPPORTED;
-    if (batch == 0 || max_q_per_seq == 0)
-        return RL_DA_OK;
-    const int tile_tok = kUnitWaves * kExtendRows / G;
-    ExtendArgs ea;
-    ea.q = (const uint16_t*)q;
-    ea.q_start = q_start;
-    ea.k_pool = (const uint8_t*)k_pool;
-    ea.v_pool = (const uint8_t*)v_pool;
-    ea.block_table = block_table;
-    ea.seq_lens = seq_lens;
-    ea.out = (uint16_t*)out;
-    ea.num_q_heads = num_q_heads;
-    ea.num_kv_heads = num_kv_heads;
-    ea.max_pages = max_pages;
-    ea.num_tiles = (max_q_per_seq + tile_tok - 1) / tile_tok;
-    ea.scale_log2 = scale * kLog2e;
-    const int64_t blocks = (int64_t)batch * num_kv_heads * ea.num_tiles;
-    if (blocks > INT32_MAX)
-        return RL_DA_ERR_UNSUPPORTED;
-    hipStream_t st = (hipStream_t)stream;
-    const dim3 grid((unsigned)blocks), block(kWave * kUnitWaves);
-    switch (G) {
-    case 1: hipLaunchKernelGGL(extend_bf16<1>, grid, block, 0, st, ea); break;
-    case 2: hipLaunchKernelGGL(extend_bf16<2>, grid, block, 0, st, ea); break;
-    case 4: hipLaunchKernelGGL(extend_bf16<4>, grid, block, 0, st, ea); break;
-    case 8: hipLaunchKernelGGL(extend_bf16<8>, grid, block, 0, st, ea); break;
-    default: hipLaunchKernelGGL(extend_bf16<16>, grid, block, 0, st, ea); break;
-    }
-    return hipGetLastError() == hipSuccess ? RL_DA_OK : RL_DA_ERR_HIP;
 }
 
 rl_da_status rl_decode_attn_set_timing_events(rl_decode_attn* h, void* split_begin,
