@@ -85,14 +85,17 @@ typedef enum { RL_DA_KV_BF16 = 0, RL_DA_KV_FP8_E4M3 = 1 } rl_da_kv_dtype;
 
 typedef struct {
     int32_t num_q_heads;       /* Hq; a multiple of num_kv_heads               */
-    int32_t num_kv_heads;      /* Hkv; Hq / Hkv in {1, 2, 4, 8}                 */
+    int32_t num_kv_heads;      /* Hkv; Hq / Hkv in {1, 2, 4, 8}                */
     int32_t head_dim;          /* 128                                         */
     int32_t page_size;         /* tokens per page: 16                         */
     int32_t max_batch;         /* largest batch a run() may pass (>= 1)       */
     int32_t max_pages_per_seq; /* largest block-table width a run() may pass  */
     int32_t kv_dtype;          /* rl_da_kv_dtype                              */
-    int32_t split_tokens;      /* tokens per split-K work unit; 0 = 512;      */
-                               /* a multiple of page_size, at most 1024       */
+    int32_t split_tokens;      /* tokens per split-K work unit: a multiple of */
+                               /* page_size, at most 4096; 0 = the longest of */
+                               /* 4096, 2048, 1024, 512 that cuts max_batch   */
+                               /* sequences of max_pages_per_seq pages into   */
+                               /* >= 256 units (a per-handle constant)        */
     uint32_t flags;            /* RL_DA_CHECKED | RL_DA_SCORES_ON_VALU or 0   */
 } rl_da_config;
 

@@ -37,6 +37,10 @@ using namespace rl_da;
 namespace {
 
 constexpr int kDefaultSplitTokens = 4096;
+constexpr int kMinDefaultSplitTokens = 512;
+// The default split is the longest that still cuts a full-capacity batch into
+// this many work units (enough to spread over the chip).
+constexpr int64_t kMinDefaultUnits = 256;
 // each wavefront holds its pages' block-table entries one per lane
 constexpr int kMaxSplitTokens = kWave * kUnitWaves * kPageSize;
 constexpr int kSlabBytesBf16 = kPageSize * kHeadDim * 2;
@@ -336,13 +340,26 @@ struct KvFp8 {
 
 // Three wavefronts per SIMD: the register budget (168) fits both page buffers
 // and the accumulators without spilling.
+// Rows of the 16-row query tile that hold a query head: every 4th row for
+// G <= 4 (one score per lane of the first G lane groups), every 2nd row for
+// G = 8 (two scores per lane).
+template <int G>
+struct ScoreRows {
+    static constexpr int kStep = G > 4 ? 2 : 4;       // head g sits in row kStep * g
+    static constexpr int kPerLane = 4 / kStep;       // scores per lane
+    static constexpr int kLdsHeads = G > 4 ? 8 : 4;  // p/alpha entries per token in LDS
+};
+
 template <int G, bool CHECKED, typename KV>
 __global__ __launch_bounds__(kWave * kUnitWaves)
-__attribute__((amdgpu_waves_per_eu(3))) void split_mfma(SplitArgs a)
+__attribute__((amdgpu_waves_per_eu(G > 4 ? 2 : 3))) void split_mfma(SplitArgs a)
 {
-    static_assert(G >= 1 && G <= 4, "MFMA score tile packs at most 4 query heads");
-    __shared__ __attribute__((aligned(16))) float lds_p_all[kUnitWaves][kPageSize * 4];
-    __shared__ __attribute__((aligned(16))) float lds_alpha_all[kUnitWaves][4];
+    static_assert(G == 1 || G == 2 || G == 4 || G == 8, "query group of 1, 2, 4 or 8 heads");
+    using SR = ScoreRows<G>;
+    constexpr int kE = SR::kPerLane;
+    constexpr int kH = SR::kLdsHeads;
+    __shared__ __attribute__((aligned(16))) float lds_p_all[kUnitWaves][kPageSize * kH];
+    __shared__ __attribute__((aligned(16))) float lds_alpha_all[kUnitWaves][kH];
     __shared__ __attribute__((aligned(16))) UnitShared<G> sh;
 
     WaveTask t;
@@ -351,7 +368,7 @@ __attribute__((amdgpu_waves_per_eu(3))) void split_mfma(SplitArgs a)
         write_zero_rows<G>(a, t);
         return;
     }
-    float* lds_p = lds_p_all[t.wave];          // [token][g]
+    float* lds_p = lds_p_all[t.wave];          // [token][head]
     float* lds_alpha = lds_alpha_all[t.wave];
 
     const int lane = t.lane;
@@ -367,12 +384,12 @@ __attribute__((amdgpu_waves_per_eu(3))) void split_mfma(SplitArgs a)
         my_vscale = a.v_scale[slab];
     }
 
-    // Query tile: rows 4g hold query head g, every other row is zero.
+    // Query tile: row kStep*g holds query head g, every other row is zero.
     uint4 qa[4];
     {
         const int row = lane & 15;
-        const int g = row >> 2;
-        const bool has = (row & 3) == 0 && g < G;
+        const int g = row / SR::kStep;
+        const bool has = row % SR::kStep == 0 && g < G;
         const uint16_t* qrow =
             a.q + ((int64_t)t.b * a.num_q_heads + h0 + (has ? g : 0)) * kHeadDim;
 #pragma unroll
@@ -380,9 +397,18 @@ __attribute__((amdgpu_waves_per_eu(3))) void split_mfma(SplitArgs a)
             qa[i] = has ? *reinterpret_cast<const uint4*>(qrow + KV::q_dim(i, kg))
                         : make_uint4(0, 0, 0, 0);
     }
+    // Head of this lane's e-th score: tile row 4kg + e*kStep.
+    int head[kE];
+#pragma unroll
+    for (int e = 0; e < kE; ++e)
+        head[e] = (4 * kg + e * SR::kStep) / SR::kStep;
 
-    float m = -INFINITY;      // reference max of row g = lane/16 (log2 units)
-    float lsum = 0.0f;        // this lane's share of the running sum
+    float m[kE], lsum[kE];    // reference max (log2 units) and this lane's share of l
+#pragma unroll
+    for (int e = 0; e < kE; ++e) {
+        m[e] = -INFINITY;
+        lsum[e] = 0.0f;
+    }
     float acc[G][8];
 #pragma unroll
     for (int g = 0; g < G; ++g)
@@ -409,39 +435,63 @@ __attribute__((amdgpu_waves_per_eu(3))) void split_mfma(SplitArgs a)
         float sl = a.scale_log2;
         if (KV::kScaled)
             sl *= __int_as_float(__builtin_amdgcn_readlane(__float_as_int(my_kscale), i));
-        float s = sacc[0] * sl;
-        s = (n < valid) ? s : -INFINITY;
-        const float mx = row16_max(s);  // finite: token 0 is valid
-        const bool grow = mx > m + kMaxSlack;
+        float s[kE], mx[kE];
+        bool grow = false;
+#pragma unroll
+        for (int e = 0; e < kE; ++e) {
+            s[e] = (n < valid) ? sacc[e * SR::kStep] * sl : -INFINITY;
+            mx[e] = row16_max(s[e]);  // finite: token 0 is valid
+            grow |= mx[e] > m[e] + kMaxSlack;
+        }
         if (__any(grow)) {
-            const float m_new = grow ? mx : m;
-            const float alpha = exp2_fast(m - m_new);  // 0 on the first page
-            lsum *= alpha;
-            m = m_new;
-            if (n == 0)
-                lds_alpha[kg] = alpha;
+#pragma unroll
+            for (int e = 0; e < kE; ++e) {
+                const float m_new = mx[e] > m[e] + kMaxSlack ? mx[e] : m[e];
+                const float alpha = exp2_fast(m[e] - m_new);  // 0 on the first page
+                lsum[e] *= alpha;
+                m[e] = m_new;
+                if (n == 0)
+                    lds_alpha[head[e]] = alpha;
+            }
             wave_lds_sync();
-            const float4 al = *reinterpret_cast<const float4*>(lds_alpha);
+            float alv[kH];
+#pragma unroll
+            for (int q4 = 0; q4 < kH / 4; ++q4) {
+                const float4 al = *reinterpret_cast<const float4*>(&lds_alpha[4 * q4]);
+                alv[4 * q4] = al.x;
+                alv[4 * q4 + 1] = al.y;
+                alv[4 * q4 + 2] = al.z;
+                alv[4 * q4 + 3] = al.w;
+            }
             wave_lds_sync();
-            const float alv[4] = {al.x, al.y, al.z, al.w};
 #pragma unroll
             for (int g = 0; g < G; ++g)
 #pragma unroll
                 for (int d = 0; d < 8; ++d)
                     acc[g][d] *= alv[g];
         }
-        const float pexp = exp2_fast(s - m);
-        lsum += pexp;
-        float pv_scale = pexp;
+        float vs = 1.0f;
         if (KV::kScaled)
-            pv_scale *= __int_as_float(__builtin_amdgcn_readlane(__float_as_int(my_vscale), i));
-
-        lds_p[n * 4 + kg] = pv_scale;
+            vs = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(my_vscale), i));
+#pragma unroll
+        for (int e = 0; e < kE; ++e) {
+            const float pexp = exp2_fast(s[e] - m[e]);
+            lsum[e] += pexp;
+            lds_p[n * kH + head[e]] = pexp * vs;
+        }
         wave_lds_sync();
-        float4 pv[4];
+        float pv[4][kH];
 #pragma unroll
         for (int k = 0; k < 4; ++k)
-            pv[k] = *reinterpret_cast<const float4*>(&lds_p[(4 * k + r) * 4]);
+#pragma unroll
+            for (int q4 = 0; q4 < kH / 4; ++q4) {
+                const float4 x =
+                    *reinterpret_cast<const float4*>(&lds_p[(4 * k + r) * kH + 4 * q4]);
+                pv[k][4 * q4] = x.x;
+                pv[k][4 * q4 + 1] = x.y;
+                pv[k][4 * q4 + 2] = x.z;
+                pv[k][4 * q4 + 3] = x.w;
+            }
         wave_lds_sync();
 
         if (valid < kPageSize) {
@@ -454,12 +504,11 @@ __attribute__((amdgpu_waves_per_eu(3))) void split_mfma(SplitArgs a)
         for (int k = 0; k < 4; ++k) {
             float v[8];
             KV::values(buf, k, v);
-            const float pg[4] = {pv[k].x, pv[k].y, pv[k].z, pv[k].w};
 #pragma unroll
             for (int g = 0; g < G; ++g)
 #pragma unroll
                 for (int d = 0; d < 8; ++d)
-                    acc[g][d] = fmaf(pg[g], v[d], acc[g][d]);
+                    acc[g][d] = fmaf(pv[k][g], v[d], acc[g][d]);
         }
     };
 
@@ -477,12 +526,16 @@ __attribute__((amdgpu_waves_per_eu(3))) void split_mfma(SplitArgs a)
             v += __shfl_xor(v, 32);
             acc[g][d] = v;
         }
-    const float l_row = row16_sum(lsum);  // l of query head g = lane/16
-
+    // Lane group kg holds m and l of heads head[e]; its value lanes (r = kg)
+    // stash those heads.
 #pragma unroll
-    for (int g = 0; g < G; ++g)
-        if (r == g)
-            stash_state<G>(sh, t.wave, g, c, acc[g], m, l_row);
+    for (int e = 0; e < kE; ++e) {
+        const float l_row = row16_sum(lsum[e]);
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+            if (g == head[e])
+                stash_state<G>(sh, t.wave, g, c, acc[g], m[e], l_row);
+    }
     __syncthreads();
     merge_unit<G>(a, t, sh);
 }
@@ -699,14 +752,10 @@ typedef void (*SplitKernel)(SplitArgs);
 template <int G, bool CHECKED>
 SplitKernel pick(bool fp8, bool mfma)
 {
-    if constexpr (G <= 4) {
-        if (fp8)
-            return split_mfma<G, CHECKED, KvFp8>;
-        if (mfma)
-            return split_mfma<G, CHECKED, KvBf16>;
-    }
     if (fp8)
-        return nullptr;  // fp8 pools are served through the MFMA score tile only
+        return split_mfma<G, CHECKED, KvFp8>;  // fp8 pools use the MFMA score tile only
+    if (mfma)
+        return split_mfma<G, CHECKED, KvBf16>;
     return split_valu_bf16<G, CHECKED>;
 }
 
@@ -771,10 +820,20 @@ rl_da_status check_config(const rl_da_config* cfg, int* split_tokens, int* split
     if (cfg->head_dim != kHeadDim || cfg->page_size != kPageSize ||
         (G != 1 && G != 2 && G != 4 && G != 8))
         return RL_DA_ERR_UNSUPPORTED;
-    if (cfg->kv_dtype == RL_DA_KV_FP8_E4M3 &&
-        (G > 4 || (cfg->flags & RL_DA_SCORES_ON_VALU) != 0))
+    if (cfg->kv_dtype == RL_DA_KV_FP8_E4M3 && (cfg->flags & RL_DA_SCORES_ON_VALU) != 0)
         return RL_DA_ERR_UNSUPPORTED;
-    const int st = cfg->split_tokens == 0 ? kDefaultSplitTokens : cfg->split_tokens;
+    int st = cfg->split_tokens;
+    if (st == 0) {
+        // depends on the handle's capacity only, never on a run's batch
+        st = kDefaultSplitTokens;
+        while (st > kMinDefaultSplitTokens) {
+            const int64_t splits =
+                ((int64_t)cfg->max_pages_per_seq * kPageSize + st - 1) / st;
+            if ((int64_t)cfg->max_batch * cfg->num_kv_heads * splits >= kMinDefaultUnits)
+                break;
+            st /= 2;
+        }
+    }
     if (st % kPageSize != 0 || st > kMaxSplitTokens)
         return RL_DA_ERR_UNSUPPORTED;
     *split_tokens = st;
@@ -843,7 +902,7 @@ rl_da_status rl_decode_attn_create(const rl_da_config* cfg, rl_decode_attn** out
     h->split_pages = sp;
     h->max_splits = ms;
     const int G = cfg->num_q_heads / cfg->num_kv_heads;
-    h->use_mfma = G <= 4 && (cfg->flags & RL_DA_SCORES_ON_VALU) == 0;
+    h->use_mfma = (cfg->flags & RL_DA_SCORES_ON_VALU) == 0;
     h->split_kernel = select_split_kernel(G, (cfg->flags & RL_DA_CHECKED) != 0,
                                           cfg->kv_dtype == RL_DA_KV_FP8_E4M3, h->use_mfma);
     if (hipGetDevice(&h->device) != hipSuccess) {

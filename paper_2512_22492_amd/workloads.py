@@ -51,6 +51,20 @@ CONFIGS = {
         kv_dtype="fp8_e4m3", seed=20251226),
 }
 
+# Variant shapes (not among the five headline workloads): the per-GPU share of
+# the Qwen3-8B step at the paper's rollout tensor parallelism of 8 (Sec. 7.1:
+# one kv head and its 4 query heads per GPU), and the Qwen3-32B head layout
+# (64 query heads, 8 kv heads; the paper evaluates 32B rollouts, Sec. 7.1,
+# without stating its head counts).
+CONFIGS.update({
+    "tp8_share_step": dict(
+        batch=64, num_q_heads=4, num_kv_heads=1, head_dim=128, page_size=16,
+        lengths=("fixed", 4096), pool_factor=1.25, kv_dtype="bf16", seed=20251227),
+    "qwen3_32b_step": dict(
+        batch=64, num_q_heads=64, num_kv_heads=8, head_dim=128, page_size=16,
+        lengths=("fixed", 4096), pool_factor=1.25, kv_dtype="bf16", seed=20251228),
+})
+
 CONFIG_ORDER = ["tiny", "qwen3_8b_step", "long_tail", "straggler",
                 "fp8_large_batch"]
 

@@ -64,6 +64,12 @@ def test_workspace_size_formula():
     assert n == expect
     rc, n2 = B.rl_decode_attn_workspace_size(cfg(split_tokens=512))
     assert rc == B.RL_DA_OK and n2 > n
+    # a small handle gets a shorter default split: 2 x 1 x 16 pages -> 512 tokens
+    rc, n3 = B.rl_decode_attn_workspace_size(cfg(max_batch=2, num_q_heads=4, num_kv_heads=1,
+                                                 max_pages_per_seq=16))
+    rows3 = 2 * 4 * 1
+    assert rc == B.RL_DA_OK
+    assert n3 == (rows3 * 128 * 4 + rows3 * 2 * 4 + 255) // 256 * 256 + 256
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -80,7 +86,6 @@ def test_workspace_size_formula():
     (dict(num_q_heads=24, num_kv_heads=8), B.RL_DA_ERR_UNSUPPORTED),   # G = 3
     (dict(num_q_heads=128, num_kv_heads=8), B.RL_DA_ERR_UNSUPPORTED),  # G = 16
     (dict(split_tokens=24), B.RL_DA_ERR_UNSUPPORTED),
-    (dict(num_q_heads=64, num_kv_heads=8, kv_dtype=B.RL_DA_KV_FP8_E4M3), B.RL_DA_ERR_UNSUPPORTED),
     (dict(kv_dtype=B.RL_DA_KV_FP8_E4M3, flags=B.RL_DA_SCORES_ON_VALU), B.RL_DA_ERR_UNSUPPORTED),
     (dict(split_tokens=4112), B.RL_DA_ERR_UNSUPPORTED),
 ])
