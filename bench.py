@@ -77,7 +77,9 @@ def read_ceilings(p, split_pages, stream):
         e1.synchronize()
         if it:
             best_page = max(best_page, kv / (e0.elapsed_time(e1) / 1e3) / 1e9)
-    return {"stream_read_GBs": round(best_stream, 1), "page_read_GBs": round(best_page, 1)}
+    # the page-read kernel walks head-major slabs whatever the pool's layout
+    return {"stream_read_GBs": round(best_stream, 1), "page_read_GBs": round(best_page, 1),
+            "page_read_layout": "hnd"}
 
 
 def parse_args():
@@ -93,6 +95,8 @@ def parse_args():
     ap.add_argument("--scores", choices=["mfma", "valu"], default="mfma",
                     help="score path of the split-K kernel")
     ap.add_argument("--split-tokens", type=int, default=0)
+    ap.add_argument("--layout", choices=["hnd", "nhd"], default="hnd",
+                    help="pool layout: [page][kv head][slot][dim] or [page][slot][kv head][dim]")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-events", action="store_true",
                     help="do not record events around the split kernel (profiling runs)")
@@ -261,7 +265,8 @@ def bench_append(args, base, stream):
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "dtype": base.kv_dtype, "data": "synthetic",
         "config": {"workload": "%s: %s" % (args.config, _describe(args.config)),
-                   "batch": base.batch, "num_kv_heads": base.num_kv_heads},
+                   "batch": base.batch, "num_kv_heads": base.num_kv_heads,
+                   "layout": base.layout},
         "bytes_per_call": moved, "GBs": round(moved / us / 1e3, 2),
     }
 
@@ -278,7 +283,8 @@ def bench_extend(args, dev):
     n = args.new_tokens
     prior = workloads.draw_lengths(np.random.default_rng(seed), cfg["batch"], cfg["lengths"])
     cfg["lengths"] = [int(x) + n for x in prior]
-    p = workloads.make_problem(args.config + "+extend", seed=seed, device=dev, **cfg)
+    p = workloads.make_problem(args.config + "+extend", seed=seed, device=dev,
+                               layout=args.layout, **cfg)
     T = n * p.batch
     gen = torch.Generator(device=dev).manual_seed(seed + 1)
     q = torch.randn((T, p.num_q_heads, p.head_dim), generator=gen, device=dev).to(torch.bfloat16)
@@ -302,10 +308,15 @@ def bench_extend(args, dev):
         "dtype": "bf16", "data": "synthetic",
         "config": {"workload": "%s cached prefixes + %d new tokens per sequence" % (args.config, n),
                    "batch": p.batch, "num_q_heads": p.num_q_heads,
-                   "num_kv_heads": p.num_kv_heads, "new_tokens": T},
+                   "num_kv_heads": p.num_kv_heads, "new_tokens": T, "layout": args.layout},
         "roofline": {"bound": "mfma", "achieved": round(tf, 2), "peak": 2500.0,
                      "unit": "TFLOP/s", "frac": round(tf / 2500.0, 4)},
     }
+
+
+def traffic_key(args):
+    """Entry of the counter file for this workload and pool layout."""
+    return args.config if args.layout == "hnd" else args.config + ":" + args.layout
 
 
 def _describe(name):
@@ -316,7 +327,7 @@ def _describe(name):
 def main():
     args = parse_args()
     if args.summarize_pmc:
-        summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.config)
+        summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], traffic_key(args))
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -339,7 +350,7 @@ def main():
     if args.op == "extend":
         print(json.dumps(bench_extend(args, dev)), flush=True)
         return
-    base = workloads.make_config(args.config, device=dev)
+    base = workloads.make_config(args.config, device=dev, layout=args.layout)
     replicas = [base]
     for _ in range(1, max(1, args.replicas)):
         replicas.append(workloads.DecodeProblem(**{
@@ -418,7 +429,7 @@ def main():
             "num_kv_heads": base.num_kv_heads, "head_dim": base.head_dim,
             "page_size": base.page_size, "seq_len_mean": float(base.lengths().mean()),
             "split_tokens": split_tokens, "num_splits": num_splits,
-            "scores": args.scores, "replicas": len(replicas),
+            "scores": args.scores, "replicas": len(replicas), "layout": base.layout,
         },
         "query_tokens_per_s": round(base.batch / (ms_per_step / 1e3), 1),
         "kv_bytes_per_step": kv_bytes,
@@ -430,7 +441,7 @@ def main():
         record["roofline"] = {
             "bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
             "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": load_traffic(args.config, kernel_source_sha()),
+            "traffic": load_traffic(traffic_key(args), kernel_source_sha()),
             "kernel": "split-K decode kernel", "avg_us": round(avg * 1e3, 2),
             "min_us": round(float(split_ms.min()) * 1e3, 2),
             "bytes_per_launch": alg_bytes,

@@ -18,6 +18,8 @@
  * owned by the caller; the library never frees or retains it past the call.
  *   q            [batch][Hq][head_dim]                         bf16
  *   k_pool       [num_pages][Hkv][page_size][head_dim]         bf16 or e4m3
+ *                (layout RL_DA_LAYOUT_HND), or
+ *                [num_pages][page_size][Hkv][head_dim]         (RL_DA_LAYOUT_NHD)
  *   v_pool       same as k_pool
  *   k_scale      [num_pages][Hkv] fp32, fp8 pools only: a stored code c of
  *   v_scale      slab (page, kvh) stands for e4m3(c) * scale[page][kvh]
@@ -72,6 +74,12 @@ typedef enum {
 
 typedef enum { RL_DA_KV_BF16 = 0, RL_DA_KV_FP8_E4M3 = 1 } rl_da_kv_dtype;
 
+/* Order of a page's (kv head, token slot) rows in the pools.  HND keeps each
+ * (page, kv head) slab contiguous; NHD keeps each token slot's kv heads
+ * together (the page-major layout many serving engines allocate).  Same page
+ * stride either way; the fp8 scales are [num_pages][Hkv] in both. */
+typedef enum { RL_DA_LAYOUT_HND = 0, RL_DA_LAYOUT_NHD = 1 } rl_da_layout;
+
 /* create() flag: kernels check block-table entries and lengths on device. */
 #define RL_DA_CHECKED 0x1u
 /* create() flag: form q.k with bf16 dot2 ops and DPP row sums on the vector
@@ -91,6 +99,7 @@ typedef struct {
     int32_t max_batch;         /* largest batch a run() may pass (>= 1)       */
     int32_t max_pages_per_seq; /* largest block-table width a run() may pass  */
     int32_t kv_dtype;          /* rl_da_kv_dtype                              */
+    int32_t layout;            /* rl_da_layout                                */
     int32_t split_tokens;      /* tokens per split-K work unit: a multiple of */
                                /* page_size, at most 4096; 0 = the longest of */
                                /* 4096, 2048, 1024, 512 that cuts max_batch   */
@@ -161,17 +170,18 @@ rl_da_status rl_decode_attn_split_info(const rl_decode_attn* h, int32_t max_page
  * seq_lens as for rl_decode_attn_run.  max_q_per_seq >= every n_b (sizes the
  * grid).  Preconditions: n_b <= L_b <= max_pages * page_size and the table
  * entries of pages 0 .. (L_b-1)/page_size in [0, num_pages).  Needs no
- * handle and no workspace; enqueues one kernel on `stream`.  bf16 pools,
- * head_dim 128, page_size 16 and Hq/Hkv in {1, 2, 4, 8, 16} only (else
- * UNSUPPORTED); q, the pools and out 16-byte aligned.
+ * handle and no workspace; enqueues one kernel on `stream`.  bf16 pools
+ * (either rl_da_layout), head_dim 128, page_size 16 and Hq/Hkv in
+ * {1, 2, 4, 8, 16} only (else UNSUPPORTED); q, the pools and out 16-byte
+ * aligned.
  */
 rl_da_status rl_extend_attn(const void* q, const int32_t* q_start, int32_t max_q_per_seq,
                             const void* k_pool, const void* v_pool, const float* k_scale,
                             const float* v_scale, int64_t num_pages, const int32_t* block_table,
                             int32_t max_pages, const int32_t* seq_lens, int32_t batch,
                             int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
-                            int32_t page_size, int32_t kv_dtype, float scale, void* out,
-                            void* stream);
+                            int32_t page_size, int32_t kv_dtype, int32_t layout, float scale,
+                            void* out, void* stream);
 
 /*
  * KV-cache append: the step before attention in every decode step (the
@@ -198,16 +208,16 @@ rl_da_status rl_extend_attn(const void* q, const int32_t* q_start, int32_t max_q
  * skipped (nothing written) and, when device_error is non-NULL, reported in
  * that int32 device word with RL_DA_DEVERR_LENGTH_TOO_LONG /
  * RL_DA_DEVERR_PAGE_OUT_OF_RANGE (bits are only ever set).  Needs no handle;
- * enqueues one kernel on `stream`.  head_dim 128 and page_size 16 only
- * (else UNSUPPORTED); k_new, v_new and the pools 16-byte aligned; k_scale and
- * v_scale non-NULL exactly for e4m3.
+ * enqueues one kernel on `stream`.  Pools in either rl_da_layout;
+ * head_dim 128 and page_size 16 only (else UNSUPPORTED); k_new, v_new and the
+ * pools 16-byte aligned; k_scale and v_scale non-NULL exactly for e4m3.
  */
 rl_da_status rl_kv_append(const void* k_new, const void* v_new, void* k_pool, void* v_pool,
                           float* k_scale, float* v_scale, int64_t num_pages,
                           const int32_t* block_table, int32_t max_pages,
                           const int32_t* seq_lens, int32_t batch, int32_t num_kv_heads,
                           int32_t head_dim, int32_t page_size, int32_t kv_dtype,
-                          int32_t* device_error, void* stream);
+                          int32_t layout, int32_t* device_error, void* stream);
 
 /*
  * Measurement hook (no counterpart in the paper): with both events non-NULL,

@@ -27,6 +27,9 @@ LIB_PATH = os.path.join(_HERE, "libdecode_attn_oracle.so")
 KV_BF16 = 0
 KV_FP8_E4M3 = 1
 
+LAYOUT_HND = 0   # pools [page][kv head][slot][dim]
+LAYOUT_NHD = 1   # pools [page][slot][kv head][dim]
+
 OK = 0
 ERR_ARG = 1
 ERR_PRECONDITION = 2
@@ -56,6 +59,7 @@ class _Append(ctypes.Structure):
         ("head_dim", ctypes.c_int32),
         ("page_size", ctypes.c_int32),
         ("kv_dtype", ctypes.c_int32),
+        ("layout", ctypes.c_int32),
         ("max_pages", ctypes.c_int32),
         ("num_pages", ctypes.c_int64),
         ("k_new", ctypes.c_void_p),
@@ -77,6 +81,7 @@ class _Problem(ctypes.Structure):
         ("head_dim", ctypes.c_int32),
         ("page_size", ctypes.c_int32),
         ("kv_dtype", ctypes.c_int32),
+        ("layout", ctypes.c_int32),
         ("max_pages", ctypes.c_int32),
         ("num_pages", ctypes.c_int64),
         ("scale", ctypes.c_double),
@@ -123,6 +128,23 @@ def _load():
     return _lib
 
 
+def _layout_code(layout):
+    codes = {LAYOUT_HND: LAYOUT_HND, LAYOUT_NHD: LAYOUT_NHD, "hnd": LAYOUT_HND,
+             "nhd": LAYOUT_NHD}
+    if layout not in codes:
+        raise ValueError("unknown pool layout %r" % (layout,))
+    return codes[layout]
+
+
+def _pool_dims(pool, layout):
+    """(num_pages, num_kv_heads, page_size, head_dim) of a pool array."""
+    if _layout_code(layout) == LAYOUT_NHD:
+        P, page, Hkv, D = pool.shape
+    else:
+        P, Hkv, page, D = pool.shape
+    return P, Hkv, page, D
+
+
 def _c(a, dtype):
     a = np.ascontiguousarray(a)
     if a.dtype != dtype:
@@ -132,7 +154,7 @@ def _c(a, dtype):
 
 def decode_attention(q_bits, k_pool, v_pool, block_table, seq_lens, *,
                      num_kv_heads, scale, kv_dtype=KV_BF16, k_scale=None,
-                     v_scale=None, rows=None):
+                     v_scale=None, rows=None, layout=LAYOUT_HND):
     """Attention rows in fp64.
 
     q_bits      uint16 [B, Hq, D] bf16 bit patterns
@@ -149,7 +171,7 @@ def decode_attention(q_bits, k_pool, v_pool, block_table, seq_lens, *,
     block_table = _c(block_table, np.int32)
     seq_lens = _c(seq_lens, np.int32)
     B, Hq, D = q_bits.shape
-    P, Hkv, page, D2 = k_pool.shape
+    P, Hkv, page, D2 = _pool_dims(k_pool, layout)
     if D2 != D or v_pool.shape != k_pool.shape or Hkv != num_kv_heads:
         raise ValueError("pool shape does not match q / num_kv_heads")
     if block_table.ndim != 2 or block_table.shape[0] != B or seq_lens.shape != (B,):
@@ -161,7 +183,8 @@ def decode_attention(q_bits, k_pool, v_pool, block_table, seq_lens, *,
             raise ValueError("scale shape")
     prob = _Problem(
         batch=B, num_q_heads=Hq, num_kv_heads=Hkv, head_dim=D, page_size=page,
-        kv_dtype=kv_dtype, max_pages=block_table.shape[1], num_pages=P,
+        kv_dtype=kv_dtype, layout=_layout_code(layout), max_pages=block_table.shape[1],
+        num_pages=P,
         scale=float(scale), q=q_bits.ctypes.data, k_pool=k_pool.ctypes.data,
         v_pool=v_pool.ctypes.data,
         k_scale=k_scale.ctypes.data if kv_dtype == KV_FP8_E4M3 else None,
@@ -182,7 +205,8 @@ def decode_attention(q_bits, k_pool, v_pool, block_table, seq_lens, *,
 
 
 def extend_attention(q_bits, q_start, k_pool, v_pool, block_table, seq_lens, *,
-                     num_kv_heads, scale, kv_dtype=KV_BF16, k_scale=None, v_scale=None):
+                     num_kv_heads, scale, kv_dtype=KV_BF16, k_scale=None, v_scale=None,
+                     layout=LAYOUT_HND):
     """Causal attention of each sequence's new tokens (q rows q_start[b] ..
     q_start[b+1]-1, the last n_b cached tokens) over its cache.  q_bits uint16
     [T, Hq, D]; returns fp64 [T, Hq, D]."""
@@ -196,7 +220,7 @@ def extend_attention(q_bits, q_start, k_pool, v_pool, block_table, seq_lens, *,
     seq_lens = _c(seq_lens, np.int32)
     T, Hq, D = q_bits.shape
     B = seq_lens.shape[0]
-    P, Hkv, page, _ = k_pool.shape
+    P, Hkv, page, _ = _pool_dims(k_pool, layout)
     if q_start.shape != (B + 1,) or q_start[-1] != T:
         raise ValueError("q_start must have batch+1 entries ending at T")
     if kv_dtype == KV_FP8_E4M3:
@@ -204,7 +228,8 @@ def extend_attention(q_bits, q_start, k_pool, v_pool, block_table, seq_lens, *,
         v_scale = _c(v_scale, np.float32)
     prob = _Problem(
         batch=B, num_q_heads=Hq, num_kv_heads=Hkv, head_dim=D, page_size=page,
-        kv_dtype=kv_dtype, max_pages=block_table.shape[1], num_pages=P,
+        kv_dtype=kv_dtype, layout=_layout_code(layout), max_pages=block_table.shape[1],
+        num_pages=P,
         scale=float(scale), q=q_bits.ctypes.data, k_pool=k_pool.ctypes.data,
         v_pool=v_pool.ctypes.data,
         k_scale=k_scale.ctypes.data if kv_dtype == KV_FP8_E4M3 else None,
@@ -218,7 +243,7 @@ def extend_attention(q_bits, q_start, k_pool, v_pool, block_table, seq_lens, *,
 
 
 def kv_append(k_new_bits, v_new_bits, k_pool, v_pool, block_table, seq_lens, *,
-              kv_dtype=KV_BF16, k_scale=None, v_scale=None):
+              kv_dtype=KV_BF16, k_scale=None, v_scale=None, layout=LAYOUT_HND):
     """Appends one token per (sequence, kv head); returns updated copies of
     (k_pool, v_pool, k_scale, v_scale).  k_new/v_new: uint16 bf16 bits
     [B, Hkv, D]; pools as in decode_attention; seq_lens = lengths before the
@@ -232,7 +257,7 @@ def kv_append(k_new_bits, v_new_bits, k_pool, v_pool, block_table, seq_lens, *,
     block_table = _c(block_table, np.int32)
     seq_lens = _c(seq_lens, np.int32)
     B, Hkv, D = k_new_bits.shape
-    P, Hkv2, page, D2 = k_pool.shape
+    P, Hkv2, page, D2 = _pool_dims(k_pool, layout)
     if (Hkv2, D2) != (Hkv, D) or v_new_bits.shape != k_new_bits.shape:
         raise ValueError("shape mismatch")
     if kv_dtype == KV_FP8_E4M3:
@@ -240,7 +265,7 @@ def kv_append(k_new_bits, v_new_bits, k_pool, v_pool, block_table, seq_lens, *,
         v_scale = _c(v_scale, np.float32).copy()
     prob = _Append(
         batch=B, num_kv_heads=Hkv, head_dim=D, page_size=page, kv_dtype=kv_dtype,
-        max_pages=block_table.shape[1], num_pages=P, k_new=k_new_bits.ctypes.data,
+        layout=_layout_code(layout), max_pages=block_table.shape[1], num_pages=P, k_new=k_new_bits.ctypes.data,
         v_new=v_new_bits.ctypes.data, k_pool=k_pool.ctypes.data, v_pool=v_pool.ctypes.data,
         k_scale=k_scale.ctypes.data if kv_dtype == KV_FP8_E4M3 else None,
         v_scale=v_scale.ctypes.data if kv_dtype == KV_FP8_E4M3 else None,

@@ -70,14 +70,22 @@ double rl_oracle_bf16_to_double(uint16_t bits)
     return oracle_bf16_to_double(bits);
 }
 
+/* Index of element d of token slot `slot`, kv head kvh, page `page`. */
+static int64_t pool_index(int layout, int64_t page, int kvh, int slot, int d, int num_kv_heads,
+                          int page_size, int head_dim)
+{
+    if (layout == RL_ORACLE_LAYOUT_NHD)
+        return ((page * page_size + slot) * num_kv_heads + kvh) * (int64_t)head_dim + d;
+    return ((page * num_kv_heads + kvh) * page_size + slot) * (int64_t)head_dim + d;
+}
+
 /* Decoded element d of token slot `slot` in slab (page, kvh) of a pool. */
 static double pool_element(const rl_oracle_problem* p, const void* pool,
                            const float* slab_scale, int64_t page, int kvh,
                            int slot, int d)
 {
-    const int64_t idx =
-        (((int64_t)page * p->num_kv_heads + kvh) * p->page_size + slot) *
-            (int64_t)p->head_dim + d;
+    const int64_t idx = pool_index(p->layout, page, kvh, slot, d, p->num_kv_heads,
+                                   p->page_size, p->head_dim);
     if (p->kv_dtype == RL_ORACLE_KV_BF16)
         return oracle_bf16_to_double(((const uint16_t*)pool)[idx]);
     return rl_oracle_e4m3_to_double(((const uint8_t*)pool)[idx]) *
@@ -177,6 +185,8 @@ int rl_oracle_decode_attn(const rl_oracle_problem* p, const int32_t* rows,
         return RL_ORACLE_ERR_ARG;
     if (p->kv_dtype != RL_ORACLE_KV_BF16 && p->kv_dtype != RL_ORACLE_KV_FP8_E4M3)
         return RL_ORACLE_ERR_ARG;
+    if (p->layout != RL_ORACLE_LAYOUT_HND && p->layout != RL_ORACLE_LAYOUT_NHD)
+        return RL_ORACLE_ERR_ARG;
     if (p->kv_dtype == RL_ORACLE_KV_FP8_E4M3 &&
         (p->k_scale == NULL || p->v_scale == NULL))
         return RL_ORACLE_ERR_ARG;
@@ -245,6 +255,8 @@ int rl_oracle_extend_attn(const rl_oracle_problem* p, const int32_t* q_start, do
         p->num_q_heads % p->num_kv_heads != 0 || p->head_dim <= 0 || p->page_size <= 0)
         return RL_ORACLE_ERR_ARG;
     if (p->kv_dtype == RL_ORACLE_KV_FP8_E4M3 && (p->k_scale == NULL || p->v_scale == NULL))
+        return RL_ORACLE_ERR_ARG;
+    if (p->layout != RL_ORACLE_LAYOUT_HND && p->layout != RL_ORACLE_LAYOUT_NHD)
         return RL_ORACLE_ERR_ARG;
     if (q_start[0] != 0)
         return RL_ORACLE_ERR_ARG;
@@ -345,6 +357,8 @@ int rl_oracle_kv_append(const rl_oracle_append* p)
     const int fp8 = p->kv_dtype == RL_ORACLE_KV_FP8_E4M3;
     if (!fp8 && p->kv_dtype != RL_ORACLE_KV_BF16)
         return RL_ORACLE_ERR_ARG;
+    if (p->layout != RL_ORACLE_LAYOUT_HND && p->layout != RL_ORACLE_LAYOUT_NHD)
+        return RL_ORACLE_ERR_ARG;
     if (fp8 && (p->k_scale == NULL || p->v_scale == NULL))
         return RL_ORACLE_ERR_ARG;
     for (int b = 0; b < p->batch; ++b) {
@@ -369,13 +383,14 @@ int rl_oracle_kv_append(const rl_oracle_append* p)
                 const uint16_t* src = (const uint16_t*)(which ? p->v_new : p->k_new) +
                                       ((int64_t)b * H + kvh) * D;
                 const int64_t slab = page * H + kvh;
+#define ELEM(sl, d) pool_index(p->layout, page, kvh, (sl), (d), H, P, D)
                 if (!fp8) {
-                    uint16_t* dst = (uint16_t*)(which ? p->v_pool : p->k_pool) +
-                                    (slab * P + slot) * D;
-                    memcpy(dst, src, sizeof(uint16_t) * (size_t)D);
+                    uint16_t* dst = (uint16_t*)(which ? p->v_pool : p->k_pool);
+                    for (int d = 0; d < D; ++d)
+                        dst[ELEM(slot, d)] = src[d];
                     continue;
                 }
-                uint8_t* codes = (uint8_t*)(which ? p->v_pool : p->k_pool) + slab * P * D;
+                uint8_t* codes = (uint8_t*)(which ? p->v_pool : p->k_pool);
                 float* scale = (which ? p->v_scale : p->k_scale) + slab;
                 float absmax = 0.0f;
                 for (int d = 0; d < D; ++d) {
@@ -392,17 +407,20 @@ int rl_oracle_kv_append(const rl_oracle_append* p)
                     s_new = wanted > s_old ? wanted : s_old;
                     if (s_new != s_old) {
                         const float ratio = s_old / s_new;
-                        for (int i = 0; i < slot * D; ++i) {
-                            const float old = (float)rl_oracle_e4m3_to_double(codes[i]);
-                            codes[i] = rl_oracle_e4m3_encode(old * ratio);
-                        }
+                        for (int sl = 0; sl < slot; ++sl)
+                            for (int d = 0; d < D; ++d) {
+                                uint8_t* c = &codes[ELEM(sl, d)];
+                                const float old = (float)rl_oracle_e4m3_to_double(*c);
+                                *c = rl_oracle_e4m3_encode(old * ratio);
+                            }
                     }
                 }
                 *scale = s_new;
                 for (int d = 0; d < D; ++d) {
                     const float x = (float)rl_oracle_bf16_to_double(src[d]);
-                    codes[slot * D + d] = rl_oracle_e4m3_encode(clamp448(x / s_new));
+                    codes[ELEM(slot, d)] = rl_oracle_e4m3_encode(clamp448(x / s_new));
                 }
+#undef ELEM
             }
         }
     }

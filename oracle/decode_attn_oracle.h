@@ -7,7 +7,8 @@
  * Every pointer is a host pointer owned by the caller.  The oracle never
  * writes its inputs.  Layouts (row-major, innermost last):
  *   q            [batch][num_q_heads][head_dim]            bf16 bit patterns
- *   k_pool/v_pool [num_pages][num_kv_heads][page_size][head_dim]
+ *   k_pool/v_pool [num_pages][num_kv_heads][page_size][head_dim] (layout HND)
+ *                 or [num_pages][page_size][num_kv_heads][head_dim] (NHD);
  *                 bf16 bit patterns, or OCP e4m3 codes for the fp8 variant
  *   k_scale/v_scale [num_pages][num_kv_heads] fp32 (fp8 only, else unused)
  *   block_table  [batch][max_pages] int32 physical page indices
@@ -32,9 +33,13 @@ enum {
 
 enum { RL_ORACLE_KV_BF16 = 0, RL_ORACLE_KV_FP8_E4M3 = 1 };
 
+/* Pool layouts: [page][kv head][slot][dim] (HND) or [page][slot][kv head][dim]. */
+enum { RL_ORACLE_LAYOUT_HND = 0, RL_ORACLE_LAYOUT_NHD = 1 };
+
 typedef struct {
     int32_t batch, num_q_heads, num_kv_heads, head_dim, page_size;
     int32_t kv_dtype;   /* RL_ORACLE_KV_*                                  */
+    int32_t layout;     /* RL_ORACLE_LAYOUT_*                              */
     int32_t max_pages;  /* columns of block_table                          */
     int64_t num_pages;  /* pages in each pool                              */
     double scale;       /* softmax scale applied to q.k                    */
@@ -79,6 +84,7 @@ int rl_oracle_extend_attn(const rl_oracle_problem* p, const int32_t* q_start, do
 typedef struct {
     int32_t batch, num_kv_heads, head_dim, page_size;
     int32_t kv_dtype;
+    int32_t layout;
     int32_t max_pages;
     int64_t num_pages;
     const void* k_new;

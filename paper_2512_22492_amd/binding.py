@@ -22,6 +22,10 @@ RL_DA_ERR_HIP = 4
 RL_DA_KV_BF16 = 0
 RL_DA_KV_FP8_E4M3 = 1
 
+RL_DA_LAYOUT_HND = 0
+RL_DA_LAYOUT_NHD = 1
+LAYOUTS = {"hnd": RL_DA_LAYOUT_HND, "nhd": RL_DA_LAYOUT_NHD}
+
 RL_DA_CHECKED = 0x1
 RL_DA_SCORES_ON_VALU = 0x2
 
@@ -52,6 +56,7 @@ class rl_da_config(ctypes.Structure):
         ("max_batch", ctypes.c_int32),
         ("max_pages_per_seq", ctypes.c_int32),
         ("kv_dtype", ctypes.c_int32),
+        ("layout", ctypes.c_int32),
         ("split_tokens", ctypes.c_int32),
         ("flags", ctypes.c_uint32),
     ]
@@ -103,10 +108,10 @@ def load_library():
     lib.rl_decode_attn_split_info.argtypes = [vp, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)]
     lib.rl_decode_attn_split_info.restype = ctypes.c_int
     lib.rl_extend_attn.argtypes = [vp, vp, i32, vp, vp, vp, vp, i64, vp, i32, vp, i32, i32, i32,
-                                   i32, i32, i32, ctypes.c_float, vp, vp]
+                                   i32, i32, i32, i32, ctypes.c_float, vp, vp]
     lib.rl_extend_attn.restype = ctypes.c_int
     lib.rl_kv_append.argtypes = [vp, vp, vp, vp, vp, vp, i64, vp, i32, vp, i32, i32, i32, i32,
-                                 i32, vp, vp]
+                                 i32, i32, vp, vp]
     lib.rl_kv_append.restype = ctypes.c_int
     lib.rl_decode_attn_set_timing_events.argtypes = [vp, vp, vp]
     lib.rl_decode_attn_set_timing_events.restype = ctypes.c_int
@@ -138,10 +143,12 @@ def _stream(s):
 
 
 def make_config(num_q_heads, num_kv_heads, max_batch, max_pages_per_seq, *,
-                head_dim=128, page_size=16, kv_dtype=RL_DA_KV_BF16, split_tokens=0,
-                flags=0) -> rl_da_config:
-    return rl_da_config(num_q_heads, num_kv_heads, head_dim, page_size, max_batch,
-                        max_pages_per_seq, kv_dtype, split_tokens, flags)
+                head_dim=128, page_size=16, kv_dtype=RL_DA_KV_BF16,
+                layout=RL_DA_LAYOUT_HND, split_tokens=0, flags=0) -> rl_da_config:
+    return rl_da_config(num_q_heads=num_q_heads, num_kv_heads=num_kv_heads,
+                        head_dim=head_dim, page_size=page_size, max_batch=max_batch,
+                        max_pages_per_seq=max_pages_per_seq, kv_dtype=kv_dtype,
+                        layout=layout, split_tokens=split_tokens, flags=flags)
 
 
 # ------------------------------------------------- C functions, same names ---
@@ -190,13 +197,13 @@ def rl_decode_attn_split_info(h, max_pages):
 
 def rl_extend_attn(q, q_start, max_q_per_seq, k_pool, v_pool, k_scale, v_scale, num_pages,
                    block_table, max_pages, seq_lens, batch, num_q_heads, num_kv_heads,
-                   head_dim=128, page_size=16, kv_dtype=RL_DA_KV_BF16, scale=1.0, out=None,
-                   stream=None) -> int:
+                   head_dim=128, page_size=16, kv_dtype=RL_DA_KV_BF16, layout=RL_DA_LAYOUT_HND,
+                   scale=1.0, out=None, stream=None) -> int:
     return load_library().rl_extend_attn(
         _ptr(q), _ptr(q_start), int(max_q_per_seq), _ptr(k_pool), _ptr(v_pool), _ptr(k_scale),
         _ptr(v_scale), int(num_pages), _ptr(block_table), int(max_pages), _ptr(seq_lens),
         int(batch), int(num_q_heads), int(num_kv_heads), int(head_dim), int(page_size),
-        int(kv_dtype), float(scale), _ptr(out), _stream(stream))
+        int(kv_dtype), int(layout), float(scale), _ptr(out), _stream(stream))
 
 
 def extend_attention(p, q, q_start, max_q_per_seq, out, stream=None):
@@ -205,20 +212,21 @@ def extend_attention(p, q, q_start, max_q_per_seq, out, stream=None):
     dt = RL_DA_KV_BF16 if p.kv_dtype == "bf16" else RL_DA_KV_FP8_E4M3
     rc = rl_extend_attn(q, q_start, max_q_per_seq, p.k_pool, p.v_pool, p.k_scale, p.v_scale,
                         p.num_pages, p.block_table, p.max_pages, p.seq_lens, p.batch,
-                        p.num_q_heads, p.num_kv_heads, p.head_dim, p.page_size, dt, p.scale,
-                        out, stream)
+                        p.num_q_heads, p.num_kv_heads, p.head_dim, p.page_size, dt,
+                        LAYOUTS[p.layout], p.scale, out, stream)
     if rc != RL_DA_OK:
         raise RLDecodeAttnError(rc, "rl_extend_attn")
 
 
 def rl_kv_append(k_new, v_new, k_pool, v_pool, k_scale, v_scale, num_pages, block_table,
                  max_pages, seq_lens, batch, num_kv_heads, head_dim=128, page_size=16,
-                 kv_dtype=RL_DA_KV_BF16, device_error=None, stream=None) -> int:
+                 kv_dtype=RL_DA_KV_BF16, layout=RL_DA_LAYOUT_HND, device_error=None,
+                 stream=None) -> int:
     return load_library().rl_kv_append(
         _ptr(k_new), _ptr(v_new), _ptr(k_pool), _ptr(v_pool), _ptr(k_scale), _ptr(v_scale),
         int(num_pages), _ptr(block_table), int(max_pages), _ptr(seq_lens), int(batch),
-        int(num_kv_heads), int(head_dim), int(page_size), int(kv_dtype), _ptr(device_error),
-        _stream(stream))
+        int(num_kv_heads), int(head_dim), int(page_size), int(kv_dtype), int(layout),
+        _ptr(device_error), _stream(stream))
 
 
 def kv_append(p, k_new, v_new, device_error=None, stream=None):
@@ -227,7 +235,7 @@ def kv_append(p, k_new, v_new, device_error=None, stream=None):
     dt = RL_DA_KV_BF16 if p.kv_dtype == "bf16" else RL_DA_KV_FP8_E4M3
     rc = rl_kv_append(k_new, v_new, p.k_pool, p.v_pool, p.k_scale, p.v_scale, p.num_pages,
                       p.block_table, p.max_pages, p.seq_lens, p.batch, p.num_kv_heads,
-                      p.head_dim, p.page_size, dt, device_error, stream)
+                      p.head_dim, p.page_size, dt, LAYOUTS[p.layout], device_error, stream)
     if rc != RL_DA_OK:
         raise RLDecodeAttnError(rc, "rl_kv_append")
 
@@ -242,12 +250,14 @@ class DecodeAttention:
     """Owns one library handle; run() enqueues one decode step."""
 
     def __init__(self, num_q_heads, num_kv_heads, max_batch, max_pages_per_seq, *,
-                 kv_dtype="bf16", split_tokens=0, flags=0, head_dim=128, page_size=16):
+                 kv_dtype="bf16", layout="hnd", split_tokens=0, flags=0, head_dim=128,
+                 page_size=16):
         dt = {"bf16": RL_DA_KV_BF16, "fp8_e4m3": RL_DA_KV_FP8_E4M3}[kv_dtype]
         self.kv_dtype = kv_dtype
+        self.layout = layout
         self.cfg = make_config(num_q_heads, num_kv_heads, max_batch, max_pages_per_seq,
                                head_dim=head_dim, page_size=page_size, kv_dtype=dt,
-                               split_tokens=split_tokens, flags=flags)
+                               layout=LAYOUTS[layout], split_tokens=split_tokens, flags=flags)
         rc, h = rl_decode_attn_create(self.cfg)
         if rc != RL_DA_OK:
             raise RLDecodeAttnError(rc, "rl_decode_attn_create")
@@ -256,7 +266,7 @@ class DecodeAttention:
     @classmethod
     def for_problem(cls, p, **kw):
         return cls(p.num_q_heads, p.num_kv_heads, p.batch, p.max_pages,
-                   kv_dtype=p.kv_dtype, **kw)
+                   kv_dtype=p.kv_dtype, layout=p.layout, **kw)
 
     def run(self, q, k_pool, v_pool, k_scale, v_scale, block_table, seq_lens, scale, out,
             stream=None):
@@ -267,6 +277,8 @@ class DecodeAttention:
             raise RLDecodeAttnError(rc, "rl_decode_attn_run")
 
     def run_problem(self, p, out, stream=None):
+        if p.layout != self.layout:
+            raise ValueError("problem layout %r, handle layout %r" % (p.layout, self.layout))
         self.run(p.q, p.k_pool, p.v_pool, p.k_scale, p.v_scale, p.block_table, p.seq_lens,
                  p.scale, out, stream)
 

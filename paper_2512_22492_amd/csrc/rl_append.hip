@@ -22,6 +22,9 @@ struct AppendArgs {
     const int32_t* seq_lens;
     int32_t* dev_error;         // may be null
     int64_t num_pages;
+    int64_t page_bytes;         // pool strides in bytes: per page,
+    int32_t head_bytes;         //   per kv head within a page,
+    int32_t row_bytes;          //   per token slot within a slab
     int32_t num_kv_heads;
     int32_t max_pages;
 };
@@ -71,17 +74,17 @@ __global__ __launch_bounds__(2 * kWave) void kv_append_kernel(AppendArgs a)
     const int64_t slab = (int64_t)page * a.num_kv_heads + kvh;
     const uint16_t* src = (which ? a.v_new : a.k_new) + ((int64_t)b * a.num_kv_heads + kvh) * kHeadDim;
     const uint32_t bits = *reinterpret_cast<const uint32_t*>(src + 2 * lane);
-    uint8_t* pool = which ? a.v_pool : a.k_pool;
+    // token slot 0 of slab (page, kvh); slot j is j * row_bytes further
+    uint8_t* codes = (which ? a.v_pool : a.k_pool) + page * a.page_bytes +
+                     (int64_t)kvh * a.head_bytes;
     if (!FP8) {
-        *reinterpret_cast<uint32_t*>(pool + (slab * kPageSize + slot) * kHeadDim * 2 + 4 * lane) =
-            bits;
+        *reinterpret_cast<uint32_t*>(codes + slot * a.row_bytes + 4 * lane) = bits;
         return;
     }
     const float x0 = bf16_lo(bits), x1 = bf16_hi(bits);
     const float absmax = wave_max(fmaxf(fabsf(x0), fabsf(x1)));
     const float wanted = absmax > 0.0f ? absmax / 448.0f : 1.0f;
     float* scale = (which ? a.v_scale : a.k_scale) + slab;
-    uint8_t* codes = pool + slab * kPageSize * kHeadDim;
     float s_new = wanted;
     if (slot != 0) {
         const float s_old = *scale;
@@ -89,18 +92,20 @@ __global__ __launch_bounds__(2 * kWave) void kv_append_kernel(AppendArgs a)
         if (s_new != s_old) {
             // re-encode the slab's earlier slots at the grown scale
             const float ratio = s_old / s_new;
-            uint32_t* words = reinterpret_cast<uint32_t*>(codes);
-            for (int w = lane; w < slot * kHeadDim / 4; w += kWave) {
-                const uint32_t c = words[w];
+            constexpr int kWordsPerRow = kHeadDim / 4;
+            for (int w = lane; w < slot * kWordsPerRow; w += kWave) {
+                uint32_t* word = reinterpret_cast<uint32_t*>(
+                    codes + (w / kWordsPerRow) * a.row_bytes + 4 * (w % kWordsPerRow));
+                const uint32_t c = *word;
                 const floatx2_t lo = __builtin_amdgcn_cvt_pk_f32_fp8(c, false);
                 const floatx2_t hi = __builtin_amdgcn_cvt_pk_f32_fp8(c, true);
-                words[w] = e4m3_pair(lo.x * ratio, lo.y * ratio) |
-                           (e4m3_pair(hi.x * ratio, hi.y * ratio) << 16);
+                *word = e4m3_pair(lo.x * ratio, lo.y * ratio) |
+                        (e4m3_pair(hi.x * ratio, hi.y * ratio) << 16);
             }
         }
     }
     const uint32_t pair = e4m3_pair(clamp448(x0 / s_new), clamp448(x1 / s_new));
-    *reinterpret_cast<uint16_t*>(codes + slot * kHeadDim + 2 * lane) = (uint16_t)pair;
+    *reinterpret_cast<uint16_t*>(codes + slot * a.row_bytes + 2 * lane) = (uint16_t)pair;
     if (lane == 0)
         *scale = s_new;
 }
@@ -114,7 +119,7 @@ rl_da_status rl_kv_append(const void* k_new, const void* v_new, void* k_pool, vo
                           const int32_t* block_table, int32_t max_pages,
                           const int32_t* seq_lens, int32_t batch, int32_t num_kv_heads,
                           int32_t head_dim, int32_t page_size, int32_t kv_dtype,
-                          int32_t* device_error, void* stream)
+                          int32_t layout, int32_t* device_error, void* stream)
 {
     if (k_new == nullptr || v_new == nullptr || k_pool == nullptr || v_pool == nullptr ||
         block_table == nullptr || seq_lens == nullptr)
@@ -129,6 +134,9 @@ rl_da_status rl_kv_append(const void* k_new, const void* v_new, void* k_pool, vo
         return RL_DA_ERR_INVALID_ARG;
     const bool fp8 = kv_dtype == RL_DA_KV_FP8_E4M3;
     if (fp8 != (k_scale != nullptr) || fp8 != (v_scale != nullptr))
+        return RL_DA_ERR_INVALID_ARG;
+    PoolStrides ps;
+    if (!pool_strides(layout, num_kv_heads, fp8 ? 1 : 2, &ps))
         return RL_DA_ERR_INVALID_ARG;
     if (batch == 0)
         return RL_DA_OK;
@@ -146,6 +154,9 @@ rl_da_status rl_kv_append(const void* k_new, const void* v_new, void* k_pool, vo
     aa.seq_lens = seq_lens;
     aa.dev_error = device_error;
     aa.num_pages = num_pages;
+    aa.page_bytes = ps.page;
+    aa.head_bytes = ps.head;
+    aa.row_bytes = ps.row;
     aa.num_kv_heads = num_kv_heads;
     aa.max_pages = max_pages;
     hipStream_t st = (hipStream_t)stream;

@@ -30,6 +30,32 @@ typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
 inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
+// Byte strides of a pool of elt-byte elements: per page, per kv head within a
+// page, per token slot within a (page, kv head) slab.
+struct PoolStrides {
+    int64_t page;
+    int32_t head;
+    int32_t row;
+};
+
+// false for an unknown layout
+inline bool pool_strides(int32_t layout, int32_t num_kv_heads, int32_t elt, PoolStrides* s)
+{
+    const int32_t row = kHeadDim * elt;
+    s->page = (int64_t)num_kv_heads * kPageSize * row;
+    if (layout == RL_DA_LAYOUT_HND) {
+        s->head = kPageSize * row;
+        s->row = row;
+        return true;
+    }
+    if (layout == RL_DA_LAYOUT_NHD) {
+        s->head = row;
+        s->row = num_kv_heads * row;
+        return true;
+    }
+    return false;
+}
+
 // ------------------------------------------------------------ helpers ---
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }

@@ -18,8 +18,9 @@
 //
 // Data movement is the whole cost: every K/V byte is read once from HBM.  A
 // (page, kv head) slab is 16 tokens x 128 dims x 2 bytes = 4 KiB, contiguous in
-// the [page][kv head][slot][dim] pool layout, and is read by one wavefront
-// with four 16-byte-per-lane non-temporal loads.  Scores are computed once per
+// the [page][kv head][slot][dim] pool layout (16 rows of 256 bytes, 256 * Hkv
+// bytes apart, in the [page][slot][kv head][dim] layout), and is read by one
+// wavefront with four 16-byte-per-lane non-temporal loads each for K and V.  Scores are computed once per
 // kv head for all G query heads of the group (the GQA reuse), either with one
 // MFMA per 32 dims (the G query rows packed into a 16-row tile) or with bf16
 // dot2 ops and DPP row reductions; the value accumulation runs in fp32 on the
@@ -43,11 +44,10 @@ constexpr int kMinDefaultSplitTokens = 512;
 constexpr int64_t kMinDefaultUnits = 256;
 // each wavefront holds its pages' block-table entries one per lane
 constexpr int kMaxSplitTokens = kWave * kUnitWaves * kPageSize;
-constexpr int kSlabBytesBf16 = kPageSize * kHeadDim * 2;
 
 struct SplitArgs {
     const uint16_t* q;          // bf16 bits [B][Hq][D]
-    const uint8_t* k_pool;      // [P][Hkv][16][D] elements
+    const uint8_t* k_pool;      // [P][Hkv][16][D] or [P][16][Hkv][D] elements
     const uint8_t* v_pool;
     const float* k_scale;       // [P][Hkv] (fp8 only)
     const float* v_scale;
@@ -58,6 +58,9 @@ struct SplitArgs {
     float* ws_ml;               // [B][Hq][num_splits][2]  (m in log2 units, l)
     int32_t* dev_error;
     int64_t num_pages;
+    int64_t page_bytes;         // pool bytes per page (all kv heads)
+    int32_t head_bytes;         // offset of kv head h's slab within a page, per h
+    int32_t row_bytes;          // offset between token slots of a slab
     int32_t num_q_heads;
     int32_t num_kv_heads;
     int32_t max_pages;
@@ -134,10 +137,11 @@ __device__ __forceinline__ void write_zero_rows(const SplitArgs& a, const WaveTa
     }
 }
 
-__device__ __forceinline__ const uint8_t* slab_base(const uint8_t* pool, int64_t page,
-                                                    int num_kv_heads, int kvh, int slab_bytes)
+// First byte (token slot 0, dim 0) of slab (page, kvh).
+__device__ __forceinline__ const uint8_t* slab_base(const SplitArgs& a, const uint8_t* pool,
+                                                    int64_t page, int kvh)
 {
-    return pool + (page * num_kv_heads + kvh) * (int64_t)slab_bytes;
+    return pool + page * a.page_bytes + (int64_t)kvh * a.head_bytes;
 }
 
 // Global page index of a wavefront's i-th page.
@@ -244,16 +248,15 @@ __device__ __forceinline__ void stream_pages(int n, Buf& a, Buf& b, Issue issue,
 
 // ------------------------------------------------------ K/V page formats ---
 //
-// A wavefront consumes one (page, kv head) slab at a time.  For the score MFMA
-// (v_mfma_f32_16x16x32_bf16, A = queries 16x32, B = keys 32x16) lane l supplies
-// key token n = l%16 and 8 of the 32 dims of each of the four k-blocks; which
-// 8 dims is the format's choice (q_dim), as long as the query tile uses the
-// same ones.  For the value pass lane l = 16r + c holds dims 8c..8c+7 of
-// tokens 4k + r, k = 0..3.
+// A wavefront consumes one (page, kv head) slab at a time: 16 token rows of
+// 128 dims, `row` bytes apart.  For the score MFMA (v_mfma_f32_16x16x32_bf16,
+// A = queries 16x32, B = keys 32x16) lane l supplies key token n = l%16 and 8
+// of the 32 dims of each of the four k-blocks; which 8 dims is the format's
+// choice (q_dim), as long as the query tile uses the same ones.  For the value
+// pass lane l = 16r + c holds dims 8c..8c+7 of tokens 4k + r, k = 0..3.
 
 // bf16 slab: 4 KiB, four 16-byte loads per lane for K and for V.
 struct KvBf16 {
-    static constexpr int kSlabBytes = kPageSize * kHeadDim * 2;
     static constexpr bool kScaled = false;
     struct Buf {
         uint4 k[4];
@@ -261,15 +264,16 @@ struct KvBf16 {
     };
     // first dim of the 8 query dims lane group kg holds for k-block i
     __device__ static int q_dim(int i, int kg) { return 32 * i + 8 * kg; }
-    __device__ static void load(Buf& b, const uint8_t* ks, const uint8_t* vs, int lane)
+    __device__ static void load(Buf& b, const uint8_t* ks, const uint8_t* vs, int lane, int row)
     {
-        const int koff = (lane & 15) * (kHeadDim * 2) + 16 * (lane >> 4);
+        const int koff = (lane & 15) * row + 16 * (lane >> 4);
 #pragma unroll
         for (int i = 0; i < 4; ++i)
             b.k[i] = load_stream16(ks + koff + 64 * i);
+        const int voff = (lane >> 4) * row + 16 * (lane & 15);
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-            b.v[i] = load_stream16(vs + lane * 16 + 1024 * i);
+            b.v[i] = load_stream16(vs + 4 * row * i + voff);
     }
     __device__ static uint4 k_block(const Buf& b, int i) { return b.k[i]; }
     __device__ static void values(const Buf& b, int k, float (&v)[8]) { unpack8(b.v[k], v); }
@@ -282,21 +286,21 @@ struct KvBf16 {
 // converted to fp32.  The slab scales stay out of the conversions: k_scale
 // multiplies the score and v_scale the probability.
 struct KvFp8 {
-    static constexpr int kSlabBytes = kPageSize * kHeadDim;
     static constexpr bool kScaled = true;
     struct Buf {
         uint4 k[2];
         uint2 v[4];
     };
     __device__ static int q_dim(int i, int kg) { return (i >> 1) * 64 + 16 * kg + (i & 1) * 8; }
-    __device__ static void load(Buf& b, const uint8_t* ks, const uint8_t* vs, int lane)
+    __device__ static void load(Buf& b, const uint8_t* ks, const uint8_t* vs, int lane, int row)
     {
-        const int koff = (lane & 15) * kHeadDim + 16 * (lane >> 4);
+        const int koff = (lane & 15) * row + 16 * (lane >> 4);
         b.k[0] = load_stream16(ks + koff);
         b.k[1] = load_stream16(ks + koff + 64);
+        const int voff = (lane >> 4) * row + 8 * (lane & 15);
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-            b.v[i] = load_stream8(vs + lane * 8 + 512 * i);
+            b.v[i] = load_stream8(vs + 4 * row * i + voff);
     }
     // Two e4m3 codes (bytes 2*HI, 2*HI+1 of x) as a bf16 pair; exact.
     template <bool HI>
@@ -418,8 +422,8 @@ __attribute__((amdgpu_waves_per_eu(G > 4 ? 2 : 3))) void split_mfma(SplitArgs a)
 
     auto issue = [&](typename KV::Buf& buf, int i) {
         const int64_t page = __builtin_amdgcn_readlane(my_page, i);
-        KV::load(buf, slab_base(a.k_pool, page, a.num_kv_heads, t.kvh, KV::kSlabBytes),
-                 slab_base(a.v_pool, page, a.num_kv_heads, t.kvh, KV::kSlabBytes), lane);
+        KV::load(buf, slab_base(a, a.k_pool, page, t.kvh), slab_base(a, a.v_pool, page, t.kvh),
+                 lane, a.row_bytes);
     };
 
     auto consume = [&](typename KV::Buf& buf, int i) {
@@ -579,17 +583,18 @@ __global__ __launch_bounds__(kWave * kUnitWaves) void split_valu_bf16(SplitArgs 
             acc[g][d] = 0.0f;
     }
 
-    const int off = lane * 16;
+    const int off = r * a.row_bytes + 16 * c;
+    const int step = 4 * a.row_bytes;
     auto issue = [&](KvBf16::Buf& buf, int i) {
         const int64_t page = __builtin_amdgcn_readlane(my_page, i);
-        const uint8_t* ks = slab_base(a.k_pool, page, a.num_kv_heads, t.kvh, kSlabBytesBf16);
-        const uint8_t* vs = slab_base(a.v_pool, page, a.num_kv_heads, t.kvh, kSlabBytesBf16);
+        const uint8_t* ks = slab_base(a, a.k_pool, page, t.kvh);
+        const uint8_t* vs = slab_base(a, a.v_pool, page, t.kvh);
 #pragma unroll
         for (int k = 0; k < 4; ++k)
-            buf.k[k] = load_stream16(ks + off + 1024 * k);
+            buf.k[k] = load_stream16(ks + step * k + off);
 #pragma unroll
         for (int k = 0; k < 4; ++k)
-            buf.v[k] = load_stream16(vs + off + 1024 * k);
+            buf.v[k] = load_stream16(vs + step * k + off);
     };
 
     auto consume = [&](KvBf16::Buf& buf, int i) {
@@ -816,6 +821,9 @@ rl_da_status check_config(const rl_da_config* cfg, int* split_tokens, int* split
         return RL_DA_ERR_INVALID_ARG;
     if (cfg->kv_dtype != RL_DA_KV_BF16 && cfg->kv_dtype != RL_DA_KV_FP8_E4M3)
         return RL_DA_ERR_INVALID_ARG;
+    PoolStrides ps;
+    if (!pool_strides(cfg->layout, cfg->num_kv_heads, 1, &ps))
+        return RL_DA_ERR_INVALID_ARG;
     const int G = cfg->num_q_heads / cfg->num_kv_heads;
     if (cfg->head_dim != kHeadDim || cfg->page_size != kPageSize ||
         (G != 1 && G != 2 && G != 4 && G != 8))
@@ -993,6 +1001,11 @@ rl_da_status rl_decode_attn_run(rl_decode_attn* h, const void* q, const void* k_
     sa.ws_ml = h->ws_ml;
     sa.dev_error = h->dev_error;
     sa.num_pages = num_pages;
+    PoolStrides ps;
+    (void)pool_strides(cfg.layout, cfg.num_kv_heads, fp8 ? 1 : 2, &ps);  // checked at create
+    sa.page_bytes = ps.page;
+    sa.head_bytes = ps.head;
+    sa.row_bytes = ps.row;
     sa.num_q_heads = cfg.num_q_heads;
     sa.num_kv_heads = cfg.num_kv_heads;
     sa.max_pages = max_pages;

@@ -33,6 +33,9 @@ struct ExtendArgs {
     const int32_t* block_table;
     const int32_t* seq_lens;
     uint16_t* out;              // bf16 [T][Hq][D]
+    int64_t page_bytes;         // pool strides in bytes: per page,
+    int32_t head_bytes;         //   per kv head within a page,
+    int32_t row_bytes;          //   per token slot within a slab
     int32_t num_q_heads;
     int32_t num_kv_heads;
     int32_t max_pages;
@@ -107,11 +110,11 @@ __global__ __launch_bounds__(kWave * kUnitWaves) void extend_bf16(ExtendArgs a)
     // Staging: thread t moves 16 bytes of K and of V: token t/16, dims 8(t%16)..+8.
     const int st_tok = threadIdx.x / 16, st_dim = (threadIdx.x % 16) * 8;
     const int32_t* bt = a.block_table + (int64_t)b * a.max_pages;
+    const int64_t st_off = (int64_t)kvh * a.head_bytes + st_tok * a.row_bytes + 2 * st_dim;
     auto fetch = [&](int j, uint4& kr, uint4& vr) {
-        const int64_t page = bt[j];
-        const int64_t off = ((page * a.num_kv_heads + kvh) * kPageSize + st_tok) * kHeadDim + st_dim;
-        kr = load_stream16(a.k_pool + 2 * off);
-        vr = load_stream16(a.v_pool + 2 * off);
+        const int64_t off = bt[j] * a.page_bytes + st_off;
+        kr = load_stream16(a.k_pool + off);
+        vr = load_stream16(a.v_pool + off);
     };
     uint4 kr, vr;
     fetch(0, kr, vr);
@@ -221,8 +224,8 @@ rl_da_status rl_extend_attn(const void* q, const int32_t* q_start, int32_t max_q
                             const float* v_scale, int64_t num_pages, const int32_t* block_table,
                             int32_t max_pages, const int32_t* seq_lens, int32_t batch,
                             int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
-                            int32_t page_size, int32_t kv_dtype, float scale, void* out,
-                            void* stream)
+                            int32_t page_size, int32_t kv_dtype, int32_t layout, float scale,
+                            void* out, void* stream)
 {
     if (q == nullptr || q_start == nullptr || k_pool == nullptr || v_pool == nullptr ||
         block_table == nullptr || seq_lens == nullptr || out == nullptr)
@@ -236,6 +239,9 @@ rl_da_status rl_extend_attn(const void* q, const int32_t* q_start, int32_t max_q
         (v_scale != nullptr) != (kv_dtype == RL_DA_KV_FP8_E4M3))
         return RL_DA_ERR_INVALID_ARG;
     if (!aligned16(q) || !aligned16(k_pool) || !aligned16(v_pool) || !aligned16(out))
+        return RL_DA_ERR_INVALID_ARG;
+    PoolStrides ps;
+    if (!pool_strides(layout, num_kv_heads, 2, &ps))
         return RL_DA_ERR_INVALID_ARG;
     const int G = num_q_heads / num_kv_heads;
     if (head_dim != kHeadDim || page_size != kPageSize || kv_dtype != RL_DA_KV_BF16 ||
@@ -252,6 +258,9 @@ rl_da_status rl_extend_attn(const void* q, const int32_t* q_start, int32_t max_q
     ea.block_table = block_table;
     ea.seq_lens = seq_lens;
     ea.out = (uint16_t*)out;
+    ea.page_bytes = ps.page;
+    ea.head_bytes = ps.head;
+    ea.row_bytes = ps.row;
     ea.num_q_heads = num_q_heads;
     ea.num_kv_heads = num_kv_heads;
     ea.max_pages = max_pages;

@@ -11,9 +11,11 @@ The shapes follow the paper's rollout workload (Sec. 7.1: Qwen3-8B rollouts,
 beyond 4k tokens).  The paper's datasets are not used; attention cost depends
 only on shapes and lengths, and values are N(0, 1).
 
-Pool layout is [num_pages][num_kv_heads][page_size][head_dim]; pages are
-drawn from one random permutation of the whole pool and sequence b takes the
-next ceil(L_b / page_size) entries for its logical pages 0, 1, ...
+Pool layout is [num_pages][num_kv_heads][page_size][head_dim] ("hnd"), or
+[num_pages][page_size][num_kv_heads][head_dim] ("nhd": the same values, only
+stored in that order); pages are drawn from one random permutation of the
+whole pool and sequence b takes the next ceil(L_b / page_size) entries for its
+logical pages 0, 1, ...
 """
 from __future__ import annotations
 
@@ -80,9 +82,10 @@ class DecodeProblem:
     head_dim: int
     page_size: int
     kv_dtype: str               # "bf16" or "fp8_e4m3"
+    layout: str                 # "hnd" or "nhd"
     scale: float
     q: torch.Tensor             # bf16 [B, Hq, D]
-    k_pool: torch.Tensor        # bf16 or uint8 (e4m3 codes) [P, Hkv, page, D]
+    k_pool: torch.Tensor        # bf16 or uint8 (e4m3 codes) [P, Hkv, page, D] or [P, page, Hkv, D]
     v_pool: torch.Tensor
     k_scale: Optional[torch.Tensor]   # fp32 [P, Hkv] (fp8 only)
     v_scale: Optional[torch.Tensor]
@@ -134,7 +137,7 @@ class DecodeProblem:
                    v_pool=bits(self.v_pool),
                    block_table=self.block_table.cpu().numpy(),
                    seq_lens=self.seq_lens.cpu().numpy(),
-                   num_kv_heads=self.num_kv_heads, scale=self.scale)
+                   num_kv_heads=self.num_kv_heads, scale=self.scale, layout=self.layout)
         if self.kv_dtype != "bf16":
             out["k_scale"] = self.k_scale.cpu().numpy()
             out["v_scale"] = self.v_scale.cpu().numpy()
@@ -236,8 +239,11 @@ def make_problem(name: str = "custom", *, batch: int, num_q_heads: int,
                  lengths, kv_dtype: str = "bf16", seed: int = 0,
                  pool_pages: Optional[int] = None, pool_factor: float = 1.25,
                  max_pages: Optional[int] = None, scale: Optional[float] = None,
-                 device="cpu") -> DecodeProblem:
-    """Build one seeded problem.  `lengths` is a distribution spec or an array."""
+                 layout: str = "hnd", device="cpu") -> DecodeProblem:
+    """Build one seeded problem.  `lengths` is a distribution spec or an array.
+    The values do not depend on `layout`."""
+    if layout not in ("hnd", "nhd"):
+        raise ValueError("layout must be 'hnd' or 'nhd'")
     rng = np.random.default_rng(seed)
     if isinstance(lengths, (list, tuple)) and lengths and isinstance(lengths[0], str):
         L = draw_lengths(rng, batch, lengths)
@@ -263,24 +269,28 @@ def make_problem(name: str = "custom", *, batch: int, num_q_heads: int,
         v_scale = vs.view(P, num_kv_heads)
     else:
         raise ValueError("kv_dtype must be 'bf16' or 'fp8_e4m3'")
+    if layout == "nhd":
+        k_pool = k_pool.transpose(1, 2).contiguous()
+        v_pool = v_pool.transpose(1, 2).contiguous()
     if scale is None:
         scale = 1.0 / math.sqrt(head_dim)
     return DecodeProblem(
         name=name, seed=int(seed), batch=batch, num_q_heads=num_q_heads,
         num_kv_heads=num_kv_heads, head_dim=head_dim, page_size=page_size,
-        kv_dtype=kv_dtype, scale=float(scale), q=q, k_pool=k_pool,
+        kv_dtype=kv_dtype, layout=layout, scale=float(scale), q=q, k_pool=k_pool,
         v_pool=v_pool, k_scale=k_scale, v_scale=v_scale,
         block_table=torch.from_numpy(table).to(device),
         seq_lens=torch.from_numpy(L.astype(np.int32)).to(device),
         pad_page=pad)
 
 
-def make_config(name: str, device="cpu", seed: Optional[int] = None) -> DecodeProblem:
-    """One of the named workloads, generated on `device`."""
+def make_config(name: str, device="cpu", seed: Optional[int] = None,
+                layout: str = "hnd") -> DecodeProblem:
+    """One of the named workloads, generated on `device`, pools in `layout`."""
     cfg = dict(CONFIGS[name])
     cfg_seed = cfg.pop("seed")
     return make_problem(name, seed=cfg_seed if seed is None else seed,
-                        device=device, **cfg)
+                        device=device, layout=layout, **cfg)
 
 
 def describe(name: str) -> str:

@@ -40,6 +40,26 @@ def test_library_needs_no_torch():
     assert not [n for n in needed if "torch" in n or "c10" in n], needed
 
 
+def test_config_struct_matches_the_header(tmp_path):
+    """ctypes' rl_da_config has the C struct's size and field offsets."""
+    import subprocess
+    fields = [f for f, _ in B.rl_da_config._fields_]
+    src = tmp_path / "offsets.c"
+    src.write_text(
+        "#include <stddef.h>\n#include <stdio.h>\n#include \"rl_decode_attn.h\"\n"
+        "int main(void) {\n  printf(\"%zu\", sizeof(rl_da_config));\n" +
+        "".join('  printf(" %%zu", offsetof(rl_da_config, %s));\n' % f for f in fields) +
+        "  return 0;\n}\n")
+    exe = tmp_path / "offsets"
+    subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)],
+                   check=True)
+    got = [int(x) for x in subprocess.run([str(exe)], stdout=subprocess.PIPE,
+                                          check=True).stdout.split()]
+    want = [ctypes.sizeof(B.rl_da_config)] + [getattr(B.rl_da_config, f).offset
+                                              for f in fields]
+    assert got == want
+
+
 def test_status_strings():
     assert B.rl_da_status_string(B.RL_DA_OK) == "ok"
     for s in (1, 2, 3, 4):
@@ -81,6 +101,7 @@ def test_workspace_size_formula():
     (dict(split_tokens=-16), B.RL_DA_ERR_INVALID_ARG),
     (dict(flags=0x80), B.RL_DA_ERR_INVALID_ARG),
     (dict(kv_dtype=7), B.RL_DA_ERR_INVALID_ARG),
+    (dict(layout=2), B.RL_DA_ERR_INVALID_ARG),
     (dict(head_dim=64), B.RL_DA_ERR_UNSUPPORTED),
     (dict(page_size=32), B.RL_DA_ERR_UNSUPPORTED),
     (dict(num_q_heads=24, num_kv_heads=8), B.RL_DA_ERR_UNSUPPORTED),   # G = 3

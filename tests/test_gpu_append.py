@@ -16,12 +16,13 @@ from gpu_util import KV, bf16_to_f64, check_close, device, oracle_ref, run_gpu
 pytestmark = pytest.mark.gpu
 
 
-def grown_problem(kv, lengths, steps, seed, hq=8, hkv=2):
+def grown_problem(kv, lengths, steps, seed, hq=8, hkv=2, layout="hnd"):
     """Pages for lengths + steps tokens are in the table already; seq_lens
     start at lengths."""
     p = workloads.make_problem("append", batch=len(lengths), num_q_heads=hq,
                                num_kv_heads=hkv, lengths=[L + steps for L in lengths],
-                               kv_dtype=kv, seed=seed, pool_factor=1.5).to(device())
+                               kv_dtype=kv, seed=seed, pool_factor=1.5,
+                               layout=layout).to(device())
     p.seq_lens.copy_(torch.tensor(lengths, dtype=torch.int32, device=device()))
     return p
 
@@ -39,11 +40,13 @@ def host_bits(t):
     return t.view(torch.int16).numpy().view(np.uint16)
 
 
+@pytest.mark.parametrize("layout", ["hnd", "nhd"])
 @pytest.mark.parametrize("kv", ["bf16", "fp8_e4m3"])
-def test_append_steps_match_oracle_byte_for_byte(kv):
+def test_append_steps_match_oracle_byte_for_byte(kv, layout):
     lengths = [0, 1, 14, 15, 16, 31, 100, 4095, 4096, 5000]
     steps = 20
-    p = grown_problem(kv, lengths, steps, seed=21)
+    p = grown_problem(kv, lengths, steps, seed=21, hkv=2 if layout == "hnd" else 4,
+                      hq=8, layout=layout)
     h = p.host_arrays()
     ok, ov = h["k_pool"], h["v_pool"]
     oks, ovs = h.get("k_scale"), h.get("v_scale")
@@ -54,7 +57,7 @@ def test_append_steps_match_oracle_byte_for_byte(kv):
         B.kv_append(p, k.to(device()), v.to(device()))
         ok, ov, oks, ovs = oracle.kv_append(host_bits(k), host_bits(v), ok, ov,
                                             h["block_table"], lens, kv_dtype=KV[kv],
-                                            k_scale=oks, v_scale=ovs)
+                                            k_scale=oks, v_scale=ovs, layout=layout)
         p.seq_lens += 1
         torch.cuda.synchronize()
         got = p.host_arrays()
@@ -67,7 +70,7 @@ def test_append_steps_match_oracle_byte_for_byte(kv):
     ref = oracle.decode_attention(
         got["q_bits"], ok, ov, h["block_table"], p.seq_lens.cpu().numpy(),
         num_kv_heads=p.num_kv_heads, scale=p.scale, kv_dtype=KV[kv], k_scale=oks,
-        v_scale=ovs)
+        v_scale=ovs, layout=layout)
     print(check_close(bf16_to_f64(run_gpu(p)), ref, "attention after appends " + kv))
 
 
@@ -113,5 +116,6 @@ def test_append_argument_validation():
     assert call(head_dim=64) == B.RL_DA_ERR_UNSUPPORTED
     assert call(page_size=32) == B.RL_DA_ERR_UNSUPPORTED
     assert call(kv_dtype=5) == B.RL_DA_ERR_INVALID_ARG
+    assert call(layout=2) == B.RL_DA_ERR_INVALID_ARG
     assert call(batch=0) == B.RL_DA_OK
     torch.cuda.synchronize()

@@ -14,10 +14,11 @@ from gpu_util import bf16_to_f64, check_close, device
 pytestmark = pytest.mark.gpu
 
 
-def extend_problem(new, prior, seed, hq=8, hkv=2):
+def extend_problem(new, prior, seed, hq=8, hkv=2, layout="hnd"):
     lengths = [a + b for a, b in zip(new, prior)]
     p = workloads.make_problem("ext", batch=len(new), num_q_heads=hq, num_kv_heads=hkv,
-                               lengths=lengths, seed=seed, pool_factor=1.25).to(device())
+                               lengths=lengths, seed=seed, pool_factor=1.25,
+                               layout=layout).to(device())
     gen = torch.Generator().manual_seed(seed + 3)
     q = torch.randn((int(sum(new)), hq, 128), generator=gen).to(torch.bfloat16).to(device())
     q_start = torch.tensor(np.concatenate([[0], np.cumsum(new)]), dtype=torch.int32,
@@ -44,7 +45,8 @@ def oracle_extend(p, q, q_start):
     return oracle.extend_attention(q.cpu().view(torch.int16).numpy().view(np.uint16),
                                    q_start.cpu().numpy(), h["k_pool"], h["v_pool"],
                                    h["block_table"], h["seq_lens"],
-                                   num_kv_heads=p.num_kv_heads, scale=p.scale)
+                                   num_kv_heads=p.num_kv_heads, scale=p.scale,
+                                   layout=p.layout)
 
 
 CASES = [
@@ -128,5 +130,18 @@ def test_extend_argument_validation():
     assert call(k_scale=p.seq_lens) == B.RL_DA_ERR_INVALID_ARG
     assert call(head_dim=64) == B.RL_DA_ERR_UNSUPPORTED
     assert call(num_q_heads=6) == B.RL_DA_ERR_UNSUPPORTED
+    assert call(layout=3) == B.RL_DA_ERR_INVALID_ARG
     assert call(max_q_per_seq=0) == B.RL_DA_OK
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("hq,hkv", [(8, 2), (32, 8), (4, 1)])
+def test_extend_nhd_pools_match_oracle_and_the_hnd_result(hq, hkv):
+    new, prior = CASES[0]
+    pn, q, q_start = extend_problem(new, prior, seed=40 + hq, hq=hq, hkv=hkv, layout="nhd")
+    ph, _, _ = extend_problem(new, prior, seed=40 + hq, hq=hq, hkv=hkv)
+    got = run_extend(pn, q, q_start, max(new))
+    print(check_close(bf16_to_f64(got), oracle_extend(pn, q, q_start),
+                      "extend nhd G=%d" % (hq // hkv), extra_abs=p_split_bound(pn)))
+    same = run_extend(ph, q, q_start, max(new))
+    assert torch.equal(got.view(torch.int16), same.view(torch.int16))

@@ -34,23 +34,28 @@ def f64_to_bf16_bits(x):
     return (u >> 16).astype(np.uint16)
 
 
-def decode_pool(arr, kv_dtype, scales):
+def decode_pool(arr, kv_dtype, scales, layout="hnd"):
     if kv_dtype == oracle.KV_BF16:
         return bf16_bits_to_f64(arr)
     vals = torch.from_numpy(arr.copy()).view(torch.float8_e4m3fn).to(
         torch.float64).numpy()
-    return vals * scales.astype(np.float64)[:, :, None, None]
+    sc = scales.astype(np.float64)
+    # scales are [page][kv head]; the kv-head axis is 1 (hnd) or 2 (nhd)
+    return vals * (sc[:, :, None, None] if layout == "hnd" else sc[:, None, :, None])
 
 
-def dense_bruteforce(h, kv_dtype=oracle.KV_BF16):
+def dense_bruteforce(h, kv_dtype=oracle.KV_BF16, layout="hnd"):
     """Independent dense reference: gather with fancy indexing, repeat heads,
     einsum, max-subtracted softmax."""
     q = bf16_bits_to_f64(h["q_bits"])
-    K = decode_pool(h["k_pool"], kv_dtype, h.get("k_scale"))
-    V = decode_pool(h["v_pool"], kv_dtype, h.get("v_scale"))
+    K = decode_pool(h["k_pool"], kv_dtype, h.get("k_scale"), layout)
+    V = decode_pool(h["v_pool"], kv_dtype, h.get("v_scale"), layout)
     bt, lens = h["block_table"], h["seq_lens"]
     B, Hq, D = q.shape
-    Hkv, page = K.shape[1], K.shape[2]
+    if layout == "hnd":
+        Hkv, page = K.shape[1], K.shape[2]
+    else:
+        page, Hkv = K.shape[1], K.shape[2]
     G = Hq // Hkv
     out = np.zeros((B, Hq, D))
     for b in range(B):
@@ -59,8 +64,12 @@ def dense_bruteforce(h, kv_dtype=oracle.KV_BF16):
             continue
         t = np.arange(L)
         pages = bt[b, t // page]
-        Kb = K[pages, :, t % page, :]            # [L, Hkv, D]
-        Vb = V[pages, :, t % page, :]
+        if layout == "hnd":
+            Kb = K[pages, :, t % page, :]        # [L, Hkv, D]
+            Vb = V[pages, :, t % page, :]
+        else:
+            Kb = K[pages, t % page, :, :]
+            Vb = V[pages, t % page, :, :]
         Kh = np.repeat(Kb, G, axis=1)            # [L, Hq, D]
         Vh = np.repeat(Vb, G, axis=1)
         s = np.einsum("hd,thd->ht", q[b], Kh) * h["scale"]
@@ -73,7 +82,7 @@ def dense_bruteforce(h, kv_dtype=oracle.KV_BF16):
 
 def run_oracle(h, kv_dtype=oracle.KV_BF16, rows=None):
     kw = dict(num_kv_heads=h["num_kv_heads"], scale=h["scale"],
-              kv_dtype=kv_dtype, rows=rows)
+              kv_dtype=kv_dtype, rows=rows, layout=h.get("layout", "hnd"))
     if kv_dtype == oracle.KV_FP8_E4M3:
         kw.update(k_scale=h["k_scale"], v_scale=h["v_scale"])
     return oracle.decode_attention(h["q_bits"], h["k_pool"], h["v_pool"],
@@ -117,6 +126,35 @@ def test_matches_dense_bruteforce(shape, seed, kv):
     got = run_oracle(h, KV[kv])
     want = dense_bruteforce(h, KV[kv])
     np.testing.assert_allclose(got, want, rtol=1e-12, atol=1e-14)
+
+
+@pytest.mark.parametrize("kv", ["bf16", "fp8_e4m3"])
+@pytest.mark.parametrize("shape", SHAPES)
+def test_token_major_pools_match_dense_bruteforce(shape, kv):
+    """[page][slot][kv head][dim] pools: the brute force indexes them directly."""
+    batch, hq, hkv, d, page, lengths = shape
+    lens = lengths if lengths[0] != "explicit" else list(lengths[1])
+    p = workloads.make_problem("nhd", batch=batch, num_q_heads=hq, num_kv_heads=hkv,
+                               head_dim=d, page_size=page, lengths=lens, kv_dtype=kv,
+                               seed=7, layout="nhd")
+    h = p.host_arrays()
+    assert h["k_pool"].shape[1:] == (page, hkv, d)
+    got = run_oracle(h, KV[kv])
+    want = dense_bruteforce(h, KV[kv], layout="nhd")
+    np.testing.assert_allclose(got, want, rtol=1e-12, atol=1e-14)
+
+
+@pytest.mark.parametrize("kv", ["bf16", "fp8_e4m3"])
+def test_layouts_store_the_same_values_and_give_the_same_result(kv):
+    """The two layouts of one seeded problem hold the same values, and the
+    oracle reads them in the same order, so the results are bit-identical."""
+    kw = dict(batch=4, num_q_heads=8, num_kv_heads=4, head_dim=16, page_size=4,
+              lengths=[0, 1, 9, 30], kv_dtype=kv, seed=8)
+    a = workloads.make_problem("hnd", **kw).host_arrays()
+    b = workloads.make_problem("nhd", layout="nhd", **kw).host_arrays()
+    assert np.array_equal(a["k_pool"].transpose(0, 2, 1, 3), b["k_pool"])
+    assert np.array_equal(a["v_pool"].transpose(0, 2, 1, 3), b["v_pool"])
+    assert np.array_equal(run_oracle(a, KV[kv]), run_oracle(b, KV[kv]))
 
 
 @pytest.mark.parametrize("seed", [3, 4])

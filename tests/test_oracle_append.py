@@ -53,13 +53,13 @@ def test_encoder_ties_and_random_values_match_torch():
     assert bad.size == 0, [(float(xs[i]), hex(got[i]), hex(want[i])) for i in bad[:5]]
 
 
-def _append_problem(seed, kv, lengths, hkv=2, d=16, page=4):
+def _append_problem(seed, kv, lengths, hkv=2, d=16, page=4, layout="hnd"):
     """Pools laid out for lengths + 1 (the engine has already given every
     sequence the page its new token goes to); seq_lens = lengths."""
     p = workloads.make_problem("app", batch=len(lengths), num_q_heads=hkv, num_kv_heads=hkv,
                                head_dim=d, page_size=page,
                                lengths=[L + 1 for L in lengths], kv_dtype=kv, seed=seed,
-                               pool_factor=2.0)
+                               pool_factor=2.0, layout=layout)
     h = p.host_arrays()
     h["seq_lens"] = (h["seq_lens"] - 1).astype(np.int32)
     gen = torch.Generator().manual_seed(seed + 1)
@@ -73,7 +73,7 @@ def _run(h, kn, vn, kv):
     code = oracle.KV_BF16 if kv == "bf16" else oracle.KV_FP8_E4M3
     return oracle.kv_append(kn, vn, h["k_pool"], h["v_pool"], h["block_table"],
                             h["seq_lens"], kv_dtype=code, k_scale=h.get("k_scale"),
-                            v_scale=h.get("v_scale"))
+                            v_scale=h.get("v_scale"), layout=h["layout"])
 
 
 def test_bf16_append_writes_exactly_one_slot_per_head():
@@ -88,6 +88,36 @@ def test_bf16_append_writes_exactly_one_slot_per_head():
         kd[page, :, slot, :] = kn[b]
         vd[page, :, slot, :] = vn[b]
     assert np.array_equal(k2, kd) and np.array_equal(v2, vd)   # nothing else touched
+
+
+def test_bf16_append_to_token_major_pools_writes_one_row_per_head():
+    lengths = [0, 3, 4, 9, 15]
+    p, h, kn, vn = _append_problem(1, "bf16", lengths, layout="nhd")
+    k2, v2, _, _ = _run(h, kn, vn, "bf16")
+    kd, vd = h["k_pool"].copy(), h["v_pool"].copy()
+    for b, L in enumerate(lengths):
+        page, slot = h["block_table"][b, L // 4], L % 4
+        kd[page, slot, :, :] = kn[b]
+        vd[page, slot, :, :] = vn[b]
+    assert np.array_equal(k2, kd) and np.array_equal(v2, vd)
+
+
+@pytest.mark.parametrize("grow", [1.0, 50.0])
+def test_fp8_append_is_the_same_in_both_layouts(grow):
+    """Same tokens into the same values stored in either order: the appended
+    pools are each other's transposes and the scales are equal."""
+    lengths = [0, 5, 6, 11]
+    res = {}
+    for layout in ("hnd", "nhd"):
+        p, h, kn, vn = _append_problem(9, "fp8_e4m3", lengths, layout=layout)
+        big = torch.from_numpy(kn.view(np.int16).copy()).view(torch.bfloat16).float() * grow
+        kn = big.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+        res[layout] = _run(h, kn, vn, "fp8_e4m3")
+    for a, b in zip(res["hnd"][:2], res["nhd"][:2]):
+        assert np.array_equal(a.transpose(0, 2, 1, 3), b)
+    for a, b in zip(res["hnd"][2:], res["nhd"][2:]):
+        assert np.array_equal(a, b)
+    assert not np.array_equal(res["hnd"][2], _append_problem(9, "fp8_e4m3", lengths)[1]["k_scale"])
 
 
 def test_fp8_append_on_an_empty_page_matches_one_token_slab_quantisation():

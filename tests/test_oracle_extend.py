@@ -13,11 +13,11 @@ from paper_2512_22492_amd import workloads
 from test_oracle import bf16_bits_to_f64, decode_pool, run_oracle
 
 
-def extend_problem(seed, new, prior, hq=8, hkv=2, d=16, page=4, kv="bf16"):
+def extend_problem(seed, new, prior, hq=8, hkv=2, d=16, page=4, kv="bf16", layout="hnd"):
     lengths = [a + b for a, b in zip(new, prior)]
     p = workloads.make_problem("ext", batch=len(new), num_q_heads=hq, num_kv_heads=hkv,
                                head_dim=d, page_size=page, lengths=lengths, kv_dtype=kv,
-                               seed=seed, pool_factor=1.5)
+                               seed=seed, pool_factor=1.5, layout=layout)
     h = p.host_arrays()
     T = int(sum(new))
     gen = torch.Generator().manual_seed(seed + 7)
@@ -28,7 +28,8 @@ def extend_problem(seed, new, prior, hq=8, hkv=2, d=16, page=4, kv="bf16"):
 
 
 def run_extend(h, kv=oracle.KV_BF16):
-    kw = dict(num_kv_heads=h["num_kv_heads"], scale=h["scale"], kv_dtype=kv)
+    kw = dict(num_kv_heads=h["num_kv_heads"], scale=h["scale"], kv_dtype=kv,
+              layout=h.get("layout", "hnd"))
     if kv == oracle.KV_FP8_E4M3:
         kw.update(k_scale=h["k_scale"], v_scale=h["v_scale"])
     return oracle.extend_attention(h["q_bits"], h["q_start"], h["k_pool"], h["v_pool"],
@@ -37,8 +38,11 @@ def run_extend(h, kv=oracle.KV_BF16):
 
 def dense_causal(h, kv=oracle.KV_BF16):
     q = bf16_bits_to_f64(h["q_bits"])
-    K = decode_pool(h["k_pool"], kv, h.get("k_scale"))
-    V = decode_pool(h["v_pool"], kv, h.get("v_scale"))
+    layout = h.get("layout", "hnd")
+    K = decode_pool(h["k_pool"], kv, h.get("k_scale"), layout)
+    V = decode_pool(h["v_pool"], kv, h.get("v_scale"), layout)
+    if layout == "nhd":                 # view as [page][kv head][slot][dim]
+        K, V = K.transpose(0, 2, 1, 3), V.transpose(0, 2, 1, 3)
     T, Hq, D = q.shape
     Hkv, page = K.shape[1], K.shape[2]
     G = Hq // Hkv
@@ -63,12 +67,13 @@ def dense_causal(h, kv=oracle.KV_BF16):
     return out
 
 
+@pytest.mark.parametrize("layout", ["hnd", "nhd"])
 @pytest.mark.parametrize("kv", ["bf16", "fp8_e4m3"])
 @pytest.mark.parametrize("new,prior", [([1, 3, 5], [0, 7, 2]), ([8, 1, 0, 12], [4, 0, 9, 1]),
                                        ([17], [40])])
-def test_matches_dense_causal_bruteforce(new, prior, kv):
+def test_matches_dense_causal_bruteforce(new, prior, kv, layout):
     code = oracle.KV_BF16 if kv == "bf16" else oracle.KV_FP8_E4M3
-    p, h = extend_problem(1, new, prior, kv=kv)
+    p, h = extend_problem(1, new, prior, kv=kv, layout=layout)
     np.testing.assert_allclose(run_extend(h, code), dense_causal(h, code), rtol=1e-12,
                                atol=1e-14)
 

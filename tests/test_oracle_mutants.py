@@ -32,8 +32,11 @@ MUTANTS = [
      "const int64_t page = pages[t / p->page_size];\n        const int slot = t % p->page_size;\n        const double w",
      "const int64_t page = pages[0];\n        const int slot = t % p->page_size;\n        const double w"),
     ("token-major pool layout",
-     "(((int64_t)page * p->num_kv_heads + kvh) * p->page_size + slot)",
-     "(((int64_t)page * p->page_size + slot) * p->num_kv_heads + kvh)"),
+     "return ((page * num_kv_heads + kvh) * page_size + slot)",
+     "return ((page * page_size + slot) * num_kv_heads + kvh)"),
+    ("NHD pools read head-major",
+     "return ((page * page_size + slot) * num_kv_heads + kvh)",
+     "return ((page * num_kv_heads + kvh) * page_size + slot)"),
     ("no max subtraction", "scores[t] = exp(scores[t] - smax);",
      "scores[t] = exp(scores[t]);"),
     ("no normalisation", "const double w = scores[t] / z;",
@@ -50,8 +53,10 @@ MUTANTS = [
      "dst[d] += w * pool_element(p, p->v_pool, p->k_scale,"),
     ("bf16 read as low half", "uint32_t u = (uint32_t)bits << 16;",
      "uint32_t u = (uint32_t)bits << 15;"),
-    ("append to the next slot", "codes[slot * D + d] = rl_oracle_e4m3_encode(",
-     "codes[((slot + 1) % P) * D + d] = rl_oracle_e4m3_encode("),
+    ("append to the next slot", "codes[ELEM(slot, d)] = rl_oracle_e4m3_encode(",
+     "codes[ELEM((slot + 1) % P, d)] = rl_oracle_e4m3_encode("),
+    ("bf16 append to the next slot", "dst[ELEM(slot, d)] = src[d];",
+     "dst[ELEM((slot + 1) % P, d)] = src[d];"),
     ("append scale never grows", "s_new = wanted > s_old ? wanted : s_old;",
      "s_new = s_old;"),
     ("append rescale ratio inverted", "const float ratio = s_old / s_new;",
