@@ -22,6 +22,8 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+# PCIe 5.0 x16, one direction: 32 GT/s x 16 lanes x 128/130 / 8
+PCIE5_X16_GBS = 63.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 COPY_CALIBRATION_BYTES = 1 << 30
 
@@ -105,7 +107,8 @@ def parse_args():
     ap.add_argument("--pmc-calibrate", action="store_true",
                     help="launch one plain copy of %d bytes first, so that a counter "
                          "run can scale FETCH_SIZE/WRITE_SIZE" % COPY_CALIBRATION_BYTES)
-    ap.add_argument("--op", choices=["attention", "append", "extend"], default="attention",
+    ap.add_argument("--op", choices=["attention", "append", "extend", "pack", "d2h"],
+                    default="attention",
                     help="attention (the decode step, default), the KV-cache append that "
                          "precedes it, or extend (prefill) attention of --new-tokens per "
                          "sequence after the workload's cached lengths (separate JSON lines "
@@ -314,6 +317,111 @@ def bench_extend(args, dev):
     }
 
 
+# Qwen3-8B weight tensors of one decoder layer, [out, in] (bf16): q, k, v, o
+# projections, gate, up, down, the two layer norms and the q/k norms.
+QWEN3_8B_LAYER = [(4096, 4096), (1024, 4096), (1024, 4096), (4096, 4096), (12288, 4096),
+                  (12288, 4096), (4096, 12288), (4096,), (4096,), (128,), (128,)]
+QWEN3_8B_LAYERS = 36
+QWEN3_8B_VOCAB = 151936
+
+
+def qwen3_8b_shapes(shard=1):
+    """Tensor shapes in layer order (embedding, 36 layers, final norm, lm head);
+    shard > 1 gives one rank's row slice of every matrix (rollout TP)."""
+    def cut(shape):
+        return (shape[0] // shard,) + tuple(shape[1:]) if len(shape) == 2 else shape
+    shapes = [cut((QWEN3_8B_VOCAB, 4096))]
+    for _ in range(QWEN3_8B_LAYERS):
+        shapes += [cut(s) for s in QWEN3_8B_LAYER]
+    return shapes + [(4096,), cut((QWEN3_8B_VOCAB, 4096))]
+
+
+def _weights(shapes, dev, seed):
+    import torch
+    gen = torch.Generator(device=dev).manual_seed(seed)
+    return [torch.empty(s, dtype=torch.bfloat16, device=dev).normal_(generator=gen)
+            for s in shapes]
+
+
+def _time_launches(fn, steps, warmup):
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        fn()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) / steps
+
+
+def bench_pack(args, dev):
+    """Layer-by-layer packing of the Qwen3-8B weights (bf16, 16.4 GB) through a
+    1 GiB device transfer buffer: one step packs every chunk in turn.  HBM
+    traffic is one read and one write of every weight byte."""
+    import torch
+    from paper_2512_22492_amd import binding
+    tensors = _weights(qwen3_8b_shapes(), dev, 7)
+    total = sum(t.numel() * 2 for t in tensors)
+    cap = 1 << 30
+    buf = torch.empty(cap, dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+    with binding.WeightSync(tensors, buf, align=256) as ws:
+        def step():
+            for c in range(ws.num_chunks):
+                ws.pack(c, stream)
+        s = _time_launches(step, args.steps, args.warmup)
+        chunks = ws.num_chunks
+    # plain device copy of one buffer's worth, for the achievable copy rate
+    src = torch.empty(cap, dtype=torch.uint8, device=dev)
+    lib = bench_kernels()
+    copy_s = _time_launches(lambda: lib.rl_bench_copy(buf.data_ptr(), src.data_ptr(), cap,
+                                                      stream.cuda_stream), 10, 2)
+    gbs = total / s / 1e9
+    hbm = 2 * total / s / 1e9
+    return {
+        "metric": "weight-sync pack GB/s of weights (layer by layer into a transfer buffer), 1 GPU",
+        "value": round(gbs, 1), "unit": "GB/s", "higher_is_better": True,
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(s * 1e3, 4),
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "Qwen3-8B weights, %d tensors, %.2f GB, 1 GiB buffer, %d chunks"
+                               % (len(tensors), total / 1e9, chunks)},
+        "roofline": {"bound": "hbm", "achieved": round(hbm, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(hbm / HBM_PEAK_GBS, 4)},
+        "plain_copy_GBs_rw": round(2 * cap / copy_s / 1e9, 1),
+    }
+
+
+def bench_d2h(args, dev):
+    """Checkpoint copy of one rank's shard (the Qwen3-8B weights cut 8 ways,
+    2.05 GB) into pinned host memory with the pack kernel; the runtime's DMA
+    copy of the same number of contiguous bytes is timed beside it."""
+    import torch
+    from paper_2512_22492_amd import binding
+    tensors = _weights(qwen3_8b_shapes(shard=8), dev, 8)
+    total = sum(t.numel() * 2 for t in tensors)
+    cap = (total + 256 * len(tensors) + 4095) // 4096 * 4096
+    host = torch.empty(cap, dtype=torch.uint8, pin_memory=True)
+    stream = torch.cuda.current_stream()
+    with binding.WeightSync(tensors, host, align=256) as ws:
+        assert ws.num_chunks == 1
+        s = _time_launches(lambda: ws.pack(0, stream), args.steps, args.warmup)
+    flat = torch.empty(total, dtype=torch.uint8, device=dev)
+    dma_s = _time_launches(lambda: host[:total].copy_(flat, non_blocking=True), 5, 1)
+    gbs = total / s / 1e9
+    return {
+        "metric": "checkpoint GPU-to-host copy GB/s (pinned host memory), 1 GPU",
+        "value": round(gbs, 2), "unit": "GB/s", "higher_is_better": True,
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(s * 1e3, 3),
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "Qwen3-8B weights / 8 (one rank's shard), %d tensors, %.3f GB"
+                               % (len(tensors), total / 1e9)},
+        "roofline": {"bound": "host-link", "achieved": round(gbs, 2), "peak": PCIE5_X16_GBS,
+                     "unit": "GB/s", "frac": round(gbs / PCIE5_X16_GBS, 4)},
+        "dma_copy_GBs": round(total / dma_s / 1e9, 2),
+    }
+
+
 def traffic_key(args):
     """Entry of the counter file for this workload and pool layout."""
     return args.config if args.layout == "hnd" else args.config + ":" + args.layout
@@ -349,6 +457,12 @@ def main():
           file=sys.stderr, flush=True)
     if args.op == "extend":
         print(json.dumps(bench_extend(args, dev)), flush=True)
+        return
+    if args.op == "pack":
+        print(json.dumps(bench_pack(args, dev)), flush=True)
+        return
+    if args.op == "d2h":
+        print(json.dumps(bench_d2h(args, dev)), flush=True)
         return
     base = workloads.make_config(args.config, device=dev, layout=args.layout)
     replicas = [base]

@@ -44,6 +44,13 @@ EXPORTED = [
     "rl_extend_attn",
     "rl_kv_append",
     "rl_decode_attn_set_timing_events",
+    "rl_ws_plan",
+    "rl_ws_create",
+    "rl_ws_num_chunks",
+    "rl_ws_chunk_bytes",
+    "rl_ws_pack",
+    "rl_ws_unpack",
+    "rl_ws_destroy",
 ]
 
 
@@ -59,6 +66,20 @@ class rl_da_config(ctypes.Structure):
         ("layout", ctypes.c_int32),
         ("split_tokens", ctypes.c_int32),
         ("flags", ctypes.c_uint32),
+    ]
+
+
+class rl_ws_tensor(ctypes.Structure):
+    _fields_ = [("ptr", ctypes.c_void_p), ("nbytes", ctypes.c_uint64)]
+
+
+class rl_ws_piece(ctypes.Structure):
+    _fields_ = [
+        ("tensor", ctypes.c_int32),
+        ("chunk", ctypes.c_int32),
+        ("tensor_offset", ctypes.c_uint64),
+        ("buffer_offset", ctypes.c_uint64),
+        ("nbytes", ctypes.c_uint64),
     ]
 
 
@@ -115,6 +136,23 @@ def load_library():
     lib.rl_kv_append.restype = ctypes.c_int
     lib.rl_decode_attn_set_timing_events.argtypes = [vp, vp, vp]
     lib.rl_decode_attn_set_timing_events.restype = ctypes.c_int
+    u64 = ctypes.c_uint64
+    lib.rl_ws_plan.argtypes = [ctypes.POINTER(u64), i32, u64, u64, ctypes.POINTER(rl_ws_piece),
+                               i64, ctypes.POINTER(i64), ctypes.POINTER(i32)]
+    lib.rl_ws_plan.restype = ctypes.c_int
+    lib.rl_ws_create.argtypes = [ctypes.POINTER(rl_ws_tensor), i32, vp, u64, u64,
+                                 ctypes.POINTER(vp)]
+    lib.rl_ws_create.restype = ctypes.c_int
+    lib.rl_ws_num_chunks.argtypes = [vp, ctypes.POINTER(i32)]
+    lib.rl_ws_num_chunks.restype = ctypes.c_int
+    lib.rl_ws_chunk_bytes.argtypes = [vp, i32, ctypes.POINTER(u64)]
+    lib.rl_ws_chunk_bytes.restype = ctypes.c_int
+    lib.rl_ws_pack.argtypes = [vp, i32, vp]
+    lib.rl_ws_pack.restype = ctypes.c_int
+    lib.rl_ws_unpack.argtypes = [vp, i32, vp]
+    lib.rl_ws_unpack.restype = ctypes.c_int
+    lib.rl_ws_destroy.argtypes = [vp]
+    lib.rl_ws_destroy.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -242,6 +280,113 @@ def kv_append(p, k_new, v_new, device_error=None, stream=None):
 
 def rl_decode_attn_set_timing_events(h, split_begin, split_end) -> int:
     return load_library().rl_decode_attn_set_timing_events(h, split_begin, split_end)
+
+
+def rl_ws_plan(tensor_bytes, capacity, align):
+    """Returns (status, pieces as (tensor, chunk, tensor_offset, buffer_offset,
+    nbytes) tuples, num_chunks)."""
+    lib = load_library()
+    n = len(tensor_bytes)
+    sizes = (ctypes.c_uint64 * max(1, n))(*[int(x) for x in tensor_bytes])
+    np_, nc = ctypes.c_int64(), ctypes.c_int32()
+    rc = lib.rl_ws_plan(sizes, n, int(capacity), int(align), None, 0, ctypes.byref(np_),
+                        ctypes.byref(nc))
+    if rc != RL_DA_OK:
+        return rc, None, None
+    buf = (rl_ws_piece * max(1, np_.value))()
+    rc = lib.rl_ws_plan(sizes, n, int(capacity), int(align), buf, np_.value,
+                        ctypes.byref(np_), ctypes.byref(nc))
+    pieces = [(p.tensor, p.chunk, p.tensor_offset, p.buffer_offset, p.nbytes)
+              for p in buf[:np_.value]]
+    return rc, pieces, nc.value
+
+
+def rl_ws_create(tensors, buffer, capacity, align):
+    """tensors: sequence of (device address, nbytes).  Returns (status, handle)."""
+    arr = (rl_ws_tensor * max(1, len(tensors)))(
+        *[rl_ws_tensor(_ptr(p) if not isinstance(p, int) else p, int(n)) for p, n in tensors])
+    h = ctypes.c_void_p()
+    rc = load_library().rl_ws_create(arr, len(tensors), _ptr(buffer), int(capacity), int(align),
+                                     ctypes.byref(h))
+    return rc, (h.value if rc == RL_DA_OK else None)
+
+
+def rl_ws_num_chunks(h):
+    n = ctypes.c_int32()
+    rc = load_library().rl_ws_num_chunks(h, ctypes.byref(n))
+    return rc, n.value
+
+
+def rl_ws_chunk_bytes(h, chunk):
+    n = ctypes.c_uint64()
+    rc = load_library().rl_ws_chunk_bytes(h, int(chunk), ctypes.byref(n))
+    return rc, n.value
+
+
+def rl_ws_pack(h, chunk, stream=None) -> int:
+    return load_library().rl_ws_pack(h, int(chunk), _stream(stream))
+
+
+def rl_ws_unpack(h, chunk, stream=None) -> int:
+    return load_library().rl_ws_unpack(h, int(chunk), _stream(stream))
+
+
+def rl_ws_destroy(h) -> int:
+    return load_library().rl_ws_destroy(h)
+
+
+class WeightSync:
+    """Owns one packing plan: tensors (torch tensors on the GPU, packed as raw
+    bytes in list order) and a transfer buffer (a uint8 tensor on the GPU or in
+    pinned host memory)."""
+
+    def __init__(self, tensors, buffer, align=256):
+        for t in tensors:
+            if not t.is_contiguous():
+                raise ValueError("tensors must be contiguous")
+        self.tensors = list(tensors)
+        self.buffer = buffer
+        spec = [(t.data_ptr(), t.numel() * t.element_size()) for t in self.tensors]
+        rc, h = rl_ws_create(spec, buffer, buffer.numel() * buffer.element_size(), align)
+        if rc != RL_DA_OK:
+            raise RLDecodeAttnError(rc, "rl_ws_create")
+        self.handle = h
+        rc, self.num_chunks = rl_ws_num_chunks(h)
+        if rc != RL_DA_OK:
+            raise RLDecodeAttnError(rc, "rl_ws_num_chunks")
+
+    def chunk_bytes(self, chunk):
+        rc, n = rl_ws_chunk_bytes(self.handle, chunk)
+        if rc != RL_DA_OK:
+            raise RLDecodeAttnError(rc, "rl_ws_chunk_bytes")
+        return n
+
+    def pack(self, chunk, stream=None):
+        rc = rl_ws_pack(self.handle, chunk, stream)
+        if rc != RL_DA_OK:
+            raise RLDecodeAttnError(rc, "rl_ws_pack")
+
+    def unpack(self, chunk, stream=None):
+        rc = rl_ws_unpack(self.handle, chunk, stream)
+        if rc != RL_DA_OK:
+            raise RLDecodeAttnError(rc, "rl_ws_unpack")
+
+    def close(self):
+        if self.handle is not None:
+            rl_ws_destroy(self.handle)
+            self.handle = None
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 # --------------------------------------------------------- handle wrapper ---

@@ -7,7 +7,7 @@ import subprocess
 PKG_DIR = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG_DIR)
 SOURCES = [os.path.join(PKG_DIR, "csrc", f)
-           for f in ("rl_decode.hip", "rl_extend.hip", "rl_append.hip")]
+           for f in ("rl_decode.hip", "rl_extend.hip", "rl_append.hip", "rl_weight_sync.hip")]
 INCLUDE = os.path.join(ROOT, "include")
 LIB_PATH = os.path.join(PKG_DIR, "librl_decode_attn.so")
 # measurement-only kernels used by bench.py (stream-read ceiling, copy)
