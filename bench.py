@@ -135,9 +135,18 @@ def _pmc_means(path, counter):
     return {k: v[0] / v[1] for k, v in sums.items()}
 
 
-def summarize_pmc(fetch_csv, write_csv, config):
-    """HBM bytes per split-kernel launch, each counter scaled by its reading for
-    the calibration copy (which moves COPY_CALIBRATION_BYTES each way)."""
+# Per measured operation: the kernel whose counters are summarised (name
+# prefix in the profiler's output) and the sources it is built from.
+OP_KERNELS = {
+    "attention": ("void (anonymous namespace)::split_", ("rl_common.h", "rl_decode.hip")),
+    "pack": ("(anonymous namespace)::copy_pieces", ("rl_common.h", "rl_weight_sync.hip")),
+}
+
+
+def summarize_pmc(fetch_csv, write_csv, config, op="attention"):
+    """HBM bytes per launch of the op's kernel, each counter scaled by its
+    reading for the calibration copy (which moves COPY_CALIBRATION_BYTES each
+    way)."""
     fetch = _pmc_means(fetch_csv, "FETCH_SIZE")
     write = _pmc_means(write_csv, "WRITE_SIZE")
 
@@ -149,13 +158,13 @@ def summarize_pmc(fetch_csv, write_csv, config):
 
     copy_kib = COPY_CALIBRATION_BYTES / 1024.0
     copy_name = "(anonymous namespace)::copy_kernel"
-    split_name = "void (anonymous namespace)::split_"
+    split_name = OP_KERNELS[op][0]
     f_scale = copy_kib / pick(fetch, copy_name)
     w_scale = copy_kib / pick(write, copy_name)
     split_f = pick(fetch, split_name)
     split_w = pick(write, split_name)
     entry = {
-        "kernel_source_sha256": kernel_source_sha(),
+        "kernel_source_sha256": kernel_source_sha(op),
         "fetch_kib_raw": split_f, "write_kib_raw": split_w,
         "fetch_scale": f_scale, "write_scale": w_scale,
         "bytes_per_launch": int(round((split_f * f_scale + split_w * w_scale) * 1024)),
@@ -195,17 +204,17 @@ def load_traffic(config, kernel_source_sha):
     return entry.get("bytes_per_launch")
 
 
-def kernel_source_sha():
-    """sha256 over the sources of the decode kernels (shared header first)."""
+def kernel_source_sha(op="attention"):
+    """sha256 over the sources of the op's kernel (shared header first)."""
     import hashlib
     h = hashlib.sha256()
-    for name in ("rl_common.h", "rl_decode.hip"):
+    for name in OP_KERNELS[op][1]:
         with open(os.path.join(ROOT, "paper_2512_22492_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()
 
 
-def cpu_baseline(p, rows_per_call=None):
+def cpu_baseline(p, min_seconds=10.0):
     """Times the oracle on the host.  The sample is the whole step (every
     (sequence, head) row) when that is bounded, else the first sequences."""
     import numpy as np
@@ -219,18 +228,23 @@ def cpu_baseline(p, rows_per_call=None):
     nseq = max(1, min(p.batch, nseq))
     rows = np.array([(b, hh) for b in range(nseq) for hh in range(p.num_q_heads)],
                     dtype=np.int32)
-    t0 = time.perf_counter()
-    oracle.decode_attention(kv_dtype=kv_code, rows=rows, **h)
-    dt = time.perf_counter() - t0
+    # repeat the sample until about min_seconds of CPU work have been timed
+    reps, dt = 0, 0.0
+    while reps == 0 or dt < min_seconds:
+        t0 = time.perf_counter()
+        oracle.decode_attention(kv_dtype=kv_code, rows=rows, **h)
+        dt += time.perf_counter() - t0
+        reps += 1
     elt = 2 if p.kv_dtype == "bf16" else 1
-    kv = int(L[:nseq].sum()) * p.num_kv_heads * p.head_dim * 2 * elt
+    kv = int(L[:nseq].sum()) * p.num_kv_heads * p.head_dim * 2 * elt * reps
     return {
         "value": kv / dt / 1e9,
         "unit": "GB/s",
         "cores": oracle.max_threads(),
         "kind": "oracle",
-        "sample": "%d of %d sequences (%d query-head rows, all tokens), fp64, %.2f s; "
-                  "%.1f query-tokens/s" % (nseq, p.batch, len(rows), dt, nseq / dt),
+        "sample": "%d of %d sequences (%d query-head rows, all tokens), fp64, %d passes "
+                  "in %.2f s; %.1f query-tokens/s" % (nseq, p.batch, len(rows), reps, dt,
+                                                     nseq * reps / dt),
         "seconds": dt,
     }
 
@@ -366,6 +380,8 @@ def bench_pack(args, dev):
     cap = 1 << 30
     buf = torch.empty(cap, dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream()
+    if args.pmc_calibrate:
+        calibrate_counters(dev, stream)
     with binding.WeightSync(tensors, buf, align=256) as ws:
         def step():
             for c in range(ws.num_chunks):
@@ -373,10 +389,12 @@ def bench_pack(args, dev):
         s = _time_launches(step, args.steps, args.warmup)
         chunks = ws.num_chunks
     # plain device copy of one buffer's worth, for the achievable copy rate
-    src = torch.empty(cap, dtype=torch.uint8, device=dev)
-    lib = bench_kernels()
-    copy_s = _time_launches(lambda: lib.rl_bench_copy(buf.data_ptr(), src.data_ptr(), cap,
-                                                      stream.cuda_stream), 10, 2)
+    copy_s = None
+    if not args.no_ceilings:
+        src = torch.empty(cap, dtype=torch.uint8, device=dev)
+        lib = bench_kernels()
+        copy_s = _time_launches(lambda: lib.rl_bench_copy(buf.data_ptr(), src.data_ptr(), cap,
+                                                          stream.cuda_stream), 10, 2)
     gbs = total / s / 1e9
     hbm = 2 * total / s / 1e9
     return {
@@ -387,8 +405,10 @@ def bench_pack(args, dev):
         "config": {"workload": "Qwen3-8B weights, %d tensors, %.2f GB, 1 GiB buffer, %d chunks"
                                % (len(tensors), total / 1e9, chunks)},
         "roofline": {"bound": "hbm", "achieved": round(hbm, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(hbm / HBM_PEAK_GBS, 4)},
-        "plain_copy_GBs_rw": round(2 * cap / copy_s / 1e9, 1),
+                     "unit": "GB/s", "frac": round(hbm / HBM_PEAK_GBS, 4),
+                     "traffic": load_traffic(traffic_key(args), kernel_source_sha("pack")),
+                     "bytes_per_launch": 2 * total // chunks},
+        "plain_copy_GBs_rw": None if copy_s is None else round(2 * cap / copy_s / 1e9, 1),
     }
 
 
@@ -423,8 +443,21 @@ def bench_d2h(args, dev):
 
 
 def traffic_key(args):
-    """Entry of the counter file for this workload and pool layout."""
+    """Entry of the counter file for this workload and pool layout, or op."""
+    if args.op == "pack":
+        return "pack:qwen3_8b_weights"
     return args.config if args.layout == "hnd" else args.config + ":" + args.layout
+
+
+def calibrate_counters(dev, stream):
+    """One plain 16-byte-per-lane copy of COPY_CALIBRATION_BYTES, whose counter
+    readings scale the op kernel's readings."""
+    import torch
+    src = torch.empty(COPY_CALIBRATION_BYTES, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    assert bench_kernels().rl_bench_copy(dst.data_ptr(), src.data_ptr(),
+                                         COPY_CALIBRATION_BYTES, stream.cuda_stream) == 0
+    torch.cuda.synchronize()
 
 
 def _describe(name):
@@ -435,7 +468,7 @@ def _describe(name):
 def main():
     args = parse_args()
     if args.summarize_pmc:
-        summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], traffic_key(args))
+        summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], traffic_key(args), args.op)
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -489,12 +522,7 @@ def main():
     torch.cuda.synchronize()
 
     if args.pmc_calibrate:
-        src = torch.empty(COPY_CALIBRATION_BYTES, dtype=torch.uint8, device=dev)
-        dst = torch.empty_like(src)
-        assert bench_kernels().rl_bench_copy(dst.data_ptr(), src.data_ptr(),
-                                             COPY_CALIBRATION_BYTES, stream.cuda_stream) == 0
-        torch.cuda.synchronize()
-        del src, dst
+        calibrate_counters(dev, stream)
 
     for i in range(args.warmup):
         attn.run_problem(replicas[i % len(replicas)], out, stream)
