@@ -99,6 +99,8 @@ def parse_args():
     ap.add_argument("--split-tokens", type=int, default=0)
     ap.add_argument("--layout", choices=["hnd", "nhd"], default="hnd",
                     help="pool layout: [page][kv head][slot][dim] or [page][slot][kv head][dim]")
+    ap.add_argument("--per-head-units", action="store_true",
+                    help="token-major pools: four-wavefront units per kv head")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-events", action="store_true",
                     help="do not record events around the split kernel (profiling runs)")
@@ -446,7 +448,8 @@ def traffic_key(args):
     """Entry of the counter file for this workload and pool layout, or op."""
     if args.op == "pack":
         return "pack:qwen3_8b_weights"
-    return args.config if args.layout == "hnd" else args.config + ":" + args.layout
+    key = args.config if args.layout == "hnd" else args.config + ":" + args.layout
+    return key + (":per-head" if args.per_head_units and args.layout != "hnd" else "")
 
 
 def calibrate_counters(dev, stream):
@@ -509,6 +512,8 @@ def main():
         return
     out = torch.empty_like(base.q)
     flags = binding.RL_DA_SCORES_ON_VALU if args.scores == "valu" else 0
+    if args.per_head_units:
+        flags |= binding.RL_DA_PER_HEAD_UNITS
     attn = binding.DecodeAttention.for_problem(base, flags=flags,
                                                split_tokens=args.split_tokens)
     split_tokens, num_splits = attn.split_info(base.max_pages)
@@ -572,6 +577,8 @@ def main():
             "page_size": base.page_size, "seq_len_mean": float(base.lengths().mean()),
             "split_tokens": split_tokens, "num_splits": num_splits,
             "scores": args.scores, "replicas": len(replicas), "layout": base.layout,
+            "units": "per-head" if (args.per_head_units or base.layout == "hnd")
+                     else "head-parallel",
         },
         "query_tokens_per_s": round(base.batch / (ms_per_step / 1e3), 1),
         "kv_bytes_per_step": kv_bytes,

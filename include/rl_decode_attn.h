@@ -86,6 +86,14 @@ typedef enum { RL_DA_LAYOUT_HND = 0, RL_DA_LAYOUT_NHD = 1 } rl_da_layout;
  * ALUs instead of packing the query group into an MFMA tile (same results up
  * to fp32 rounding; kept to measure one path against the other). */
 #define RL_DA_SCORES_ON_VALU 0x2u
+/* create() flag for token-major (RL_DA_LAYOUT_NHD) pools.  By default such a
+ * handle runs one work-group per (sequence, split, group of up to 8 kv
+ * heads), one wavefront per kv head, so the group reads each page's token
+ * rows together; with this flag it runs the head-major pools' units instead
+ * (four wavefronts per (sequence, kv head, split) sharing its pages), which
+ * balance better when lengths have a long tail.  No effect on head-major
+ * pools, with RL_DA_SCORES_ON_VALU, or with one kv head per group. */
+#define RL_DA_PER_HEAD_UNITS 0x4u
 
 /* Device error word bits reported by rl_decode_attn_check_error(). */
 #define RL_DA_DEVERR_PAGE_OUT_OF_RANGE 0x1
@@ -104,8 +112,9 @@ typedef struct {
                                /* page_size, at most 4096; 0 = the longest of */
                                /* 4096, 2048, 1024, 512 that cuts max_batch   */
                                /* sequences of max_pages_per_seq pages into   */
-                               /* >= 256 units (a per-handle constant)        */
-    uint32_t flags;            /* RL_DA_CHECKED | RL_DA_SCORES_ON_VALU or 0   */
+                               /* >= 256 work-groups (a per-handle constant)  */
+    uint32_t flags;            /* RL_DA_CHECKED, RL_DA_SCORES_ON_VALU,        */
+                               /* RL_DA_PER_HEAD_UNITS, or 0                  */
 } rl_da_config;
 
 /*

@@ -44,6 +44,10 @@ constexpr int kMinDefaultSplitTokens = 512;
 constexpr int64_t kMinDefaultUnits = 256;
 // each wavefront holds its pages' block-table entries one per lane
 constexpr int kMaxSplitTokens = kWave * kUnitWaves * kPageSize;
+// head-parallel units (token-major pools): up to 8 kv heads per work-group,
+// every wavefront walks all pages of its split
+constexpr int kMaxHeadsPerUnit = 8;
+constexpr int kMaxSplitTokensHp = 4096;
 
 struct SplitArgs {
     const uint16_t* q;          // bf16 bits [B][Hq][D]
@@ -66,6 +70,7 @@ struct SplitArgs {
     int32_t max_pages;
     int32_t split_pages;
     int32_t num_splits;         // ceil(max_pages / split_pages)
+    int32_t heads_per_unit;     // kv heads per head-parallel work-group
     float scale_log2;           // scale * log2(e)
 };
 
@@ -88,7 +93,7 @@ template <bool CHECKED>
 __device__ __forceinline__ bool begin_task(const SplitArgs& a, WaveTask& t, int32_t& my_page)
 {
     t.lane = threadIdx.x % kWave;
-    t.wave = threadIdx.x / kWave;
+    t.wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);  // uniform: scalar
     const int unit = blockIdx.x;
     t.s = unit % a.num_splits;
     const int bk = unit / a.num_splits;
@@ -342,8 +347,6 @@ struct KvFp8 {
 // where some head's max moves.  Results are the same up to fp32 rounding: m
 // cancels in acc / l.
 
-// Three wavefronts per SIMD: the register budget (168) fits both page buffers
-// and the accumulators without spilling.
 // Rows of the 16-row query tile that hold a query head: every 4th row for
 // G <= 4 (one score per lane of the first G lane groups), every 2nd row for
 // G = 8 (two scores per lane).
@@ -354,39 +357,33 @@ struct ScoreRows {
     static constexpr int kLdsHeads = G > 4 ? 8 : 4;  // p/alpha entries per token in LDS
 };
 
-template <int G, bool CHECKED, typename KV>
-__global__ __launch_bounds__(kWave * kUnitWaves)
-__attribute__((amdgpu_waves_per_eu(G > 4 ? 2 : 3))) void split_mfma(SplitArgs a)
+// One wavefront's pass over its pages of one (sequence, kv head): the pages
+// are t.p0 + t.wave + PAGE_STEP * i for the four-wavefront units (at most
+// kWave of them, block-table entries in my_page) and t.p0 + i for the
+// head-parallel units (PAGE_STEP 1, wave index not part of the page), which
+// take their block-table entries kWave pages at a time: my_page holds the
+// first kWave on entry.  On return every lane holds the wave's full acc for
+// dims 8c..8c+7 of all G heads, and lane group kg holds (m, l) of heads
+// head[e].
+template <int G, bool CHECKED, typename KV, int PAGE_STEP>
+__device__ __forceinline__ void attend_pages(const SplitArgs& a, const WaveTask& t,
+                                             int32_t my_page, float* lds_p, float* lds_alpha,
+                                             float (&acc)[G][8],
+                                             float (&m)[ScoreRows<G>::kPerLane],
+                                             float (&l_row)[ScoreRows<G>::kPerLane],
+                                             int (&head)[ScoreRows<G>::kPerLane])
 {
-    static_assert(G == 1 || G == 2 || G == 4 || G == 8, "query group of 1, 2, 4 or 8 heads");
     using SR = ScoreRows<G>;
     constexpr int kE = SR::kPerLane;
     constexpr int kH = SR::kLdsHeads;
-    __shared__ __attribute__((aligned(16))) float lds_p_all[kUnitWaves][kPageSize * kH];
-    __shared__ __attribute__((aligned(16))) float lds_alpha_all[kUnitWaves][kH];
-    __shared__ __attribute__((aligned(16))) UnitShared<G> sh;
-
-    WaveTask t;
-    int32_t my_page;
-    if (!begin_task<CHECKED>(a, t, my_page)) {
-        write_zero_rows<G>(a, t);
-        return;
-    }
-    float* lds_p = lds_p_all[t.wave];          // [token][head]
-    float* lds_alpha = lds_alpha_all[t.wave];
-
     const int lane = t.lane;
     const int n = lane & 15, kg = lane >> 4;  // score layout
-    const int r = lane >> 4, c = lane & 15;   // value layout
+    const int r = lane >> 4;                  // value layout row
     const int h0 = t.kvh * G;
-
-    // Slab scales of this wavefront's pages, one per lane like the pages.
+    constexpr bool kChunked = PAGE_STEP == 1;
+    const int first = kChunked ? t.p0 : t.p0 + t.wave;
+    int c0 = 0;  // wavefront-local index of my_page's first entry
     float my_kscale = 1.0f, my_vscale = 1.0f;
-    if (KV::kScaled && lane < t.count) {
-        const int64_t slab = (int64_t)my_page * a.num_kv_heads + t.kvh;
-        my_kscale = a.k_scale[slab];
-        my_vscale = a.v_scale[slab];
-    }
 
     // Query tile: row kStep*g holds query head g, every other row is zero.
     uint4 qa[4];
@@ -402,18 +399,16 @@ __attribute__((amdgpu_waves_per_eu(G > 4 ? 2 : 3))) void split_mfma(SplitArgs a)
                         : make_uint4(0, 0, 0, 0);
     }
     // Head of this lane's e-th score: tile row 4kg + e*kStep.
-    int head[kE];
 #pragma unroll
     for (int e = 0; e < kE; ++e)
         head[e] = (4 * kg + e * SR::kStep) / SR::kStep;
 
-    float m[kE], lsum[kE];    // reference max (log2 units) and this lane's share of l
+    float lsum[kE];    // this lane's share of l
 #pragma unroll
     for (int e = 0; e < kE; ++e) {
-        m[e] = -INFINITY;
+        m[e] = -INFINITY;    // reference max (log2 units)
         lsum[e] = 0.0f;
     }
-    float acc[G][8];
 #pragma unroll
     for (int g = 0; g < G; ++g)
 #pragma unroll
@@ -426,6 +421,7 @@ __attribute__((amdgpu_waves_per_eu(G > 4 ? 2 : 3))) void split_mfma(SplitArgs a)
                  lane, a.row_bytes);
     };
 
+    // i: index within the current run of my_page entries
     auto consume = [&](typename KV::Buf& buf, int i) {
         // Scores of the 16 tokens of the page for the G query heads.
         floatx4_t sacc = {0.0f, 0.0f, 0.0f, 0.0f};
@@ -435,7 +431,8 @@ __attribute__((amdgpu_waves_per_eu(G > 4 ? 2 : 3))) void split_mfma(SplitArgs a)
                 __builtin_bit_cast(bf16x8_t, qa[k]),
                 __builtin_bit_cast(bf16x8_t, KV::k_block(buf, k)), sacc, 0, 0, 0);
 
-        const int valid = t.seq_len - task_page(t, i) * kPageSize;  // >= 1 valid tokens
+        const int page_idx = first + PAGE_STEP * ((kChunked ? c0 : 0) + i);
+        const int valid = t.seq_len - page_idx * kPageSize;  // >= 1 valid tokens
         float sl = a.scale_log2;
         if (KV::kScaled)
             sl *= __int_as_float(__builtin_amdgcn_readlane(__float_as_int(my_kscale), i));
@@ -517,7 +514,34 @@ __attribute__((amdgpu_waves_per_eu(G > 4 ? 2 : 3))) void split_mfma(SplitArgs a)
     };
 
     typename KV::Buf buf_a, buf_b;
-    stream_pages(t.count, buf_a, buf_b, issue, consume);
+    for (;;) {
+        const int n_here = kChunked ? min(t.count - c0, kWave) : t.count;
+        // slab scales of these pages, one per lane like the pages
+        if (KV::kScaled && lane < n_here) {
+            const int64_t slab = (int64_t)my_page * a.num_kv_heads + t.kvh;
+            my_kscale = a.k_scale[slab];
+            my_vscale = a.v_scale[slab];
+        }
+        stream_pages(n_here, buf_a, buf_b, issue, consume);
+        if (!kChunked)
+            break;
+        c0 += kWave;
+        if (c0 >= t.count)
+            break;
+        // the next kWave block-table entries
+        my_page = c0 + lane < t.count
+                      ? a.block_table[(int64_t)t.b * a.max_pages + t.p0 + c0 + lane]
+                      : 0;
+        if (CHECKED) {
+            const bool bad =
+                c0 + lane < t.count && (my_page < 0 || (int64_t)my_page >= a.num_pages);
+            if (__any(bad)) {
+                if (lane == 0)
+                    atomicOr(a.dev_error, RL_DA_DEVERR_PAGE_OUT_OF_RANGE);
+                break;  // the rest is skipped; the output is unspecified
+            }
+        }
+    }
 
     // Every lane of a value row holds a partial over tokens = r (mod 4); all
     // rows share the reference max, so the partials simply add.
@@ -530,18 +554,161 @@ __attribute__((amdgpu_waves_per_eu(G > 4 ? 2 : 3))) void split_mfma(SplitArgs a)
             v += __shfl_xor(v, 32);
             acc[g][d] = v;
         }
+#pragma unroll
+    for (int e = 0; e < kE; ++e)
+        l_row[e] = row16_sum(lsum[e]);
+}
+
+// Three wavefronts per SIMD (two for G = 8): the register budget fits both
+// page buffers and the accumulators without spilling.
+template <int G, bool CHECKED, typename KV>
+__global__ __launch_bounds__(kWave * kUnitWaves)
+__attribute__((amdgpu_waves_per_eu(G > 4 ? 2 : 3))) void split_mfma(SplitArgs a)
+{
+    static_assert(G == 1 || G == 2 || G == 4 || G == 8, "query group of 1, 2, 4 or 8 heads");
+    using SR = ScoreRows<G>;
+    constexpr int kE = SR::kPerLane;
+    constexpr int kH = SR::kLdsHeads;
+    __shared__ __attribute__((aligned(16))) float lds_p_all[kUnitWaves][kPageSize * kH];
+    __shared__ __attribute__((aligned(16))) float lds_alpha_all[kUnitWaves][kH];
+    __shared__ __attribute__((aligned(16))) UnitShared<G> sh;
+
+    WaveTask t;
+    int32_t my_page;
+    if (!begin_task<CHECKED>(a, t, my_page)) {
+        write_zero_rows<G>(a, t);
+        return;
+    }
+    float acc[G][8], m[kE], l_row[kE];
+    int head[kE];
+    attend_pages<G, CHECKED, KV, kUnitWaves>(a, t, my_page, lds_p_all[t.wave],
+                                             lds_alpha_all[t.wave], acc, m, l_row, head);
     // Lane group kg holds m and l of heads head[e]; its value lanes (r = kg)
     // stash those heads.
+    const int c = t.lane & 15;
 #pragma unroll
     for (int e = 0; e < kE; ++e) {
-        const float l_row = row16_sum(lsum[e]);
 #pragma unroll
         for (int g = 0; g < G; ++g)
             if (g == head[e])
-                stash_state<G>(sh, t.wave, g, c, acc[g], m[e], l_row);
+                stash_state<G>(sh, t.wave, g, c, acc[g], m[e], l_row[e]);
     }
     __syncthreads();
     merge_unit<G>(a, t, sh);
+}
+
+// ------------------------------------- head-parallel split kernel, MFMA QK ---
+//
+// For token-major pools, where a (page, kv head) slab is 16 rows spread over
+// the page, the four-wavefront unit of one kv head reads 256-byte pieces
+// (128 for e4m3) of pages whose other heads are read by other units at other
+// times.  Here one work-group covers (sequence, split, group of kHeadsPerUnit
+// consecutive kv heads): wavefront w owns kv head group * kHeadsPerUnit + w
+// and walks every page of the split, so the group's wavefronts read each
+// page's token rows together (one contiguous run per row).  No merge inside
+// the unit: each wavefront finishes its own heads, or writes one partial per
+// split for the merge kernel.
+
+template <bool CHECKED>
+__device__ __forceinline__ bool begin_task_hp(const SplitArgs& a, WaveTask& t, int32_t& my_page)
+{
+    t.lane = threadIdx.x % kWave;
+    t.wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);  // uniform: scalar
+    const int unit = blockIdx.x;
+    t.s = unit % a.num_splits;
+    const int bg = unit / a.num_splits;
+    const int groups = a.num_kv_heads / a.heads_per_unit;
+    t.kvh = __builtin_amdgcn_readfirstlane((bg % groups) * a.heads_per_unit + t.wave);
+    t.b = bg / groups;
+    t.p0 = t.s * a.split_pages;
+    // the first kWave pages' block-table entries (later ones are loaded as
+    // the wavefront reaches them)
+    const int col = t.p0 + t.lane;
+    const bool in_split = t.lane < a.split_pages && col < a.max_pages;
+    my_page = in_split ? a.block_table[(int64_t)t.b * a.max_pages + col] : 0;
+    int L = __builtin_amdgcn_readfirstlane(a.seq_lens[t.b]);  // uniform: scalar
+    const int cap = a.max_pages * kPageSize;
+    if (L > cap) {
+        if (CHECKED && t.lane == 0 && t.s == 0 && t.kvh == 0)
+            atomicOr(a.dev_error, RL_DA_DEVERR_LENGTH_TOO_LONG);
+        L = cap;
+    }
+    t.seq_len = L;
+    t.npages = L > 0 ? (L + kPageSize - 1) / kPageSize : 0;
+    t.nsplit = (t.npages + a.split_pages - 1) / a.split_pages;
+    const int p1 = min(t.p0 + a.split_pages, t.npages);
+    if (t.p0 >= p1)
+        return false;
+    t.count = p1 - t.p0;
+    if (CHECKED) {
+        const bool bad = t.lane < min(t.count, kWave) &&
+                         (my_page < 0 || (int64_t)my_page >= a.num_pages);
+        if (__any(bad)) {
+            if (t.lane == 0)
+                atomicOr(a.dev_error, RL_DA_DEVERR_PAGE_OUT_OF_RANGE);
+            t.count = 0;  // read nothing; the wavefront's output is unspecified
+        }
+    }
+    return true;
+}
+
+// A work-group of up to eight wavefronts fills two waves per SIMD, so the
+// kernel may use the two-wave register budget.
+template <int G, bool CHECKED, typename KV>
+__global__ __launch_bounds__(kWave * kMaxHeadsPerUnit)
+__attribute__((amdgpu_waves_per_eu(2))) void split_mfma_hp(SplitArgs a)
+{
+    static_assert(G == 1 || G == 2 || G == 4 || G == 8, "query group of 1, 2, 4 or 8 heads");
+    using SR = ScoreRows<G>;
+    constexpr int kE = SR::kPerLane;
+    constexpr int kH = SR::kLdsHeads;
+    __shared__ __attribute__((aligned(16))) float lds_p_all[kMaxHeadsPerUnit][kPageSize * kH];
+    __shared__ __attribute__((aligned(16))) float lds_alpha_all[kMaxHeadsPerUnit][kH];
+
+    WaveTask t;
+    int32_t my_page;
+    if (!begin_task_hp<CHECKED>(a, t, my_page)) {
+        // an empty sequence produces zeros, written by the first split
+        if (t.npages == 0 && t.s == 0)
+            for (int e = t.lane; e < G * (kHeadDim / 8); e += kWave) {
+                const int g = e / (kHeadDim / 8), chunk = e % (kHeadDim / 8);
+                *reinterpret_cast<uint4*>(
+                    a.out + ((int64_t)t.b * a.num_q_heads + t.kvh * G + g) * kHeadDim +
+                    chunk * 8) = make_uint4(0, 0, 0, 0);
+            }
+        return;
+    }
+    float acc[G][8], m[kE], l_row[kE];
+    int head[kE];
+    attend_pages<G, CHECKED, KV, 1>(a, t, my_page, lds_p_all[t.wave], lds_alpha_all[t.wave],
+                                    acc, m, l_row, head);
+    // Lane 16kg + c writes dims 8c..8c+7 of the heads its lane group holds.
+    const int c = t.lane & 15;
+#pragma unroll
+    for (int e = 0; e < kE; ++e) {
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            if (g != head[e])
+                continue;
+            const int64_t row = (int64_t)t.b * a.num_q_heads + t.kvh * G + g;
+            if (t.nsplit == 1) {
+                const float inv = 1.0f / l_row[e];
+                uint4 o;
+                o.x = f32_to_bf16(acc[g][0] * inv) | (f32_to_bf16(acc[g][1] * inv) << 16);
+                o.y = f32_to_bf16(acc[g][2] * inv) | (f32_to_bf16(acc[g][3] * inv) << 16);
+                o.z = f32_to_bf16(acc[g][4] * inv) | (f32_to_bf16(acc[g][5] * inv) << 16);
+                o.w = f32_to_bf16(acc[g][6] * inv) | (f32_to_bf16(acc[g][7] * inv) << 16);
+                *reinterpret_cast<uint4*>(a.out + row * kHeadDim + 8 * c) = o;
+            } else {
+                const int64_t part = row * a.num_splits + t.s;
+                float4* dst = reinterpret_cast<float4*>(a.ws_acc + part * kHeadDim + 8 * c);
+                dst[0] = make_float4(acc[g][0], acc[g][1], acc[g][2], acc[g][3]);
+                dst[1] = make_float4(acc[g][4], acc[g][5], acc[g][6], acc[g][7]);
+                if (c == 0)
+                    *reinterpret_cast<float2*>(a.ws_ml + part * 2) = make_float2(m[e], l_row[e]);
+            }
+        }
+    }
 }
 
 // ------------------------------------------- split kernel, VALU dot2 QK ---
@@ -755,8 +922,10 @@ __global__ __launch_bounds__(kWave * kMergeWaves) void merge_splits(MergeArgs a)
 typedef void (*SplitKernel)(SplitArgs);
 
 template <int G, bool CHECKED>
-SplitKernel pick(bool fp8, bool mfma)
+SplitKernel pick(bool fp8, bool mfma, bool hp)
 {
+    if (hp)
+        return fp8 ? split_mfma_hp<G, CHECKED, KvFp8> : split_mfma_hp<G, CHECKED, KvBf16>;
     if (fp8)
         return split_mfma<G, CHECKED, KvFp8>;  // fp8 pools use the MFMA score tile only
     if (mfma)
@@ -765,21 +934,40 @@ SplitKernel pick(bool fp8, bool mfma)
 }
 
 template <bool CHECKED>
-SplitKernel select_for_group(int G, bool fp8, bool mfma)
+SplitKernel select_for_group(int G, bool fp8, bool mfma, bool hp)
 {
     switch (G) {
-    case 1: return pick<1, CHECKED>(fp8, mfma);
-    case 2: return pick<2, CHECKED>(fp8, mfma);
-    case 4: return pick<4, CHECKED>(fp8, mfma);
-    case 8: return pick<8, CHECKED>(fp8, mfma);
+    case 1: return pick<1, CHECKED>(fp8, mfma, hp);
+    case 2: return pick<2, CHECKED>(fp8, mfma, hp);
+    case 4: return pick<4, CHECKED>(fp8, mfma, hp);
+    case 8: return pick<8, CHECKED>(fp8, mfma, hp);
     default: return nullptr;
     }
 }
 
-SplitKernel select_split_kernel(int G, bool checked, bool fp8, bool mfma)
+SplitKernel select_split_kernel(int G, bool checked, bool fp8, bool mfma, bool hp)
 {
-    return checked ? select_for_group<true>(G, fp8, mfma)
-                   : select_for_group<false>(G, fp8, mfma);
+    return checked ? select_for_group<true>(G, fp8, mfma, hp)
+                   : select_for_group<false>(G, fp8, mfma, hp);
+}
+
+// kv heads per head-parallel work-group: the largest divisor of Hkv up to 8
+int heads_per_unit_for(int num_kv_heads)
+{
+    for (int d = kMaxHeadsPerUnit; d > 1; --d)
+        if (num_kv_heads % d == 0)
+            return d;
+    return 1;
+}
+
+// Token-major pools with at least two kv heads per work-group take the
+// head-parallel units (MFMA scores only) unless the caller asks for the
+// four-wavefront units; everything else the four-wavefront units.
+bool uses_head_parallel(const rl_da_config* cfg)
+{
+    return cfg->layout == RL_DA_LAYOUT_NHD &&
+           (cfg->flags & (RL_DA_SCORES_ON_VALU | RL_DA_PER_HEAD_UNITS)) == 0 &&
+           heads_per_unit_for(cfg->num_kv_heads) >= 2;
 }
 
 }  // namespace
@@ -793,6 +981,8 @@ struct rl_decode_attn {
     int max_splits;
     int device;
     bool use_mfma;
+    bool head_parallel;
+    int heads_per_unit;
     SplitKernel split_kernel;
     void* workspace;
     size_t workspace_bytes;
@@ -817,7 +1007,7 @@ rl_da_status check_config(const rl_da_config* cfg, int* split_tokens, int* split
         return RL_DA_ERR_INVALID_ARG;
     if (cfg->num_q_heads % cfg->num_kv_heads != 0)
         return RL_DA_ERR_INVALID_ARG;
-    if ((cfg->flags & ~(RL_DA_CHECKED | RL_DA_SCORES_ON_VALU)) != 0)
+    if ((cfg->flags & ~(RL_DA_CHECKED | RL_DA_SCORES_ON_VALU | RL_DA_PER_HEAD_UNITS)) != 0)
         return RL_DA_ERR_INVALID_ARG;
     if (cfg->kv_dtype != RL_DA_KV_BF16 && cfg->kv_dtype != RL_DA_KV_FP8_E4M3)
         return RL_DA_ERR_INVALID_ARG;
@@ -830,6 +1020,10 @@ rl_da_status check_config(const rl_da_config* cfg, int* split_tokens, int* split
         return RL_DA_ERR_UNSUPPORTED;
     if (cfg->kv_dtype == RL_DA_KV_FP8_E4M3 && (cfg->flags & RL_DA_SCORES_ON_VALU) != 0)
         return RL_DA_ERR_UNSUPPORTED;
+    const bool hp = uses_head_parallel(cfg);
+    // work units per (sequence, split)
+    const int64_t units_per_split =
+        hp ? cfg->num_kv_heads / heads_per_unit_for(cfg->num_kv_heads) : cfg->num_kv_heads;
     int st = cfg->split_tokens;
     if (st == 0) {
         // depends on the handle's capacity only, never on a run's batch
@@ -837,12 +1031,12 @@ rl_da_status check_config(const rl_da_config* cfg, int* split_tokens, int* split
         while (st > kMinDefaultSplitTokens) {
             const int64_t splits =
                 ((int64_t)cfg->max_pages_per_seq * kPageSize + st - 1) / st;
-            if ((int64_t)cfg->max_batch * cfg->num_kv_heads * splits >= kMinDefaultUnits)
+            if ((int64_t)cfg->max_batch * units_per_split * splits >= kMinDefaultUnits)
                 break;
             st /= 2;
         }
     }
-    if (st % kPageSize != 0 || st > kMaxSplitTokens)
+    if (st % kPageSize != 0 || st > (hp ? kMaxSplitTokensHp : kMaxSplitTokens))
         return RL_DA_ERR_UNSUPPORTED;
     *split_tokens = st;
     *split_pages = st / kPageSize;
@@ -911,8 +1105,11 @@ rl_da_status rl_decode_attn_create(const rl_da_config* cfg, rl_decode_attn** out
     h->max_splits = ms;
     const int G = cfg->num_q_heads / cfg->num_kv_heads;
     h->use_mfma = (cfg->flags & RL_DA_SCORES_ON_VALU) == 0;
-    h->split_kernel = select_split_kernel(G, (cfg->flags & RL_DA_CHECKED) != 0,
-                                          cfg->kv_dtype == RL_DA_KV_FP8_E4M3, h->use_mfma);
+    h->head_parallel = uses_head_parallel(cfg);
+    h->heads_per_unit = h->head_parallel ? heads_per_unit_for(cfg->num_kv_heads) : 1;
+    h->split_kernel =
+        select_split_kernel(G, (cfg->flags & RL_DA_CHECKED) != 0,
+                            cfg->kv_dtype == RL_DA_KV_FP8_E4M3, h->use_mfma, h->head_parallel);
     if (hipGetDevice(&h->device) != hipSuccess) {
         free(h);
         return RL_DA_ERR_HIP;
@@ -984,7 +1181,7 @@ rl_da_status rl_decode_attn_run(rl_decode_attn* h, const void* q, const void* k_
         return RL_DA_OK;
 
     const int num_splits = (max_pages + h->split_pages - 1) / h->split_pages;
-    const int64_t units = (int64_t)batch * cfg.num_kv_heads * num_splits;
+    const int64_t units = (int64_t)batch * (cfg.num_kv_heads / h->heads_per_unit) * num_splits;
     if (units > INT32_MAX)
         return RL_DA_ERR_UNSUPPORTED;
 
@@ -1011,13 +1208,14 @@ rl_da_status rl_decode_attn_run(rl_decode_attn* h, const void* q, const void* k_
     sa.max_pages = max_pages;
     sa.split_pages = h->split_pages;
     sa.num_splits = num_splits;
+    sa.heads_per_unit = h->heads_per_unit;
     sa.scale_log2 = scale * kLog2e;
 
     hipStream_t st = (hipStream_t)stream;
     if (h->ev_split_begin != nullptr && hipEventRecord(h->ev_split_begin, st) != hipSuccess)
         return RL_DA_ERR_HIP;
-    hipLaunchKernelGGL(h->split_kernel, dim3((unsigned)units), dim3(kWave * kUnitWaves), 0, st,
-                       sa);
+    const int threads = h->head_parallel ? kWave * h->heads_per_unit : kWave * kUnitWaves;
+    hipLaunchKernelGGL(h->split_kernel, dim3((unsigned)units), dim3(threads), 0, st, sa);
     if (hipGetLastError() != hipSuccess)
         return RL_DA_ERR_HIP;
     if (h->ev_split_end != nullptr && hipEventRecord(h->ev_split_end, st) != hipSuccess)

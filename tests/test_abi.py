@@ -92,6 +92,21 @@ def test_workspace_size_formula():
     assert n3 == (rows3 * 128 * 4 + rows3 * 2 * 4 + 255) // 256 * 256 + 256
 
 
+def test_token_major_pools_default_split():
+    """Token-major pools with several kv heads per work-group use one
+    work-group per (sequence, split, eight kv heads), so the default split
+    that still gives 256 work-groups is 1024 tokens here; the workspace
+    follows."""
+    rc, n = B.rl_decode_attn_workspace_size(cfg(layout=B.RL_DA_LAYOUT_NHD))
+    rows = 64 * 32 * 4                       # 256 pages -> four 1024-token splits
+    assert rc == B.RL_DA_OK
+    assert n == (rows * 128 * 4 + rows * 2 * 4 + 255) // 256 * 256 + 256
+    # the VALU score path keeps the four-wavefront units and their 4096 default
+    rc, n1 = B.rl_decode_attn_workspace_size(cfg(layout=B.RL_DA_LAYOUT_NHD,
+                                                 flags=B.RL_DA_SCORES_ON_VALU))
+    assert rc == B.RL_DA_OK and n1 == B.rl_decode_attn_workspace_size(cfg())[1]
+
+
 @pytest.mark.parametrize("kw,status", [
     (dict(num_q_heads=0), B.RL_DA_ERR_INVALID_ARG),
     (dict(num_kv_heads=-1), B.RL_DA_ERR_INVALID_ARG),
@@ -100,6 +115,7 @@ def test_workspace_size_formula():
     (dict(max_pages_per_seq=0), B.RL_DA_ERR_INVALID_ARG),
     (dict(split_tokens=-16), B.RL_DA_ERR_INVALID_ARG),
     (dict(flags=0x80), B.RL_DA_ERR_INVALID_ARG),
+    (dict(flags=0x8), B.RL_DA_ERR_INVALID_ARG),
     (dict(kv_dtype=7), B.RL_DA_ERR_INVALID_ARG),
     (dict(layout=2), B.RL_DA_ERR_INVALID_ARG),
     (dict(head_dim=64), B.RL_DA_ERR_UNSUPPORTED),
@@ -109,6 +125,7 @@ def test_workspace_size_formula():
     (dict(split_tokens=24), B.RL_DA_ERR_UNSUPPORTED),
     (dict(kv_dtype=B.RL_DA_KV_FP8_E4M3, flags=B.RL_DA_SCORES_ON_VALU), B.RL_DA_ERR_UNSUPPORTED),
     (dict(split_tokens=4112), B.RL_DA_ERR_UNSUPPORTED),
+    (dict(layout=B.RL_DA_LAYOUT_NHD, split_tokens=4112), B.RL_DA_ERR_UNSUPPORTED),
 ])
 def test_create_rejects_bad_config_without_gpu(kw, status):
     c = cfg(**kw)
