@@ -58,6 +58,17 @@ inline bool pool_strides(int32_t layout, int32_t num_kv_heads, int32_t elt, Pool
 
 // ------------------------------------------------------------ helpers ---
 
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// Two fp32 values as packed bf16 (one v_cvt_pk_bf16_f32, round to nearest
+// even), a in the low half.
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b)
+{
+    const f32x2_t v = {a, b};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
+}
+
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 

@@ -10,20 +10,34 @@ namespace {
 //
 // Causal attention of each sequence's n_b new tokens (already appended: the
 // last n_b of its L_b cached tokens).  A work unit is one work-group of four
-// wavefronts for (sequence b, kv head, tile of 64/G new tokens); wavefront w
-// owns 16/G of the tile's tokens and all G query heads of the kv head: 16
-// query rows, row m = (token m / G, head m % G).  Every K/V page the tile can
-// see is loaded once into LDS for the four wavefronts (K as [token][dim], V
-// transposed to [dim][token]); each wavefront then forms its 16x16 score tile
-// with four v_mfma_f32_16x16x32_bf16 (as the decode kernel), applies the
-// causal mask where a page crosses a query position, keeps an online softmax
-// per row, and accumulates O += P V with v_mfma_f32_16x16x16_bf16 over eight
-// 16-dim blocks.  P goes to the PV MFMA as two bf16 terms (hi + lo), so the
-// value sum keeps fp32-level accuracy; l sums the same fp32 probabilities.
+// wavefronts for (sequence b, kv head, tile of 128/G new tokens): 128 query
+// rows, row r = (token r / G, head r % G); wavefront w owns rows 32w..32w+31 as
+// two blocks of 16.  The keys the tile can see pass through LDS 64 at a time
+// (four pages: K as [key][dim], V transposed to [dim][key]), double-buffered
+// with one barrier per stage.
+//
+// Both products run transposed so that every lane keeps one query row from
+// the scores to the output.  S^T = K Q^T (v_mfma_f32_16x16x32_bf16, A = 16
+// keys x 32 dims from LDS, B = Q^T held in registers) leaves lane l with row
+// l%16 and keys 4(l/16)+j of each 16-key block; O^T += V^T P^T (same MFMA,
+// 32 keys) takes P^T straight from those registers, with the k index of the
+// product running over keys in the order (4g..4g+3, 16+4g..16+4g+3) for lane
+// group g, and V^T read from LDS in the same order.  Row max, rescale and sum
+// are therefore lane-local but for two shuffles per 64 keys.  P enters the
+// PV product as two bf16 terms (hi + lo), so the value sum keeps fp32-level
+// accuracy; l sums the same fp32 probabilities.
 
-constexpr int kExtendRows = 16;                   // query rows per wavefront
-constexpr int kKRowPad = 8;                       // bf16 elements of row padding
-constexpr int kVtRow = kPageSize + 4;             // [dim][token] row, padded
+constexpr int kRowBlocks = 2;                      // 16-row blocks per wavefront
+constexpr int kTileRows = kUnitWaves * kRowBlocks * 16;
+constexpr int kStageKeys = 64;                     // keys per LDS stage (4 pages)
+constexpr int kStagePages = kStageKeys / kPageSize;
+constexpr int kKRow = kHeadDim + 8;                // K [key][dim] row, padded (bf16)
+constexpr int kVtRow = kStageKeys + 4;             // V^T [dim][key] row, padded (bf16)
+
+// Column of key k in V^T row `dim`: keys are XORed with 8 * (dim / 16 % 8), so
+// that the staging writes of one instruction (8 dim blocks x 4 key pairs)
+// fall in 32 different banks; runs of 4 keys stay contiguous for the reads.
+__device__ __forceinline__ int vt_col(int dim, int key) { return key ^ (8 * ((dim >> 4) & 7)); }
 
 struct ExtendArgs {
     const uint16_t* q;          // bf16 [T][Hq][D]
@@ -44,14 +58,13 @@ struct ExtendArgs {
 };
 
 template <int G>
-__global__ __launch_bounds__(kWave * kUnitWaves) void extend_bf16(ExtendArgs a)
+__global__ __launch_bounds__(kWave * kUnitWaves)
+__attribute__((amdgpu_waves_per_eu(2))) void extend_bf16(ExtendArgs a)
 {
-    static_assert(G >= 1 && G <= 16 && 16 % G == 0, "16 rows per wavefront hold whole groups");
-    constexpr int kTokPerWave = kExtendRows / G;
-    constexpr int kTileTok = kUnitWaves * kTokPerWave;
-    __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][kPageSize][kHeadDim + kKRowPad];
+    static_assert(G >= 1 && G <= 16 && 16 % G == 0, "16-row blocks hold whole groups");
+    constexpr int kTileTok = kTileRows / G;
+    __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][kStageKeys][kKRow];
     __shared__ __attribute__((aligned(16))) uint16_t vt_lds[2][kHeadDim][kVtRow];
-    __shared__ __attribute__((aligned(16))) uint16_t p_lds[kUnitWaves][2][kExtendRows][kVtRow];
 
     const int tile = blockIdx.x % a.num_tiles;
     const int bk = blockIdx.x / a.num_tiles;
@@ -64,154 +77,244 @@ __global__ __launch_bounds__(kWave * kUnitWaves) void extend_bf16(ExtendArgs a)
     const int tok0 = tile * kTileTok;
     if (tok0 >= n_new)
         return;
-    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-    const int n = lane & 15, kg = lane >> 4;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int lane = threadIdx.x % kWave;
+    const int i16 = lane & 15, g4 = lane >> 4;
     const int h0 = kvh * G;
     const int base_pos = L - n_new;  // position of new token 0
 
-    // Query operand rows: lane holds row m = lane % 16 for the MFMA A operand.
-    uint4 qa[4];
-    {
-        const int m = lane & 15;
-        const int qi = tok0 + wave * kTokPerWave + m / G;
-        const bool real = qi < n_new;
+    // Q^T operand and the causal limit of this lane's row in each block.
+    uint4 qb[kRowBlocks][4];
+    int row_pos[kRowBlocks];
+    bool row_real[kRowBlocks];
+#pragma unroll
+    for (int rb = 0; rb < kRowBlocks; ++rb) {
+        const int r = wave * (kRowBlocks * 16) + rb * 16 + i16;
+        const int qi = tok0 + r / G;
+        row_real[rb] = qi < n_new;
+        row_pos[rb] = base_pos + qi;
         const uint16_t* qrow =
-            a.q + ((int64_t)(q0 + (real ? qi : 0)) * a.num_q_heads + h0 + m % G) * kHeadDim;
+            a.q + ((int64_t)(q0 + (row_real[rb] ? qi : 0)) * a.num_q_heads + h0 + r % G) *
+                      kHeadDim;
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-            qa[i] = real ? *reinterpret_cast<const uint4*>(qrow + 32 * i + 8 * kg)
-                         : make_uint4(0, 0, 0, 0);
-    }
-    // Rows this lane holds in the C layout: m = 4kg + j.
-    int row_pos[4];
-    bool row_real[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int m = 4 * kg + j;
-        const int qi = tok0 + wave * kTokPerWave + m / G;
-        row_real[j] = qi < n_new;
-        row_pos[j] = base_pos + qi;
+        for (int ks = 0; ks < 4; ++ks)
+            qb[rb][ks] = row_real[rb] ? *reinterpret_cast<const uint4*>(qrow + 32 * ks + 8 * g4)
+                                      : make_uint4(0, 0, 0, 0);
     }
     const int tile_last = min(tok0 + kTileTok, n_new) - 1;
-    const int npages = (base_pos + tile_last) / kPageSize + 1;  // pages the tile sees
-    const int first_masked_page = (base_pos + tok0) / kPageSize;
+    const int nkeys = base_pos + tile_last + 1;           // keys the tile sees
+    const int nstages = (nkeys + kStageKeys - 1) / kStageKeys;
+    const int first_masked_stage = (base_pos + tok0) / kStageKeys;
 
-    float m_run[4], lsum[4];
-    floatx4_t o[8];
+    float m_run[kRowBlocks], lsum[kRowBlocks];
+    floatx4_t o[kRowBlocks][8];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        m_run[j] = -INFINITY;
-        lsum[j] = 0.0f;
+    for (int rb = 0; rb < kRowBlocks; ++rb) {
+        m_run[rb] = -INFINITY;
+        lsum[rb] = 0.0f;
+#pragma unroll
+        for (int db = 0; db < 8; ++db)
+            o[rb][db] = floatx4_t{0.0f, 0.0f, 0.0f, 0.0f};
     }
-#pragma unroll
-    for (int nb = 0; nb < 8; ++nb)
-        o[nb] = floatx4_t{0.0f, 0.0f, 0.0f, 0.0f};
 
-    // Staging: thread t moves 16 bytes of K and of V: token t/16, dims 8(t%16)..+8.
-    const int st_tok = threadIdx.x / 16, st_dim = (threadIdx.x % 16) * 8;
+    // Staging: thread t moves keys 2(t/8) and 2(t/8)+1, dims 16(t%8)..+15, of
+    // K and of V (four 16-byte loads each).
+    const int st_kp = threadIdx.x / 8, st_c = threadIdx.x % 8;
     const int32_t* bt = a.block_table + (int64_t)b * a.max_pages;
-    const int64_t st_off = (int64_t)kvh * a.head_bytes + st_tok * a.row_bytes + 2 * st_dim;
-    auto fetch = [&](int j, uint4& kr, uint4& vr) {
-        const int64_t off = bt[j] * a.page_bytes + st_off;
-        kr = load_stream16(a.k_pool + off);
-        vr = load_stream16(a.v_pool + off);
-    };
-    uint4 kr, vr;
-    fetch(0, kr, vr);
-
-    for (int j = 0; j < npages; ++j) {
-        const int buf = j & 1;
-        // slots past the sequence end may hold NaN: they must not reach P.V
-        if (j * kPageSize + st_tok >= L) {
-            kr = make_uint4(0, 0, 0, 0);
-            vr = make_uint4(0, 0, 0, 0);
-        }
-        *reinterpret_cast<uint4*>(&k_lds[buf][st_tok][st_dim]) = kr;
-        {
-            const uint32_t w[4] = {vr.x, vr.y, vr.z, vr.w};
+    const int64_t st_off = (int64_t)kvh * a.head_bytes + 2 * (16 * st_c);
+    uint4 kr[2][2], vr[2][2];  // [key of the pair][half of the 16 dims]
+    auto fetch = [&](int stage) {
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                vt_lds[buf][st_dim + 2 * e][st_tok] = (uint16_t)(w[e] & 0xffffu);
-                vt_lds[buf][st_dim + 2 * e + 1][st_tok] = (uint16_t)(w[e] >> 16);
+        for (int e = 0; e < 2; ++e) {
+            const int key = stage * kStageKeys + 2 * st_kp + e;
+            if (key < L) {  // pages past the sequence are never read
+                const int64_t off = bt[key / kPageSize] * a.page_bytes + st_off +
+                                    (int64_t)(key % kPageSize) * a.row_bytes;
+                kr[e][0] = load_stream16(a.k_pool + off);
+                kr[e][1] = load_stream16(a.k_pool + off + 16);
+                vr[e][0] = load_stream16(a.v_pool + off);
+                vr[e][1] = load_stream16(a.v_pool + off + 16);
+            } else {  // slots past the sequence end may hold NaN: stage zeros
+                kr[e][0] = kr[e][1] = vr[e][0] = vr[e][1] = make_uint4(0, 0, 0, 0);
             }
         }
-        if (j + 1 < npages)
-            fetch(j + 1, kr, vr);
+    };
+    auto stash = [&](int buf) {
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+            uint4* krow = reinterpret_cast<uint4*>(&k_lds[buf][2 * st_kp + e][16 * st_c]);
+            krow[0] = kr[e][0];
+            krow[1] = kr[e][1];
+        }
+        // V^T: dims 16c..16c+15, the key pair as one 32-bit word per dim
+        const uint32_t w0[8] = {vr[0][0].x, vr[0][0].y, vr[0][0].z, vr[0][0].w,
+                                vr[0][1].x, vr[0][1].y, vr[0][1].z, vr[0][1].w};
+        const uint32_t w1[8] = {vr[1][0].x, vr[1][0].y, vr[1][0].z, vr[1][0].w,
+                                vr[1][1].x, vr[1][1].y, vr[1][1].z, vr[1][1].w};
+        const int col = vt_col(16 * st_c, 2 * st_kp);  // same swizzle for all 16 dims
+#pragma unroll
+        for (int d = 0; d < 8; ++d) {
+            *reinterpret_cast<uint32_t*>(&vt_lds[buf][16 * st_c + 2 * d][col]) =
+                (w0[d] & 0xffffu) | (w1[d] << 16);
+            *reinterpret_cast<uint32_t*>(&vt_lds[buf][16 * st_c + 2 * d + 1][col]) =
+                (w0[d] >> 16) | (w1[d] & 0xffff0000u);
+        }
+    };
+
+    fetch(0);
+    for (int j = 0; j < nstages; ++j) {
+        const int buf = j & 1;
+        stash(buf);
+        if (j + 1 < nstages)
+            fetch(j + 1);
         __syncthreads();
 
-        // scores S[row 4kg+jj][token n]
-        floatx4_t sacc = {0.0f, 0.0f, 0.0f, 0.0f};
+        // S^T for the stage's four 16-key blocks: lane holds row i16, keys
+        // 16kb + 4g4 + jj.
+        floatx4_t sacc[kRowBlocks][4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const uint4 kb = *reinterpret_cast<const uint4*>(&k_lds[buf][n][32 * i + 8 * kg]);
-            sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                __builtin_bit_cast(bf16x8_t, qa[i]), __builtin_bit_cast(bf16x8_t, kb), sacc,
-                0, 0, 0);
-        }
-        const int key = j * kPageSize + n;
-        float s[4];
+        for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-        for (int jj = 0; jj < 4; ++jj) {
-            float x = sacc[jj] * a.scale_log2;
-            if (j >= first_masked_page)
-                x = key <= row_pos[jj] ? x : -INFINITY;
-            s[jj] = row_real[jj] ? x : 0.0f;  // rows past the tile's tokens stay finite
-        }
-        float mx[4];
-        bool grow_any = false;
+            for (int rb = 0; rb < kRowBlocks; ++rb)
+                sacc[rb][kb] = floatx4_t{0.0f, 0.0f, 0.0f, 0.0f};
+        // dims outermost: eight independent accumulators between dependent MFMAs
 #pragma unroll
-        for (int jj = 0; jj < 4; ++jj) {
-            mx[jj] = row16_max(s[jj]);   // finite: key 0 is visible to every row
-            grow_any |= mx[jj] > m_run[jj] + kMaxSlack;
-        }
-        if (__any(grow_any)) {
+        for (int ks = 0; ks < 4; ++ks) {
 #pragma unroll
-            for (int jj = 0; jj < 4; ++jj) {
-                const float m_new = mx[jj] > m_run[jj] + kMaxSlack ? mx[jj] : m_run[jj];
-                const float alpha = exp2_fast(m_run[jj] - m_new);
-                m_run[jj] = m_new;
-                lsum[jj] *= alpha;
+            for (int kb = 0; kb < 4; ++kb) {
+                const uint4 kv =
+                    *reinterpret_cast<const uint4*>(&k_lds[buf][16 * kb + i16][32 * ks + 8 * g4]);
 #pragma unroll
-                for (int nb = 0; nb < 8; ++nb)
-                    o[nb][jj] *= alpha;
+                for (int rb = 0; rb < kRowBlocks; ++rb)
+                    sacc[rb][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        __builtin_bit_cast(bf16x8_t, kv), __builtin_bit_cast(bf16x8_t, qb[rb][ks]),
+                        sacc[rb][kb], 0, 0, 0);
             }
         }
+        // Probabilities (masked only in stages that can cross a query
+        // position; rows past the tile's tokens score 0 and stay finite) and
+        // O^T += V^T P^T: lane holds dims 16db + 4g4 + jj of row i16.
+        const bool masked = j >= first_masked_stage;
+        // Row max over the stage for both row blocks (lane-local over 16
+        // keys, then the two other lane groups of the row).
+        float raw[kRowBlocks][4][4], mx[kRowBlocks];
 #pragma unroll
-        for (int jj = 0; jj < 4; ++jj) {
-            const float p = exp2_fast(s[jj] - m_run[jj]);
-            lsum[jj] += p;
-            const uint32_t hi = f32_to_bf16(p);
-            const float rest = p - __uint_as_float(hi << 16);
-            p_lds[wave][0][4 * kg + jj][n] = (uint16_t)hi;
-            p_lds[wave][1][4 * kg + jj][n] = (uint16_t)f32_to_bf16(rest);
+        for (int rb = 0; rb < kRowBlocks; ++rb) {
+            mx[rb] = -INFINITY;
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) {
+                    float x = sacc[rb][kb][jj];
+                    if (masked)
+                        x = j * kStageKeys + 16 * kb + 4 * g4 + jj <= row_pos[rb] ? x : -INFINITY;
+                    raw[rb][kb][jj] = x;
+                    mx[rb] = fmaxf(mx[rb], x);
+                }
         }
-        wave_lds_sync();
-        const uint2 ph = *reinterpret_cast<const uint2*>(&p_lds[wave][0][n][4 * kg]);
-        const uint2 pl = *reinterpret_cast<const uint2*>(&p_lds[wave][1][n][4 * kg]);
-        wave_lds_sync();
 #pragma unroll
-        for (int nb = 0; nb < 8; ++nb) {
-            const uint2 vb = *reinterpret_cast<const uint2*>(&vt_lds[buf][16 * nb + n][4 * kg]);
-            o[nb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(
-                __builtin_bit_cast(bf16x4_t, ph), __builtin_bit_cast(bf16x4_t, vb), o[nb], 0, 0, 0);
-            o[nb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(
-                __builtin_bit_cast(bf16x4_t, pl), __builtin_bit_cast(bf16x4_t, vb), o[nb], 0, 0, 0);
+        for (int rb = 0; rb < kRowBlocks; ++rb)
+            mx[rb] = fmaxf(mx[rb], __shfl_xor(mx[rb], 16));
+#pragma unroll
+        for (int rb = 0; rb < kRowBlocks; ++rb)
+            mx[rb] = fmaxf(mx[rb], __shfl_xor(mx[rb], 32)) * a.scale_log2;  // finite: key 0
+        bool grow = false;
+#pragma unroll
+        for (int rb = 0; rb < kRowBlocks; ++rb)
+            grow |= mx[rb] > m_run[rb] + kMaxSlack;
+        if (__any(grow)) {
+#pragma unroll
+            for (int rb = 0; rb < kRowBlocks; ++rb) {
+                const float m_new = mx[rb] > m_run[rb] + kMaxSlack ? mx[rb] : m_run[rb];
+                const float alpha = exp2_fast(m_run[rb] - m_new);  // 0 on the first stage
+                m_run[rb] = m_new;
+                lsum[rb] *= alpha;
+#pragma unroll
+                for (int db = 0; db < 8; ++db)
+#pragma unroll
+                    for (int jj = 0; jj < 4; ++jj)
+                        o[rb][db][jj] *= alpha;
+            }
+        }
+        // Probabilities as P^T operands: [rb][key half][hi, lo] bf16 x 8.
+        uint4 pt[kRowBlocks][2][2];
+#pragma unroll
+        for (int rb = 0; rb < kRowBlocks; ++rb) {
+            const float neg_m = -m_run[rb];
+            uint32_t hi[4][2], lo[4][2];
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                for (int jp = 0; jp < 2; ++jp) {
+                    const float p0 = exp2_fast(fmaf(raw[rb][kb][2 * jp], a.scale_log2, neg_m));
+                    const float p1 = exp2_fast(fmaf(raw[rb][kb][2 * jp + 1], a.scale_log2, neg_m));
+                    lsum[rb] += p0 + p1;
+                    const uint32_t h = pack_bf16x2(p0, p1);
+                    hi[kb][jp] = h;
+                    lo[kb][jp] = pack_bf16x2(p0 - __uint_as_float(h << 16),
+                                             p1 - __uint_as_float(h & 0xffff0000u));
+                }
+#pragma unroll
+            for (int kh = 0; kh < 2; ++kh) {
+                pt[rb][kh][0] = make_uint4(hi[2 * kh][0], hi[2 * kh][1], hi[2 * kh + 1][0],
+                                           hi[2 * kh + 1][1]);
+                pt[rb][kh][1] = make_uint4(lo[2 * kh][0], lo[2 * kh][1], lo[2 * kh + 1][0],
+                                           lo[2 * kh + 1][1]);
+            }
+        }
+        // O^T += V^T P^T: lane holds dims 16db + 4g4 + jj of row i16.  The V^T
+        // operand of the next (db, kh) is read before this one's MFMAs.
+        auto vt_operand = [&](int step) {
+            const int db = step >> 1, kh = step & 1;
+            const int dim = 16 * db + i16;
+            const uint16_t* vrow = &vt_lds[buf][dim][0];
+            const uint2 va =
+                *reinterpret_cast<const uint2*>(vrow + vt_col(dim, 32 * kh + 4 * g4));
+            const uint2 vb =
+                *reinterpret_cast<const uint2*>(vrow + vt_col(dim, 32 * kh + 16 + 4 * g4));
+            return make_uint4(va.x, va.y, vb.x, vb.y);
+        };
+        uint4 vt_next = vt_operand(0);
+#pragma unroll
+        for (int step = 0; step < 16; ++step) {
+            const uint4 vt = vt_next;
+            if (step + 1 < 16)
+                vt_next = vt_operand(step + 1);
+            // keep the read ahead of this step's MFMAs (the scheduler would
+            // otherwise sink it next to its own use)
+            __builtin_amdgcn_sched_barrier(0);
+            const int db = step >> 1, kh = step & 1;
+#pragma unroll
+            for (int rb = 0; rb < kRowBlocks; ++rb) {
+                o[rb][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                    __builtin_bit_cast(bf16x8_t, vt), __builtin_bit_cast(bf16x8_t, pt[rb][kh][0]),
+                    o[rb][db], 0, 0, 0);
+                o[rb][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                    __builtin_bit_cast(bf16x8_t, vt), __builtin_bit_cast(bf16x8_t, pt[rb][kh][1]),
+                    o[rb][db], 0, 0, 0);
+            }
         }
     }
 
-    // out[row] = O[row] / l[row]; lane holds rows 4kg+jj, dims 16nb + n.
+    // out[row] = O[row] / l[row]; lane holds row i16, dims 16db + 4g4 + jj.
 #pragma unroll
-    for (int jj = 0; jj < 4; ++jj) {
-        const float l = row16_sum(lsum[jj]);
-        if (!row_real[jj])
+    for (int rb = 0; rb < kRowBlocks; ++rb) {
+        float l = lsum[rb];
+        l += __shfl_xor(l, 16);
+        l += __shfl_xor(l, 32);
+        if (!row_real[rb])
             continue;
-        const int m = 4 * kg + jj;
-        const int qi = tok0 + wave * kTokPerWave + m / G;
-        uint16_t* orow = a.out + ((int64_t)(q0 + qi) * a.num_q_heads + h0 + m % G) * kHeadDim;
+        const int r = wave * (kRowBlocks * 16) + rb * 16 + i16;
+        const int qi = tok0 + r / G;
+        uint16_t* orow = a.out + ((int64_t)(q0 + qi) * a.num_q_heads + h0 + r % G) * kHeadDim;
         const float inv = 1.0f / l;
 #pragma unroll
-        for (int nb = 0; nb < 8; ++nb)
-            orow[16 * nb + n] = (uint16_t)f32_to_bf16(o[nb][jj] * inv);
+        for (int db = 0; db < 8; ++db) {
+            const floatx4_t& v = o[rb][db];
+            *reinterpret_cast<uint2*>(orow + 16 * db + 4 * g4) =
+                make_uint2(f32_to_bf16(v[0] * inv) | (f32_to_bf16(v[1] * inv) << 16),
+                           f32_to_bf16(v[2] * inv) | (f32_to_bf16(v[3] * inv) << 16));
+        }
     }
 }
 
@@ -249,7 +352,7 @@ rl_da_status rl_extend_attn(const void* q, const int32_t* q_start, int32_t max_q
         return RL_DA_ERR_UNSUPPORTED;
     if (batch == 0 || max_q_per_seq == 0)
         return RL_DA_OK;
-    const int tile_tok = kUnitWaves * kExtendRows / G;
+    const int tile_tok = kTileRows / G;
     ExtendArgs ea;
     ea.q = (const uint16_t*)q;
     ea.q_start = q_start;
