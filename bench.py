@@ -141,7 +141,7 @@ def _pmc_means(path, counter):
 # prefix in the profiler's output) and the sources it is built from.
 OP_KERNELS = {
     "attention": ("void (anonymous namespace)::split_", ("rl_common.h", "rl_decode.hip")),
-    "pack": ("(anonymous namespace)::copy_pieces", ("rl_common.h", "rl_weight_sync.hip")),
+    "pack": ("void (anonymous namespace)::copy_pieces<true>", ("rl_common.h", "rl_weight_sync.hip")),
 }
 
 

@@ -4,7 +4,8 @@
 //
 // Plan on the host, copy on the GPU.  A chunk's pieces are cut into 32 KiB
 // tiles; one work-group of 256 threads copies one tile, each thread eight
-// 16-byte vectors with all loads issued before the stores.  A work-group finds
+// 16-byte vectors with all loads issued before the stores (non-temporal
+// loads, and non-temporal stores into device memory).  A work-group finds
 // its piece by binary search over the pieces' first-tile numbers, so pieces of
 // any size share one launch.  The copy is bound by HBM (read + write of every
 // byte) when the buffer is device memory and by the host link when it is
@@ -39,6 +40,12 @@ struct CopyArgs {
     int32_t unpack;           // 0: tensor -> buffer, 1: buffer -> tensor
 };
 
+// STREAM_STORES: the destination is device memory and gets non-temporal
+// stores (data written once, not read back soon; into pinned host memory
+// they measured slower).  A template parameter, not a run-time flag: the
+// branch made the compiler reorder the loads so that stores waited for
+// seven of the eight.
+template <bool STREAM_STORES>
 __global__ __launch_bounds__(kCopyThreads) void copy_pieces(CopyArgs a)
 {
     const uint64_t tile = blockIdx.x;
@@ -72,8 +79,14 @@ __global__ __launch_bounds__(kCopyThreads) void copy_pieces(CopyArgs a)
         for (int i = 0; i < kVecPerThread; ++i)
             v[i] = load_stream16(s + 16 * (t + i * kCopyThreads));
 #pragma unroll
-        for (int i = 0; i < kVecPerThread; ++i)
-            d[t + i * kCopyThreads] = v[i];
+        for (int i = 0; i < kVecPerThread; ++i) {
+            if (STREAM_STORES) {
+                const u32x4_t w = {v[i].x, v[i].y, v[i].z, v[i].w};
+                __builtin_nontemporal_store(w, reinterpret_cast<u32x4_t*>(d + t + i * kCopyThreads));
+            } else {
+                d[t + i * kCopyThreads] = v[i];
+            }
+        }
         return;
     }
     for (uint64_t i = t; i < nvec; i += kCopyThreads)
@@ -121,13 +134,15 @@ rl_da_status make_plan(const uint64_t* tensor_bytes, int32_t num_tensors, uint64
 
 // Device address at which a kernel may access `p`: device memory as is,
 // pinned host memory through its device mapping; null for anything else.
-void* device_view(const void* p)
+// *on_device tells which.
+void* device_view(const void* p, bool* on_device)
 {
     hipPointerAttribute_t attr;
     if (hipPointerGetAttributes(&attr, p) != hipSuccess) {
         (void)hipGetLastError();
         return nullptr;
     }
+    *on_device = attr.type == hipMemoryTypeDevice;
     if (attr.type == hipMemoryTypeDevice)
         return const_cast<void*>(p);
     if (attr.type == hipMemoryTypeHost) {
@@ -145,6 +160,7 @@ void* device_view(const void* p)
 
 struct rl_weight_sync {
     int32_t num_chunks;
+    bool buffer_on_device;              // else pinned host memory
     std::vector<int64_t> chunk_first;   // index of each chunk's first piece; [num_chunks + 1]
     std::vector<uint64_t> chunk_tiles;  // tiles of each chunk
     std::vector<uint64_t> chunk_bytes;  // tensor bytes of each chunk
@@ -193,7 +209,8 @@ rl_da_status rl_ws_create(const rl_ws_tensor* tensors, int32_t num_tensors, void
         if (attr.type != hipMemoryTypeDevice)
             return RL_DA_ERR_INVALID_ARG;
     }
-    uint8_t* buf = static_cast<uint8_t*>(device_view(buffer));
+    bool buffer_on_device = false;
+    uint8_t* buf = static_cast<uint8_t*>(device_view(buffer, &buffer_on_device));
     if (buf == nullptr)
         return RL_DA_ERR_INVALID_ARG;
     std::vector<rl_ws_piece> plan;
@@ -207,6 +224,7 @@ rl_da_status rl_ws_create(const rl_ws_tensor* tensors, int32_t num_tensors, void
     if (h == nullptr)
         return RL_DA_ERR_OUT_OF_MEMORY;
     h->num_chunks = nc;
+    h->buffer_on_device = buffer_on_device;
     h->chunk_first.assign(nc + 1, np);
     h->chunk_tiles.assign(nc, 0);
     h->chunk_bytes.assign(nc, 0);
@@ -269,8 +287,11 @@ static rl_da_status launch_copy(rl_weight_sync* h, int32_t chunk, int unpack, vo
     a.pieces = h->dev_pieces + h->chunk_first[chunk];
     a.num_pieces = (int32_t)(h->chunk_first[chunk + 1] - h->chunk_first[chunk]);
     a.unpack = unpack;
-    hipLaunchKernelGGL(copy_pieces, dim3((unsigned)h->chunk_tiles[chunk]), dim3(kCopyThreads), 0,
-                       (hipStream_t)stream, a);
+    const dim3 grid((unsigned)h->chunk_tiles[chunk]), block(kCopyThreads);
+    if (unpack || h->buffer_on_device)  // destination in device memory
+        hipLaunchKernelGGL(copy_pieces<true>, grid, block, 0, (hipStream_t)stream, a);
+    else
+        hipLaunchKernelGGL(copy_pieces<false>, grid, block, 0, (hipStream_t)stream, a);
     return hipGetLastError() == hipSuccess ? RL_DA_OK : RL_DA_ERR_HIP;
 }
 
