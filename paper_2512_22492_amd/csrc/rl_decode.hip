@@ -70,6 +70,7 @@ struct SplitArgs {
     int32_t max_pages;
     int32_t split_pages;
     int32_t num_splits;         // ceil(max_pages / split_pages)
+    int32_t units_per_level;    // work-groups per split level (batch x heads or head groups)
     int32_t heads_per_unit;     // kv heads per head-parallel work-group
     float scale_log2;           // scale * log2(e)
 };
@@ -82,40 +83,74 @@ struct WaveTask {
     int nsplit;    // splits of this sequence
     int p0;        // first page of the unit
     int count;     // pages of this wavefront (may be 0)
+    bool last_level;  // the unit runs in the grid's last split level
 };
+
+// Split level of a work-group and its sequence's split.  The grid runs in
+// num_splits levels of units_per_level work-groups; level v holds, for every
+// (sequence, head), the split with num_splits - 1 - v splits after it, so
+// that every sequence's last split -- the only one that can be short -- is
+// dispatched after all full ones (the dispatcher hands out work-groups in
+// order, and short units at the end leave the smallest tail).  A sequence
+// with fewer splits has no unit on the first levels.  The split a unit
+// computes, and so every result, does not depend on this order.
+__device__ __forceinline__ int split_of_level(int level, int nsplit, int num_splits)
+{
+    return nsplit - num_splits + level;  // < 0: no such split
+}
 
 // Decodes (blockIdx.x, wavefront) into a task and loads its block-table
 // entries (lane i: page p0 + wave + 4i) together with the sequence length.
 // Entries past the sequence's end lie inside the table row and are loaded
 // but never used.  Returns false, for every wavefront of the unit alike, when
 // the unit holds no page of its sequence.
-template <bool CHECKED>
+template <bool CHECKED, bool ORDERED>
 __device__ __forceinline__ bool begin_task(const SplitArgs& a, WaveTask& t, int32_t& my_page)
 {
     t.lane = threadIdx.x % kWave;
     t.wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);  // uniform: scalar
     const int unit = blockIdx.x;
-    t.s = unit % a.num_splits;
-    const int bk = unit / a.num_splits;
-    t.kvh = bk % a.num_kv_heads;
-    t.b = bk / a.num_kv_heads;
-    t.p0 = t.s * a.split_pages;
-    const int col = t.p0 + t.wave + kUnitWaves * t.lane;
-    const bool in_split = col < t.p0 + a.split_pages && col < a.max_pages;
-    my_page = in_split ? a.block_table[(int64_t)t.b * a.max_pages + col] : 0;
+    int level;
+    if (ORDERED) {
+        level = unit / a.units_per_level;
+        const int bk = unit % a.units_per_level;
+        t.kvh = bk % a.num_kv_heads;
+        t.b = bk / a.num_kv_heads;
+    } else {  // one split per sequence: every unit is split 0
+        level = 0;
+        t.kvh = unit % a.num_kv_heads;
+        t.b = unit / a.num_kv_heads;
+        t.s = 0;
+        t.p0 = 0;
+    }
+    t.last_level = level == a.num_splits - 1;
+    auto load_pages = [&] {
+        const int col = t.p0 + t.wave + kUnitWaves * t.lane;
+        const bool in_split = col < t.p0 + a.split_pages && col < a.max_pages;
+        my_page = in_split ? a.block_table[(int64_t)t.b * a.max_pages + col] : 0;
+    };
+    if (!ORDERED)
+        load_pages();  // issued together with the length load
     int L = a.seq_lens[t.b];
     const int cap = a.max_pages * kPageSize;
     if (L > cap) {
-        if (CHECKED && threadIdx.x == 0 && t.s == 0 && t.kvh == 0)
+        if (CHECKED && threadIdx.x == 0 && t.last_level && t.kvh == 0)
             atomicOr(a.dev_error, RL_DA_DEVERR_LENGTH_TOO_LONG);
         L = cap;
     }
     t.seq_len = L;
     t.npages = L > 0 ? (L + kPageSize - 1) / kPageSize : 0;
     t.nsplit = (t.npages + a.split_pages - 1) / a.split_pages;
-    const int p1 = min(t.p0 + a.split_pages, t.npages);
-    if (t.p0 >= p1)
+    if (ORDERED) {
+        t.s = split_of_level(level, t.nsplit, a.num_splits);
+        if (t.s < 0)
+            return false;
+        t.p0 = t.s * a.split_pages;
+        load_pages();
+    } else if (t.npages == 0) {
         return false;
+    }
+    const int p1 = min(t.p0 + a.split_pages, t.npages);
     t.count = max(0, (p1 - t.p0 - t.wave + kUnitWaves - 1) / kUnitWaves);
     if (CHECKED) {
         const bool bad = t.lane < t.count && (my_page < 0 || (int64_t)my_page >= a.num_pages);
@@ -128,11 +163,11 @@ __device__ __forceinline__ bool begin_task(const SplitArgs& a, WaveTask& t, int3
     return true;
 }
 
-// An empty sequence produces zeros (written once, by the first unit).
+// An empty sequence produces zeros (written once, by its last-level unit).
 template <int G>
 __device__ __forceinline__ void write_zero_rows(const SplitArgs& a, const WaveTask& t)
 {
-    if (t.npages != 0 || t.s != 0)
+    if (t.npages != 0 || !t.last_level)
         return;
     for (int e = threadIdx.x; e < G * (kHeadDim / 8); e += kWave * kUnitWaves) {
         const int g = e / (kHeadDim / 8), chunk = e % (kHeadDim / 8);
@@ -561,7 +596,7 @@ __device__ __forceinline__ void attend_pages(const SplitArgs& a, const WaveTask&
 
 // Three wavefronts per SIMD (two for G = 8): the register budget fits both
 // page buffers and the accumulators without spilling.
-template <int G, bool CHECKED, typename KV>
+template <int G, bool CHECKED, typename KV, bool ORDERED>
 __global__ __launch_bounds__(kWave * kUnitWaves)
 __attribute__((amdgpu_waves_per_eu(G > 4 ? 2 : 3))) void split_mfma(SplitArgs a)
 {
@@ -575,7 +610,7 @@ __attribute__((amdgpu_waves_per_eu(G > 4 ? 2 : 3))) void split_mfma(SplitArgs a)
 
     WaveTask t;
     int32_t my_page;
-    if (!begin_task<CHECKED>(a, t, my_page)) {
+    if (!begin_task<CHECKED, ORDERED>(a, t, my_page)) {
         write_zero_rows<G>(a, t);
         return;
     }
@@ -614,12 +649,17 @@ __device__ __forceinline__ bool begin_task_hp(const SplitArgs& a, WaveTask& t, i
 {
     t.lane = threadIdx.x % kWave;
     t.wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);  // uniform: scalar
+    // Sequence-major order (b, head group, split): a head-parallel unit walks
+    // four times as many pages per wavefront as a four-wavefront unit, and
+    // putting every sequence's last split at the end of the grid measured
+    // worse here (the last level then holds most of a long-tailed batch).
     const int unit = blockIdx.x;
     t.s = unit % a.num_splits;
     const int bg = unit / a.num_splits;
     const int groups = a.num_kv_heads / a.heads_per_unit;
     t.kvh = __builtin_amdgcn_readfirstlane((bg % groups) * a.heads_per_unit + t.wave);
     t.b = bg / groups;
+    t.last_level = t.s == 0;  // the unit that writes an empty sequence's zeros
     t.p0 = t.s * a.split_pages;
     // the first kWave pages' block-table entries (later ones are loaded as
     // the wavefront reaches them)
@@ -668,8 +708,8 @@ __attribute__((amdgpu_waves_per_eu(2))) void split_mfma_hp(SplitArgs a)
     WaveTask t;
     int32_t my_page;
     if (!begin_task_hp<CHECKED>(a, t, my_page)) {
-        // an empty sequence produces zeros, written by the first split
-        if (t.npages == 0 && t.s == 0)
+        // an empty sequence produces zeros, written by its last-level unit
+        if (t.npages == 0 && t.last_level)
             for (int e = t.lane; e < G * (kHeadDim / 8); e += kWave) {
                 const int g = e / (kHeadDim / 8), chunk = e % (kHeadDim / 8);
                 *reinterpret_cast<uint4*>(
@@ -718,14 +758,14 @@ __attribute__((amdgpu_waves_per_eu(2))) void split_mfma_hp(SplitArgs a)
 // lanes of the row with DPP; each row r keeps its own online softmax over its
 // tokens and the four rows are merged with the log-sum-exp rule at the end.
 
-template <int G, bool CHECKED>
+template <int G, bool CHECKED, bool ORDERED>
 __global__ __launch_bounds__(kWave * kUnitWaves) void split_valu_bf16(SplitArgs a)
 {
     __shared__ __attribute__((aligned(16))) UnitShared<G> sh;
 
     WaveTask t;
     int32_t my_page;
-    if (!begin_task<CHECKED>(a, t, my_page)) {
+    if (!begin_task<CHECKED, ORDERED>(a, t, my_page)) {
         write_zero_rows<G>(a, t);
         return;
     }
@@ -921,34 +961,39 @@ __global__ __launch_bounds__(kWave * kMergeWaves) void merge_splits(MergeArgs a)
 
 typedef void (*SplitKernel)(SplitArgs);
 
-template <int G, bool CHECKED>
+// ORDERED: the split-level unit order for runs with more than one split
+// (four-wavefront units only).
+template <int G, bool CHECKED, bool ORDERED>
 SplitKernel pick(bool fp8, bool mfma, bool hp)
 {
     if (hp)
         return fp8 ? split_mfma_hp<G, CHECKED, KvFp8> : split_mfma_hp<G, CHECKED, KvBf16>;
     if (fp8)
-        return split_mfma<G, CHECKED, KvFp8>;  // fp8 pools use the MFMA score tile only
+        return split_mfma<G, CHECKED, KvFp8, ORDERED>;  // fp8 pools: MFMA score tile only
     if (mfma)
-        return split_mfma<G, CHECKED, KvBf16>;
-    return split_valu_bf16<G, CHECKED>;
+        return split_mfma<G, CHECKED, KvBf16, ORDERED>;
+    return split_valu_bf16<G, CHECKED, ORDERED>;
 }
 
-template <bool CHECKED>
+template <bool CHECKED, bool ORDERED>
 SplitKernel select_for_group(int G, bool fp8, bool mfma, bool hp)
 {
     switch (G) {
-    case 1: return pick<1, CHECKED>(fp8, mfma, hp);
-    case 2: return pick<2, CHECKED>(fp8, mfma, hp);
-    case 4: return pick<4, CHECKED>(fp8, mfma, hp);
-    case 8: return pick<8, CHECKED>(fp8, mfma, hp);
+    case 1: return pick<1, CHECKED, ORDERED>(fp8, mfma, hp);
+    case 2: return pick<2, CHECKED, ORDERED>(fp8, mfma, hp);
+    case 4: return pick<4, CHECKED, ORDERED>(fp8, mfma, hp);
+    case 8: return pick<8, CHECKED, ORDERED>(fp8, mfma, hp);
     default: return nullptr;
     }
 }
 
-SplitKernel select_split_kernel(int G, bool checked, bool fp8, bool mfma, bool hp)
+SplitKernel select_split_kernel(int G, bool checked, bool fp8, bool mfma, bool hp, bool ordered)
 {
-    return checked ? select_for_group<true>(G, fp8, mfma, hp)
-                   : select_for_group<false>(G, fp8, mfma, hp);
+    if (checked)
+        return ordered ? select_for_group<true, true>(G, fp8, mfma, hp)
+                       : select_for_group<true, false>(G, fp8, mfma, hp);
+    return ordered ? select_for_group<false, true>(G, fp8, mfma, hp)
+                   : select_for_group<false, false>(G, fp8, mfma, hp);
 }
 
 // kv heads per head-parallel work-group: the largest divisor of Hkv up to 8
@@ -983,7 +1028,8 @@ struct rl_decode_attn {
     bool use_mfma;
     bool head_parallel;
     int heads_per_unit;
-    SplitKernel split_kernel;
+    SplitKernel split_kernel;          // runs with one split per sequence
+    SplitKernel split_kernel_ordered;  // runs with more
     void* workspace;
     size_t workspace_bytes;
     float* ws_acc;
@@ -1107,9 +1153,10 @@ rl_da_status rl_decode_attn_create(const rl_da_config* cfg, rl_decode_attn** out
     h->use_mfma = (cfg->flags & RL_DA_SCORES_ON_VALU) == 0;
     h->head_parallel = uses_head_parallel(cfg);
     h->heads_per_unit = h->head_parallel ? heads_per_unit_for(cfg->num_kv_heads) : 1;
-    h->split_kernel =
-        select_split_kernel(G, (cfg->flags & RL_DA_CHECKED) != 0,
-                            cfg->kv_dtype == RL_DA_KV_FP8_E4M3, h->use_mfma, h->head_parallel);
+    for (int ordered = 0; ordered < 2; ++ordered)
+        (ordered ? h->split_kernel_ordered : h->split_kernel) = select_split_kernel(
+            G, (cfg->flags & RL_DA_CHECKED) != 0, cfg->kv_dtype == RL_DA_KV_FP8_E4M3, h->use_mfma,
+            h->head_parallel, ordered != 0);
     if (hipGetDevice(&h->device) != hipSuccess) {
         free(h);
         return RL_DA_ERR_HIP;
@@ -1208,6 +1255,7 @@ rl_da_status rl_decode_attn_run(rl_decode_attn* h, const void* q, const void* k_
     sa.max_pages = max_pages;
     sa.split_pages = h->split_pages;
     sa.num_splits = num_splits;
+    sa.units_per_level = (int32_t)(units / num_splits);
     sa.heads_per_unit = h->heads_per_unit;
     sa.scale_log2 = scale * kLog2e;
 
@@ -1215,7 +1263,8 @@ rl_da_status rl_decode_attn_run(rl_decode_attn* h, const void* q, const void* k_
     if (h->ev_split_begin != nullptr && hipEventRecord(h->ev_split_begin, st) != hipSuccess)
         return RL_DA_ERR_HIP;
     const int threads = h->head_parallel ? kWave * h->heads_per_unit : kWave * kUnitWaves;
-    hipLaunchKernelGGL(h->split_kernel, dim3((unsigned)units), dim3(threads), 0, st, sa);
+    hipLaunchKernelGGL(num_splits > 1 ? h->split_kernel_ordered : h->split_kernel,
+                       dim3((unsigned)units), dim3(threads), 0, st, sa);
     if (hipGetLastError() != hipSuccess)
         return RL_DA_ERR_HIP;
     if (h->ev_split_end != nullptr && hipEventRecord(h->ev_split_end, st) != hipSuccess)
