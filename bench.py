@@ -102,6 +102,8 @@ def parse_args():
     ap.add_argument("--per-head-units", action="store_true",
                     help="token-major pools: four-wavefront units per kv head")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-input-digests", action="store_true",
+                    help="skip the SHA-256 of the input buffers")
     ap.add_argument("--no-kernel-events", action="store_true",
                     help="do not record events around the split kernel (profiling runs)")
     ap.add_argument("--no-ceilings", action="store_true",
@@ -239,16 +241,58 @@ def cpu_baseline(p, min_seconds=10.0):
         reps += 1
     elt = 2 if p.kv_dtype == "bf16" else 1
     kv = int(L[:nseq].sum()) * p.num_kv_heads * p.head_dim * 2 * elt * reps
+    cores = oracle.max_threads()
+    # one thread, on the first sequence's rows (a few seconds)
+    rows1 = rows[:p.num_q_heads]
+    oracle.set_threads(1)
+    try:
+        t0 = time.perf_counter()
+        oracle.decode_attention(kv_dtype=kv_code, rows=rows1, **h)
+        dt1 = time.perf_counter() - t0
+    finally:
+        oracle.set_threads(cores)
+    kv1 = int(L[0]) * p.num_kv_heads * p.head_dim * 2 * elt
     return {
         "value": kv / dt / 1e9,
         "unit": "GB/s",
-        "cores": oracle.max_threads(),
+        "cores": cores,
         "kind": "oracle",
         "sample": "%d of %d sequences (%d query-head rows, all tokens), fp64, %d passes "
                   "in %.2f s; %.1f query-tokens/s" % (nseq, p.batch, len(rows), reps, dt,
                                                      nseq * reps / dt),
+        "single_thread_GBs": round(kv1 / dt1 / 1e9, 4),
+        "cpu_model": _cpu_model(),
         "seconds": dt,
     }
+
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def input_digests(p):
+    """SHA-256 of every input buffer of a decode problem (host copies)."""
+    import hashlib
+    import torch
+    out = {}
+    for name in ("q", "k_pool", "v_pool", "k_scale", "v_scale", "block_table", "seq_lens"):
+        t = getattr(p, name)
+        if t is None:
+            continue
+        h = hashlib.sha256()
+        flat = t.reshape(-1).view(torch.uint8) if t.dtype != torch.uint8 else t.reshape(-1)
+        step = 1 << 28
+        for i in range(0, flat.numel(), step):
+            h.update(flat[i:i + step].cpu().numpy().tobytes())
+        out[name] = h.hexdigest()[:16]
+    return out
 
 
 def bench_append(args, base, stream):
@@ -584,6 +628,8 @@ def main():
         "kv_bytes_per_step": kv_bytes,
         "hbm_frac": round(value / HBM_PEAK_GBS, 4),
     }
+    if not args.no_input_digests:
+        record["config"]["input_sha256_16"] = input_digests(base)
     if split_ms is not None:
         avg = float(split_ms.mean())
         achieved = alg_bytes / (avg / 1e3) / 1e9
@@ -593,6 +639,8 @@ def main():
             "traffic": load_traffic(traffic_key(args), kernel_source_sha()),
             "kernel": "split-K decode kernel", "avg_us": round(avg * 1e3, 2),
             "min_us": round(float(split_ms.min()) * 1e3, 2),
+            "p10_p50_p90_us": [round(float(x) * 1e3, 2)
+                               for x in np.percentile(split_ms, [10, 50, 90])],
             "bytes_per_launch": alg_bytes,
         }
     attn.close()

@@ -290,3 +290,11 @@ def bf16_to_double(bits: int) -> float:
 
 def max_threads() -> int:
     return _load().rl_oracle_max_threads()
+
+
+def set_threads(n: int) -> None:
+    """Threads for later oracle calls (OpenMP)."""
+    lib = _load()
+    lib.rl_oracle_set_threads.argtypes = [ctypes.c_int]
+    lib.rl_oracle_set_threads.restype = None
+    lib.rl_oracle_set_threads(int(n))

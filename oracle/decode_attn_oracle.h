@@ -111,6 +111,9 @@ double rl_oracle_bf16_to_double(uint16_t bits);
 /* OpenMP threads the oracle will use (1 without OpenMP). */
 int rl_oracle_max_threads(void);
 
+/* Sets the number of OpenMP threads for later calls (no effect without OpenMP). */
+void rl_oracle_set_threads(int n);
+
 #ifdef __cplusplus
 }
 #endif

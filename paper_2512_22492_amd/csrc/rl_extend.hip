@@ -195,9 +195,11 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_bf16(ExtendArgs a)
         // position; rows past the tile's tokens score 0 and stay finite) and
         // O^T += V^T P^T: lane holds dims 16db + 4g4 + jj of row i16.
         const bool masked = j >= first_masked_stage;
-        // Row max over the stage for both row blocks (lane-local over 16
-        // keys, then the two other lane groups of the row).
-        float raw[kRowBlocks][4][4], mx[kRowBlocks];
+        // Scaled scores (log2 units; the mask after the scale, so that any
+        // scale, 0 or negative included, leaves masked keys at -inf) and
+        // their row max over the stage for both row blocks (lane-local over
+        // 16 keys, then the two other lane groups of the row).
+        float sc[kRowBlocks][4][4], mx[kRowBlocks];
 #pragma unroll
         for (int rb = 0; rb < kRowBlocks; ++rb) {
             mx[rb] = -INFINITY;
@@ -205,10 +207,10 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_bf16(ExtendArgs a)
             for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
                 for (int jj = 0; jj < 4; ++jj) {
-                    float x = sacc[rb][kb][jj];
+                    float x = sacc[rb][kb][jj] * a.scale_log2;
                     if (masked)
                         x = j * kStageKeys + 16 * kb + 4 * g4 + jj <= row_pos[rb] ? x : -INFINITY;
-                    raw[rb][kb][jj] = x;
+                    sc[rb][kb][jj] = x;
                     mx[rb] = fmaxf(mx[rb], x);
                 }
         }
@@ -217,7 +219,7 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_bf16(ExtendArgs a)
             mx[rb] = fmaxf(mx[rb], __shfl_xor(mx[rb], 16));
 #pragma unroll
         for (int rb = 0; rb < kRowBlocks; ++rb)
-            mx[rb] = fmaxf(mx[rb], __shfl_xor(mx[rb], 32)) * a.scale_log2;  // finite: key 0
+            mx[rb] = fmaxf(mx[rb], __shfl_xor(mx[rb], 32));  // finite: key 0 is visible
         bool grow = false;
 #pragma unroll
         for (int rb = 0; rb < kRowBlocks; ++rb)
@@ -240,14 +242,13 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_bf16(ExtendArgs a)
         uint4 pt[kRowBlocks][2][2];
 #pragma unroll
         for (int rb = 0; rb < kRowBlocks; ++rb) {
-            const float neg_m = -m_run[rb];
             uint32_t hi[4][2], lo[4][2];
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
                 for (int jp = 0; jp < 2; ++jp) {
-                    const float p0 = exp2_fast(fmaf(raw[rb][kb][2 * jp], a.scale_log2, neg_m));
-                    const float p1 = exp2_fast(fmaf(raw[rb][kb][2 * jp + 1], a.scale_log2, neg_m));
+                    const float p0 = exp2_fast(sc[rb][kb][2 * jp] - m_run[rb]);
+                    const float p1 = exp2_fast(sc[rb][kb][2 * jp + 1] - m_run[rb]);
                     lsum[rb] += p0 + p1;
                     const uint32_t h = pack_bf16x2(p0, p1);
                     hi[kb][jp] = h;
