@@ -371,7 +371,8 @@ def bench_extend(args, dev):
         "dtype": "bf16", "data": "synthetic",
         "config": {"workload": "%s cached prefixes + %d new tokens per sequence" % (args.config, n),
                    "batch": p.batch, "num_q_heads": p.num_q_heads,
-                   "num_kv_heads": p.num_kv_heads, "new_tokens": T, "layout": args.layout},
+                   "num_kv_heads": p.num_kv_heads, "new_tokens": T, "layout": args.layout,
+                   "kv_dtype": p.kv_dtype},
         "roofline": {"bound": "mfma", "achieved": round(tf, 2), "peak": 2500.0,
                      "unit": "TFLOP/s", "frac": round(tf / 2500.0, 4)},
     }

@@ -179,8 +179,9 @@ rl_da_status rl_decode_attn_split_info(const rl_decode_attn* h, int32_t max_page
  * seq_lens as for rl_decode_attn_run.  max_q_per_seq >= every n_b (sizes the
  * grid).  Preconditions: n_b <= L_b <= max_pages * page_size and the table
  * entries of pages 0 .. (L_b-1)/page_size in [0, num_pages).  Needs no
- * handle and no workspace; enqueues one kernel on `stream`.  bf16 pools
- * (either rl_da_layout), head_dim 128, page_size 16 and Hq/Hkv in
+ * handle and no workspace; enqueues one kernel on `stream`.  bf16 or e4m3
+ * pools (k_scale and v_scale non-NULL exactly for e4m3, as for decode),
+ * either rl_da_layout, head_dim 128, page_size 16 and Hq/Hkv in
  * {1, 2, 4, 8, 16} only (else UNSUPPORTED); q, the pools and out 16-byte
  * aligned.
  */

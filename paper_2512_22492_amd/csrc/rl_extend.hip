@@ -1,5 +1,7 @@
 // rl_extend.hip -- extend (prefill) attention over the paged KV cache.
 
+#include <type_traits>
+
 #include "rl_common.h"
 
 using namespace rl_da;
@@ -44,6 +46,8 @@ struct ExtendArgs {
     const int32_t* q_start;     // [B+1]
     const uint8_t* k_pool;
     const uint8_t* v_pool;
+    const float* k_scale;       // [P][Hkv], e4m3 pools only
+    const float* v_scale;
     const int32_t* block_table;
     const int32_t* seq_lens;
     uint16_t* out;              // bf16 [T][Hq][D]
@@ -57,9 +61,12 @@ struct ExtendArgs {
     float scale_log2;
 };
 
-template <int G>
+// FP8: e4m3 pools.  Codes are staged as exact bf16 (scale 1); a page's
+// k_scale multiplies its keys' scores and its v_scale the probabilities that
+// weight its values (l sums the unscaled probabilities), as in decode.
+template <int G, bool FP8>
 __global__ __launch_bounds__(kWave * kUnitWaves)
-__attribute__((amdgpu_waves_per_eu(2))) void extend_bf16(ExtendArgs a)
+__attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
 {
     static_assert(G >= 1 && G <= 16 && 16 % G == 0, "16-row blocks hold whole groups");
     constexpr int kTileTok = kTileRows / G;
@@ -118,11 +125,13 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_bf16(ExtendArgs a)
     }
 
     // Staging: thread t moves keys 2(t/8) and 2(t/8)+1, dims 16(t%8)..+15, of
-    // K and of V (four 16-byte loads each).
+    // K and of V (two 16-byte loads each, one for e4m3).
     const int st_kp = threadIdx.x / 8, st_c = threadIdx.x % 8;
     const int32_t* bt = a.block_table + (int64_t)b * a.max_pages;
-    const int64_t st_off = (int64_t)kvh * a.head_bytes + 2 * (16 * st_c);
-    uint4 kr[2][2], vr[2][2];  // [key of the pair][half of the 16 dims]
+    constexpr int kElt = FP8 ? 1 : 2;
+    const int64_t st_off = (int64_t)kvh * a.head_bytes + kElt * (16 * st_c);
+    const int npages = (L + kPageSize - 1) / kPageSize;
+    uint4 kr[2][2], vr[2][2];  // [key of the pair][half of the 16 dims] (bf16)
     auto fetch = [&](int stage) {
 #pragma unroll
         for (int e = 0; e < 2; ++e) {
@@ -131,15 +140,36 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_bf16(ExtendArgs a)
                 const int64_t off = bt[key / kPageSize] * a.page_bytes + st_off +
                                     (int64_t)(key % kPageSize) * a.row_bytes;
                 kr[e][0] = load_stream16(a.k_pool + off);
-                kr[e][1] = load_stream16(a.k_pool + off + 16);
                 vr[e][0] = load_stream16(a.v_pool + off);
-                vr[e][1] = load_stream16(a.v_pool + off + 16);
+                if (!FP8) {
+                    kr[e][1] = load_stream16(a.k_pool + off + 16);
+                    vr[e][1] = load_stream16(a.v_pool + off + 16);
+                }
             } else {  // slots past the sequence end may hold NaN: stage zeros
                 kr[e][0] = kr[e][1] = vr[e][0] = vr[e][1] = make_uint4(0, 0, 0, 0);
             }
         }
     };
+    // 16 e4m3 codes to 16 bf16 (exact), in order.
+    auto widen = [](const uint4& c, uint4& lo, uint4& hi) {
+        auto cvt = [](uint32_t w, auto upper) {
+            return __builtin_bit_cast(
+                uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, decltype(upper)::value));
+        };
+        using F = std::false_type;
+        using T = std::true_type;
+        lo = make_uint4(cvt(c.x, F{}), cvt(c.x, T{}), cvt(c.y, F{}), cvt(c.y, T{}));
+        hi = make_uint4(cvt(c.z, F{}), cvt(c.z, T{}), cvt(c.w, F{}), cvt(c.w, T{}));
+    };
     auto stash = [&](int buf) {
+        if (FP8) {
+#pragma unroll
+            for (int e = 0; e < 2; ++e) {
+                const uint4 kc = kr[e][0], vc = vr[e][0];
+                widen(kc, kr[e][0], kr[e][1]);
+                widen(vc, vr[e][0], vr[e][1]);
+            }
+        }
 #pragma unroll
         for (int e = 0; e < 2; ++e) {
             uint4* krow = reinterpret_cast<uint4*>(&k_lds[buf][2 * st_kp + e][16 * st_c]);
@@ -168,6 +198,24 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_bf16(ExtendArgs a)
         if (j + 1 < nstages)
             fetch(j + 1);
         __syncthreads();
+
+        // Score multiplier (scale * log2 e, times k_scale) and value scale
+        // of the stage's four pages; pages past the sequence get 1 (their
+        // keys are masked and their values staged as zeros).
+        float sl[4], vsc[4];
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) {
+            sl[kb] = a.scale_log2;
+            vsc[kb] = 1.0f;
+            if (FP8) {
+                const int pg = j * kStagePages + kb;
+                if (pg < npages) {
+                    const int64_t slab = (int64_t)bt[pg] * a.num_kv_heads + kvh;
+                    sl[kb] *= a.k_scale[slab];
+                    vsc[kb] = a.v_scale[slab];
+                }
+            }
+        }
 
         // S^T for the stage's four 16-key blocks: lane holds row i16, keys
         // 16kb + 4g4 + jj.
@@ -207,7 +255,7 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_bf16(ExtendArgs a)
             for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
                 for (int jj = 0; jj < 4; ++jj) {
-                    float x = sacc[rb][kb][jj] * a.scale_log2;
+                    float x = sacc[rb][kb][jj] * sl[kb];
                     if (masked)
                         x = j * kStageKeys + 16 * kb + 4 * g4 + jj <= row_pos[rb] ? x : -INFINITY;
                     sc[rb][kb][jj] = x;
@@ -247,9 +295,13 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_bf16(ExtendArgs a)
             for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
                 for (int jp = 0; jp < 2; ++jp) {
-                    const float p0 = exp2_fast(sc[rb][kb][2 * jp] - m_run[rb]);
-                    const float p1 = exp2_fast(sc[rb][kb][2 * jp + 1] - m_run[rb]);
+                    float p0 = exp2_fast(sc[rb][kb][2 * jp] - m_run[rb]);
+                    float p1 = exp2_fast(sc[rb][kb][2 * jp + 1] - m_run[rb]);
                     lsum[rb] += p0 + p1;
+                    if (FP8) {
+                        p0 *= vsc[kb];
+                        p1 *= vsc[kb];
+                    }
                     const uint32_t h = pack_bf16x2(p0, p1);
                     hi[kb][jp] = h;
                     lo[kb][jp] = pack_bf16x2(p0 - __uint_as_float(h << 16),
@@ -344,11 +396,12 @@ rl_da_status rl_extend_attn(const void* q, const int32_t* q_start, int32_t max_q
         return RL_DA_ERR_INVALID_ARG;
     if (!aligned16(q) || !aligned16(k_pool) || !aligned16(v_pool) || !aligned16(out))
         return RL_DA_ERR_INVALID_ARG;
+    const bool fp8 = kv_dtype == RL_DA_KV_FP8_E4M3;
     PoolStrides ps;
-    if (!pool_strides(layout, num_kv_heads, 2, &ps))
+    if (!pool_strides(layout, num_kv_heads, fp8 ? 1 : 2, &ps))
         return RL_DA_ERR_INVALID_ARG;
     const int G = num_q_heads / num_kv_heads;
-    if (head_dim != kHeadDim || page_size != kPageSize || kv_dtype != RL_DA_KV_BF16 ||
+    if (head_dim != kHeadDim || page_size != kPageSize ||
         (G != 1 && G != 2 && G != 4 && G != 8 && G != 16))
         return RL_DA_ERR_UNSUPPORTED;
     if (batch == 0 || max_q_per_seq == 0)
@@ -359,6 +412,8 @@ rl_da_status rl_extend_attn(const void* q, const int32_t* q_start, int32_t max_q
     ea.q_start = q_start;
     ea.k_pool = (const uint8_t*)k_pool;
     ea.v_pool = (const uint8_t*)v_pool;
+    ea.k_scale = k_scale;
+    ea.v_scale = v_scale;
     ea.block_table = block_table;
     ea.seq_lens = seq_lens;
     ea.out = (uint16_t*)out;
@@ -375,13 +430,16 @@ rl_da_status rl_extend_attn(const void* q, const int32_t* q_start, int32_t max_q
         return RL_DA_ERR_UNSUPPORTED;
     hipStream_t st = (hipStream_t)stream;
     const dim3 grid((unsigned)blocks), block(kWave * kUnitWaves);
+    typedef void (*Kernel)(ExtendArgs);
+    Kernel k;
     switch (G) {
-    case 1: hipLaunchKernelGGL(extend_bf16<1>, grid, block, 0, st, ea); break;
-    case 2: hipLaunchKernelGGL(extend_bf16<2>, grid, block, 0, st, ea); break;
-    case 4: hipLaunchKernelGGL(extend_bf16<4>, grid, block, 0, st, ea); break;
-    case 8: hipLaunchKernelGGL(extend_bf16<8>, grid, block, 0, st, ea); break;
-    default: hipLaunchKernelGGL(extend_bf16<16>, grid, block, 0, st, ea); break;
+    case 1: k = fp8 ? extend_attn<1, true> : extend_attn<1, false>; break;
+    case 2: k = fp8 ? extend_attn<2, true> : extend_attn<2, false>; break;
+    case 4: k = fp8 ? extend_attn<4, true> : extend_attn<4, false>; break;
+    case 8: k = fp8 ? extend_attn<8, true> : extend_attn<8, false>; break;
+    default: k = fp8 ? extend_attn<16, true> : extend_attn<16, false>; break;
     }
+    hipLaunchKernelGGL(k, grid, block, 0, st, ea);
     return hipGetLastError() == hipSuccess ? RL_DA_OK : RL_DA_ERR_HIP;
 }
 

@@ -14,11 +14,11 @@ from gpu_util import bf16_to_f64, check_close, device
 pytestmark = pytest.mark.gpu
 
 
-def extend_problem(new, prior, seed, hq=8, hkv=2, layout="hnd"):
+def extend_problem(new, prior, seed, hq=8, hkv=2, layout="hnd", kv="bf16"):
     lengths = [a + b for a, b in zip(new, prior)]
     p = workloads.make_problem("ext", batch=len(new), num_q_heads=hq, num_kv_heads=hkv,
                                lengths=lengths, seed=seed, pool_factor=1.25,
-                               layout=layout).to(device())
+                               layout=layout, kv_dtype=kv).to(device())
     gen = torch.Generator().manual_seed(seed + 3)
     q = torch.randn((int(sum(new)), hq, 128), generator=gen).to(torch.bfloat16).to(device())
     q_start = torch.tensor(np.concatenate([[0], np.cumsum(new)]), dtype=torch.int32,
@@ -36,17 +36,27 @@ def run_extend(p, q, q_start, max_new):
 def p_split_bound(p):
     """The PV MFMA takes each probability as two bf16 terms, so every weight
     carries up to 2^-18 relative error and the normalisation up to another
-    2^-18: the output may move by 2^-17 * max|V| beyond the bf16 rounding."""
-    return 2.0 ** -17 * float(p.v_pool.float().abs().max())
+    2^-18: the output may move by 2^-17 * max|V| beyond the bf16 rounding
+    (V decoded with its slab scales for e4m3 pools)."""
+    if p.kv_dtype == "bf16":
+        vmax = float(p.v_pool.float().abs().max())
+    else:
+        codes = p.v_pool.view(torch.float8_e4m3fn).float().abs()
+        dims = (2, 3) if p.layout == "hnd" else (1, 3)   # slot and dim axes
+        vmax = float((codes.amax(dim=dims) * p.v_scale).max())
+    return 2.0 ** -17 * vmax
 
 
 def oracle_extend(p, q, q_start):
     h = p.host_arrays()
+    kw = {}
+    if p.kv_dtype != "bf16":
+        kw = dict(kv_dtype=oracle.KV_FP8_E4M3, k_scale=h["k_scale"], v_scale=h["v_scale"])
     return oracle.extend_attention(q.cpu().view(torch.int16).numpy().view(np.uint16),
                                    q_start.cpu().numpy(), h["k_pool"], h["v_pool"],
                                    h["block_table"], h["seq_lens"],
                                    num_kv_heads=p.num_kv_heads, scale=p.scale,
-                                   layout=p.layout)
+                                   layout=p.layout, **kw)
 
 
 CASES = [
@@ -145,3 +155,18 @@ def test_extend_nhd_pools_match_oracle_and_the_hnd_result(hq, hkv):
                       "extend nhd G=%d" % (hq // hkv), extra_abs=p_split_bound(pn)))
     same = run_extend(ph, q, q_start, max(new))
     assert torch.equal(got.view(torch.int16), same.view(torch.int16))
+
+
+@pytest.mark.parametrize("layout", ["hnd", "nhd"])
+@pytest.mark.parametrize("hq,hkv", [(8, 2), (32, 8), (16, 16)])
+@pytest.mark.parametrize("case", range(len(CASES)))
+def test_extend_fp8_pools_match_oracle(hq, hkv, case, layout):
+    """e4m3 pools with per-slab scales: codes staged as exact bf16, k_scale on
+    the scores, v_scale on the probabilities."""
+    new, prior = CASES[case]
+    p, q, q_start = extend_problem(new, prior, seed=50 + case, hq=hq, hkv=hkv, layout=layout,
+                                   kv="fp8_e4m3")
+    got = bf16_to_f64(run_extend(p, q, q_start, max(new)))
+    print(check_close(got, oracle_extend(p, q, q_start),
+                      "extend fp8 %s G=%d case %d" % (layout, hq // hkv, case),
+                      extra_abs=p_split_bound(p)))
