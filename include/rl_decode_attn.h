@@ -36,7 +36,11 @@
  * stream.  Results are deterministic: no atomics take part in any reduction,
  * the split size is fixed per handle and partial results merge in a fixed
  * order, so a sequence's output does not depend on the rest of the batch or
- * on where its pages sit in the pool.
+ * on where its pages sit in the pool.  With several splits per sequence and
+ * more work units than the device holds at once, the split kernel runs
+ * persistent work-groups that take units, longest first, from a counter in
+ * the handle's workspace (the last work-group resets it); which work-group
+ * computes a unit never changes a result.
  *
  * Errors.  Every entry point returns an rl_da_status; nothing is thrown
  * across the interface.  run() checks its host-visible arguments and returns

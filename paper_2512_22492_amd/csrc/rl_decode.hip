@@ -48,6 +48,17 @@ constexpr int kMaxSplitTokens = kWave * kUnitWaves * kPageSize;
 // every wavefront walks all pages of its split
 constexpr int kMaxHeadsPerUnit = 8;
 constexpr int kMaxSplitTokensHp = 4096;
+// Launches with more than one split run persistent work-groups that take
+// units longest first from a plan built in LDS; batches above this size
+// take the units in sequence order instead (the plan would not fit).
+constexpr int kMaxPlanBatch = 4096;
+
+// How the split kernel of a launch with several splits takes its units.
+enum Schedule : int32_t {
+    kOnePerGroup = 0,   // grid = units: work-group g runs unit g (sequence order)
+    kQueueInOrder = 1,  // persistent, units in sequence order (empty ones included)
+    kQueuePlanned = 2,  // persistent, units longest first from the LDS plan
+};
 
 struct SplitArgs {
     const uint16_t* q;          // bf16 bits [B][Hq][D]
@@ -70,8 +81,10 @@ struct SplitArgs {
     int32_t max_pages;
     int32_t split_pages;
     int32_t num_splits;         // ceil(max_pages / split_pages)
-    int32_t units_per_level;    // work-groups per split level (batch x heads or head groups)
     int32_t heads_per_unit;     // kv heads per head-parallel work-group
+    int32_t batch;
+    int32_t schedule;           // several splits: a Schedule
+    int32_t* queue;             // persistent launch: [0] next unit, [1] finished work-groups
     float scale_log2;           // scale * log2(e)
 };
 
@@ -83,71 +96,51 @@ struct WaveTask {
     int nsplit;    // splits of this sequence
     int p0;        // first page of the unit
     int count;     // pages of this wavefront (may be 0)
-    bool last_level;  // the unit runs in the grid's last split level
+    bool owner;    // the one unit per (sequence, head) that writes an empty
+                   // sequence's zeros and reports a too-long sequence
 };
 
-// Split level of a work-group and its sequence's split.  The grid runs in
-// num_splits levels of units_per_level work-groups; level v holds, for every
-// (sequence, head), the split with num_splits - 1 - v splits after it, so
-// that every sequence's last split -- the only one that can be short -- is
-// dispatched after all full ones (the dispatcher hands out work-groups in
-// order, and short units at the end leave the smallest tail).  A sequence
-// with fewer splits has no unit on the first levels.  The split a unit
-// computes, and so every result, does not depend on this order.
-__device__ __forceinline__ int split_of_level(int level, int nsplit, int num_splits)
-{
-    return nsplit - num_splits + level;  // < 0: no such split
-}
-
-// Decodes (blockIdx.x, wavefront) into a task and loads its block-table
+// Fills a wavefront's task for the unit (sequence b, kv head kvh, split s)
+// -- s < 0 meaning the sequence's last split -- and loads its block-table
 // entries (lane i: page p0 + wave + 4i) together with the sequence length.
 // Entries past the sequence's end lie inside the table row and are loaded
 // but never used.  Returns false, for every wavefront of the unit alike, when
 // the unit holds no page of its sequence.
-template <bool CHECKED, bool ORDERED>
-__device__ __forceinline__ bool begin_task(const SplitArgs& a, WaveTask& t, int32_t& my_page)
+template <bool CHECKED>
+__device__ __forceinline__ bool begin_unit(const SplitArgs& a, WaveTask& t, int32_t& my_page,
+                                           int b, int kvh, int s, bool owner)
 {
     t.lane = threadIdx.x % kWave;
     t.wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);  // uniform: scalar
-    const int unit = blockIdx.x;
-    int level;
-    if (ORDERED) {
-        level = unit / a.units_per_level;
-        const int bk = unit % a.units_per_level;
-        t.kvh = bk % a.num_kv_heads;
-        t.b = bk / a.num_kv_heads;
-    } else {  // one split per sequence: every unit is split 0
-        level = 0;
-        t.kvh = unit % a.num_kv_heads;
-        t.b = unit / a.num_kv_heads;
-        t.s = 0;
-        t.p0 = 0;
-    }
-    t.last_level = level == a.num_splits - 1;
+    t.b = b;
+    t.kvh = kvh;
+    t.owner = owner;
+    t.s = max(s, 0);
+    t.p0 = t.s * a.split_pages;
     auto load_pages = [&] {
         const int col = t.p0 + t.wave + kUnitWaves * t.lane;
         const bool in_split = col < t.p0 + a.split_pages && col < a.max_pages;
         my_page = in_split ? a.block_table[(int64_t)t.b * a.max_pages + col] : 0;
     };
-    if (!ORDERED)
+    if (s >= 0)
         load_pages();  // issued together with the length load
     int L = a.seq_lens[t.b];
     const int cap = a.max_pages * kPageSize;
     if (L > cap) {
-        if (CHECKED && threadIdx.x == 0 && t.last_level && t.kvh == 0)
+        if (CHECKED && threadIdx.x == 0 && t.owner && t.kvh == 0)
             atomicOr(a.dev_error, RL_DA_DEVERR_LENGTH_TOO_LONG);
         L = cap;
     }
     t.seq_len = L;
     t.npages = L > 0 ? (L + kPageSize - 1) / kPageSize : 0;
     t.nsplit = (t.npages + a.split_pages - 1) / a.split_pages;
-    if (ORDERED) {
-        t.s = split_of_level(level, t.nsplit, a.num_splits);
-        if (t.s < 0)
+    if (s < 0) {
+        if (t.nsplit == 0)
             return false;
+        t.s = t.nsplit - 1;
         t.p0 = t.s * a.split_pages;
         load_pages();
-    } else if (t.npages == 0) {
+    } else if (t.s >= t.nsplit) {
         return false;
     }
     const int p1 = min(t.p0 + a.split_pages, t.npages);
@@ -163,11 +156,263 @@ __device__ __forceinline__ bool begin_task(const SplitArgs& a, WaveTask& t, int3
     return true;
 }
 
-// An empty sequence produces zeros (written once, by its last-level unit).
+// ------------------------------------------------- persistent schedule ---
+//
+// A launch with more than one split runs about one work-group per resident
+// slot; each takes units one after another from a counter in the workspace.
+// (The hardware hands out the work-groups of a grid in index order,
+// round-robin over the XCDs and their shader engines, and stalls while the
+// engine next in turn is full, so a static grid of unequal units leaves
+// engines idle behind a busy one.)  Units go longest first: every full split,
+// then each sequence's last split in descending length, empty sequences last,
+// so the launch ends on its shortest units.  Each work-group builds that
+// order in LDS from the sequence lengths:
+//   full[b]  = splits of sequence b before its last one, prefix-summed
+//              (full[batch] = F, all full splits);
+//   order[j] = sequences by the length of their last split, longest first:
+//              kLengthClasses classes of last-split page counts, each class
+//              in sequence order (a stable counting sort, so that every
+//              work-group builds the same order).
+// With U units per (sequence, split), unit i < F*U is full split i/U of the
+// sequence found by binary search in full[], and unit F*U + i is the last
+// split of order[i/U].  Without a plan (kQueueInOrder, or kOnePerGroup when
+// every unit has a work-group of its own) unit i is split (i/U) % num_splits
+// of sequence i/(U*num_splits), empty ones included.
+// Which work-group takes a unit never changes a result.
+
+// Exclusive prefix sum of data[0 .. n) in place by the work-group; returns
+// the total.  tmp holds one int per wavefront.
+__device__ __forceinline__ int block_exclusive_scan(int* data, int n, int* tmp)
+{
+    const int tid = threadIdx.x;
+    const int nt = blockDim.x;
+    const int per = (n + nt - 1) / nt;
+    const int lo = min(tid * per, n), hi = min(lo + per, n);
+    int sum = 0;
+    for (int i = lo; i < hi; ++i)
+        sum += data[i];
+    const int lane = tid % kWave;
+    int x = sum;
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+        const int y = __shfl_up(x, d, kWave);
+        if (lane >= d)
+            x += y;
+    }
+    if (lane == kWave - 1)
+        tmp[tid / kWave] = x;
+    __syncthreads();
+    int before = 0, total = 0;
+    for (int w = 0; w < nt / kWave; ++w) {
+        const int v = tmp[w];
+        before += w < tid / kWave ? v : 0;
+        total += v;
+    }
+    int run = before + x - sum;
+    for (int i = lo; i < hi; ++i) {
+        const int v = data[i];
+        data[i] = run;
+        run += v;
+    }
+    __syncthreads();
+    return total;
+}
+
+constexpr int kLengthClasses = 8;
+constexpr int kMaxPlanWaves = kMaxHeadsPerUnit;  // wavefronts of the largest work-group
+
+// Ints of LDS the plan needs for `batch` sequences: full[], order[], one
+// byte per sequence for its length class, the scans' per-wavefront totals.
+__host__ __device__ constexpr int plan_ints(int batch)
+{
+    return 2 * batch + 1 + (batch + 3) / 4 + kLengthClasses * kMaxPlanWaves;
+}
+
+// Full splits of sequence b and the length class of its last split (0 for
+// a full-length last split, rising as it gets shorter; an empty sequence is
+// in the last class).
+__device__ __forceinline__ void split_shape(const SplitArgs& a, int b, int& full, int& cls)
+{
+    const int L = min(a.seq_lens[b], a.max_pages * kPageSize);
+    const int np = L > 0 ? (L + kPageSize - 1) / kPageSize : 0;
+    const int ns = (np + a.split_pages - 1) / a.split_pages;
+    full = max(ns - 1, 0);
+    const int last = ns > 0 ? np - (ns - 1) * a.split_pages : 0;  // 0 .. split_pages
+    cls = (a.split_pages - last) * kLengthClasses / (a.split_pages + 1);
+}
+
+// Exclusive prefix over the work-group's threads of K counts per thread, in
+// place; total[c] gets the sum of count c.  tmp holds K * kMaxPlanWaves ints.
+template <int K>
+__device__ __forceinline__ void block_scan_counts(int (&v)[K], int (&total)[K], int* tmp)
+{
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    const int nw = blockDim.x / kWave;
+    int x[K];
+#pragma unroll
+    for (int c = 0; c < K; ++c)
+        x[c] = v[c];
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+#pragma unroll
+        for (int c = 0; c < K; ++c) {
+            const int y = __shfl_up(x[c], d, kWave);
+            if (lane >= d)
+                x[c] += y;
+        }
+    }
+    if (lane == kWave - 1) {
+#pragma unroll
+        for (int c = 0; c < K; ++c)
+            tmp[c * kMaxPlanWaves + wave] = x[c];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int c = 0; c < K; ++c) {
+        int before = 0, tot = 0;
+        for (int w = 0; w < nw; ++w) {
+            const int t = tmp[c * kMaxPlanWaves + w];
+            before += w < wave ? t : 0;
+            tot += t;
+        }
+        v[c] = before + x[c] - v[c];
+        total[c] = tot;
+    }
+    __syncthreads();
+}
+
+// Builds full[] and order[] (see above); returns F.  The result depends only
+// on the sequence lengths, read once.  Ends with a barrier.
+__device__ __forceinline__ int build_plan(const SplitArgs& a, int* plan)
+{
+    const int B = a.batch, nt = blockDim.x;
+    int* full = plan;
+    int* order = plan + B + 1;
+    uint8_t* cls_of = reinterpret_cast<uint8_t*>(order + B);
+    int* tmp = order + B + (B + 3) / 4;
+    for (int b = threadIdx.x; b < B; b += nt) {
+        int f, cls;
+        split_shape(a, b, f, cls);
+        full[b] = f;
+        cls_of[b] = (uint8_t)cls;
+    }
+    if (threadIdx.x == 0)
+        full[B] = 0;
+    __syncthreads();
+    const int F = block_exclusive_scan(full, B + 1, tmp);
+    // order: each thread takes a contiguous slice of sequences
+    const int per = (B + nt - 1) / nt;
+    const int lo = min((int)threadIdx.x * per, B), hi = min(lo + per, B);
+    int pos[kLengthClasses], total[kLengthClasses];
+#pragma unroll
+    for (int c = 0; c < kLengthClasses; ++c)
+        pos[c] = 0;
+    for (int b = lo; b < hi; ++b) {
+        const int cls = cls_of[b];
+#pragma unroll
+        for (int c = 0; c < kLengthClasses; ++c)
+            pos[c] += cls == c;
+    }
+    block_scan_counts(pos, total, tmp);
+    int start = 0;
+#pragma unroll
+    for (int c = 0; c < kLengthClasses; ++c) {
+        pos[c] += start;  // class c begins after every longer class
+        start += total[c];
+    }
+    for (int b = lo; b < hi; ++b) {
+        const int cls = cls_of[b];
+        int at = 0;
+#pragma unroll
+        for (int c = 0; c < kLengthClasses; ++c) {
+            at = cls == c ? pos[c] : at;
+            pos[c] += cls == c;
+        }
+        order[at] = b;
+    }
+    __syncthreads();
+    return F;
+}
+
+// Runs unit(b, k, s, owner) -- k the unit's index within its (sequence,
+// split), s < 0 for a last split -- for every unit of the launch.  Work-group
+// g starts with unit g; later units come from a.queue (gridDim.x + the
+// count of earlier requests), requested when the current unit starts and
+// needed only when it ends.  The last work-group to finish resets the queue
+// for the next launch.  plan: the dynamic LDS (unused without a plan).
+template <typename Unit>
+__device__ __forceinline__ void run_persistent(const SplitArgs& a, int U, int* plan, Unit unit)
+{
+    if (a.schedule == kOnePerGroup) {
+        const int j = blockIdx.x / U;
+        const int s = j % a.num_splits;
+        unit(a, j / a.num_splits, blockIdx.x % U, s, s == 0);
+        return;
+    }
+    __shared__ int s_item[2];
+    unsigned* const counter = reinterpret_cast<unsigned*>(&a.queue[0]);
+    const bool planned = a.schedule == kQueuePlanned;
+    int F = 0, total;
+    if (planned) {
+        F = build_plan(a, plan);
+        total = (F + a.batch) * U;
+    } else {
+        total = a.batch * a.num_splits * U;
+    }
+    const int* full = plan;
+    const int* order = plan + a.batch + 1;
+    int item = blockIdx.x;
+    for (int cur = 0;; cur ^= 1) {
+        if (item >= total)
+            break;
+        // atomicInc (not atomicAdd) leaves the wait for the result at its use
+        unsigned next = 0;
+        if (threadIdx.x == 0)
+            next = atomicInc(counter, 0xffffffffu);
+        const int k = item % U, j = item / U;
+        int b, s;
+        bool owner;
+        if (!planned) {
+            s = j % a.num_splits;
+            b = j / a.num_splits;
+            owner = s == 0;
+        } else if (j < F) {
+            int lo = 0, hi = a.batch;  // full[lo] <= j < full[hi]
+            while (hi - lo > 1) {
+                const int mid = (lo + hi) >> 1;
+                if (full[mid] <= j)
+                    lo = mid;
+                else
+                    hi = mid;
+            }
+            b = lo;
+            s = j - full[lo];
+            owner = false;
+        } else {
+            b = order[j - F];
+            s = -1;
+            owner = true;
+        }
+        b = __builtin_amdgcn_readfirstlane(b);
+        s = __builtin_amdgcn_readfirstlane(s);
+        if (b >= 0 && b < a.batch && s < a.num_splits)  // holds by construction
+            unit(a, b, k, s, owner);
+        if (threadIdx.x == 0)
+            s_item[cur] = (int)gridDim.x + (int)next;
+        __syncthreads();
+        item = __builtin_amdgcn_readfirstlane(s_item[cur]);
+    }
+    if (threadIdx.x == 0 && atomicAdd(&a.queue[1], 1) == (int)gridDim.x - 1) {
+        atomicExch(&a.queue[0], 0);
+        atomicExch(&a.queue[1], 0);
+    }
+}
+
+// An empty sequence produces zeros (written once, by its owner unit).
 template <int G>
 __device__ __forceinline__ void write_zero_rows(const SplitArgs& a, const WaveTask& t)
 {
-    if (t.npages != 0 || !t.last_level)
+    if (t.npages != 0 || !t.owner)
         return;
     for (int e = threadIdx.x; e < G * (kHeadDim / 8); e += kWave * kUnitWaves) {
         const int g = e / (kHeadDim / 8), chunk = e % (kHeadDim / 8);
@@ -596,9 +841,11 @@ __device__ __forceinline__ void attend_pages(const SplitArgs& a, const WaveTask&
 
 // Three wavefronts per SIMD (two for G = 8): the register budget fits both
 // page buffers and the accumulators without spilling.
-template <int G, bool CHECKED, typename KV, bool ORDERED>
+// A persistent work-group keeps values live across its units; it takes the
+// two-wave register budget, which holds them without spilling.
+template <int G, bool CHECKED, typename KV, bool PERSISTENT>
 __global__ __launch_bounds__(kWave * kUnitWaves)
-__attribute__((amdgpu_waves_per_eu(G > 4 ? 2 : 3))) void split_mfma(SplitArgs a)
+__attribute__((amdgpu_waves_per_eu(G > 4 || PERSISTENT ? 2 : 3))) void split_mfma(SplitArgs a)
 {
     static_assert(G == 1 || G == 2 || G == 4 || G == 8, "query group of 1, 2, 4 or 8 heads");
     using SR = ScoreRows<G>;
@@ -607,29 +854,36 @@ __attribute__((amdgpu_waves_per_eu(G > 4 ? 2 : 3))) void split_mfma(SplitArgs a)
     __shared__ __attribute__((aligned(16))) float lds_p_all[kUnitWaves][kPageSize * kH];
     __shared__ __attribute__((aligned(16))) float lds_alpha_all[kUnitWaves][kH];
     __shared__ __attribute__((aligned(16))) UnitShared<G> sh;
+    extern __shared__ int plan[];
 
-    WaveTask t;
-    int32_t my_page;
-    if (!begin_task<CHECKED, ORDERED>(a, t, my_page)) {
-        write_zero_rows<G>(a, t);
-        return;
-    }
-    float acc[G][8], m[kE], l_row[kE];
-    int head[kE];
-    attend_pages<G, CHECKED, KV, kUnitWaves>(a, t, my_page, lds_p_all[t.wave],
-                                             lds_alpha_all[t.wave], acc, m, l_row, head);
-    // Lane group kg holds m and l of heads head[e]; its value lanes (r = kg)
-    // stash those heads.
-    const int c = t.lane & 15;
+    auto unit = [&](const SplitArgs& a, int b, int kvh, int s, bool owner) {
+        WaveTask t;
+        int32_t my_page;
+        if (!begin_unit<CHECKED>(a, t, my_page, b, kvh, s, owner)) {
+            write_zero_rows<G>(a, t);
+            return;
+        }
+        float acc[G][8], m[kE], l_row[kE];
+        int head[kE];
+        attend_pages<G, CHECKED, KV, kUnitWaves>(a, t, my_page, lds_p_all[t.wave],
+                                                 lds_alpha_all[t.wave], acc, m, l_row, head);
+        // Lane group kg holds m and l of heads head[e]; its value lanes (r = kg)
+        // stash those heads.
+        const int c = t.lane & 15;
 #pragma unroll
-    for (int e = 0; e < kE; ++e) {
+        for (int e = 0; e < kE; ++e) {
 #pragma unroll
-        for (int g = 0; g < G; ++g)
-            if (g == head[e])
-                stash_state<G>(sh, t.wave, g, c, acc[g], m[e], l_row[e]);
-    }
-    __syncthreads();
-    merge_unit<G>(a, t, sh);
+            for (int g = 0; g < G; ++g)
+                if (g == head[e])
+                    stash_state<G>(sh, t.wave, g, c, acc[g], m[e], l_row[e]);
+        }
+        __syncthreads();
+        merge_unit<G>(a, t, sh);
+    };
+    if (PERSISTENT)
+        run_persistent(a, a.num_kv_heads, plan, unit);
+    else  // one split per sequence: unit (b, kv head) = blockIdx.x
+        unit(a, blockIdx.x / a.num_kv_heads, blockIdx.x % a.num_kv_heads, 0, true);
 }
 
 // ------------------------------------- head-parallel split kernel, MFMA QK ---
@@ -645,37 +899,42 @@ __attribute__((amdgpu_waves_per_eu(G > 4 ? 2 : 3))) void split_mfma(SplitArgs a)
 // split for the merge kernel.
 
 template <bool CHECKED>
-__device__ __forceinline__ bool begin_task_hp(const SplitArgs& a, WaveTask& t, int32_t& my_page)
+__device__ __forceinline__ bool begin_unit_hp(const SplitArgs& a, WaveTask& t, int32_t& my_page,
+                                              int b, int group, int s, bool owner)
 {
     t.lane = threadIdx.x % kWave;
     t.wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);  // uniform: scalar
-    // Sequence-major order (b, head group, split): a head-parallel unit walks
-    // four times as many pages per wavefront as a four-wavefront unit, and
-    // putting every sequence's last split at the end of the grid measured
-    // worse here (the last level then holds most of a long-tailed batch).
-    const int unit = blockIdx.x;
-    t.s = unit % a.num_splits;
-    const int bg = unit / a.num_splits;
-    const int groups = a.num_kv_heads / a.heads_per_unit;
-    t.kvh = __builtin_amdgcn_readfirstlane((bg % groups) * a.heads_per_unit + t.wave);
-    t.b = bg / groups;
-    t.last_level = t.s == 0;  // the unit that writes an empty sequence's zeros
+    t.kvh = __builtin_amdgcn_readfirstlane(group * a.heads_per_unit + t.wave);
+    t.b = b;
+    t.owner = owner;
+    t.s = max(s, 0);
     t.p0 = t.s * a.split_pages;
     // the first kWave pages' block-table entries (later ones are loaded as
     // the wavefront reaches them)
-    const int col = t.p0 + t.lane;
-    const bool in_split = t.lane < a.split_pages && col < a.max_pages;
-    my_page = in_split ? a.block_table[(int64_t)t.b * a.max_pages + col] : 0;
+    auto load_pages = [&] {
+        const int col = t.p0 + t.lane;
+        const bool in_split = t.lane < a.split_pages && col < a.max_pages;
+        my_page = in_split ? a.block_table[(int64_t)t.b * a.max_pages + col] : 0;
+    };
+    if (s >= 0)
+        load_pages();
     int L = __builtin_amdgcn_readfirstlane(a.seq_lens[t.b]);  // uniform: scalar
     const int cap = a.max_pages * kPageSize;
     if (L > cap) {
-        if (CHECKED && t.lane == 0 && t.s == 0 && t.kvh == 0)
+        if (CHECKED && t.lane == 0 && t.owner && t.kvh == 0)
             atomicOr(a.dev_error, RL_DA_DEVERR_LENGTH_TOO_LONG);
         L = cap;
     }
     t.seq_len = L;
     t.npages = L > 0 ? (L + kPageSize - 1) / kPageSize : 0;
     t.nsplit = (t.npages + a.split_pages - 1) / a.split_pages;
+    if (s < 0) {
+        if (t.nsplit == 0)
+            return false;
+        t.s = t.nsplit - 1;
+        t.p0 = t.s * a.split_pages;
+        load_pages();
+    }
     const int p1 = min(t.p0 + a.split_pages, t.npages);
     if (t.p0 >= p1)
         return false;
@@ -694,7 +953,7 @@ __device__ __forceinline__ bool begin_task_hp(const SplitArgs& a, WaveTask& t, i
 
 // A work-group of up to eight wavefronts fills two waves per SIMD, so the
 // kernel may use the two-wave register budget.
-template <int G, bool CHECKED, typename KV>
+template <int G, bool CHECKED, typename KV, bool PERSISTENT>
 __global__ __launch_bounds__(kWave * kMaxHeadsPerUnit)
 __attribute__((amdgpu_waves_per_eu(2))) void split_mfma_hp(SplitArgs a)
 {
@@ -705,50 +964,59 @@ __attribute__((amdgpu_waves_per_eu(2))) void split_mfma_hp(SplitArgs a)
     __shared__ __attribute__((aligned(16))) float lds_p_all[kMaxHeadsPerUnit][kPageSize * kH];
     __shared__ __attribute__((aligned(16))) float lds_alpha_all[kMaxHeadsPerUnit][kH];
 
-    WaveTask t;
-    int32_t my_page;
-    if (!begin_task_hp<CHECKED>(a, t, my_page)) {
-        // an empty sequence produces zeros, written by its last-level unit
-        if (t.npages == 0 && t.last_level)
-            for (int e = t.lane; e < G * (kHeadDim / 8); e += kWave) {
-                const int g = e / (kHeadDim / 8), chunk = e % (kHeadDim / 8);
-                *reinterpret_cast<uint4*>(
-                    a.out + ((int64_t)t.b * a.num_q_heads + t.kvh * G + g) * kHeadDim +
-                    chunk * 8) = make_uint4(0, 0, 0, 0);
-            }
-        return;
-    }
-    float acc[G][8], m[kE], l_row[kE];
-    int head[kE];
-    attend_pages<G, CHECKED, KV, 1>(a, t, my_page, lds_p_all[t.wave], lds_alpha_all[t.wave],
-                                    acc, m, l_row, head);
-    // Lane 16kg + c writes dims 8c..8c+7 of the heads its lane group holds.
-    const int c = t.lane & 15;
-#pragma unroll
-    for (int e = 0; e < kE; ++e) {
-#pragma unroll
-        for (int g = 0; g < G; ++g) {
-            if (g != head[e])
-                continue;
-            const int64_t row = (int64_t)t.b * a.num_q_heads + t.kvh * G + g;
-            if (t.nsplit == 1) {
-                const float inv = 1.0f / l_row[e];
-                uint4 o;
-                o.x = f32_to_bf16(acc[g][0] * inv) | (f32_to_bf16(acc[g][1] * inv) << 16);
-                o.y = f32_to_bf16(acc[g][2] * inv) | (f32_to_bf16(acc[g][3] * inv) << 16);
-                o.z = f32_to_bf16(acc[g][4] * inv) | (f32_to_bf16(acc[g][5] * inv) << 16);
-                o.w = f32_to_bf16(acc[g][6] * inv) | (f32_to_bf16(acc[g][7] * inv) << 16);
-                *reinterpret_cast<uint4*>(a.out + row * kHeadDim + 8 * c) = o;
-            } else {
-                const int64_t part = row * a.num_splits + t.s;
-                float4* dst = reinterpret_cast<float4*>(a.ws_acc + part * kHeadDim + 8 * c);
-                dst[0] = make_float4(acc[g][0], acc[g][1], acc[g][2], acc[g][3]);
-                dst[1] = make_float4(acc[g][4], acc[g][5], acc[g][6], acc[g][7]);
-                if (c == 0)
-                    *reinterpret_cast<float2*>(a.ws_ml + part * 2) = make_float2(m[e], l_row[e]);
+    extern __shared__ int plan[];
+
+    auto unit = [&](const SplitArgs& a, int b, int group, int s, bool owner) {
+        WaveTask t;
+        int32_t my_page;
+        if (!begin_unit_hp<CHECKED>(a, t, my_page, b, group, s, owner)) {
+            // an empty sequence produces zeros, written by its owner unit
+            if (t.npages == 0 && t.owner)
+                for (int e = t.lane; e < G * (kHeadDim / 8); e += kWave) {
+                    const int g = e / (kHeadDim / 8), chunk = e % (kHeadDim / 8);
+                    *reinterpret_cast<uint4*>(
+                        a.out + ((int64_t)t.b * a.num_q_heads + t.kvh * G + g) * kHeadDim +
+                        chunk * 8) = make_uint4(0, 0, 0, 0);
+                }
+            return;
+        }
+        float acc[G][8], m[kE], l_row[kE];
+        int head[kE];
+        attend_pages<G, CHECKED, KV, 1>(a, t, my_page, lds_p_all[t.wave], lds_alpha_all[t.wave],
+                                        acc, m, l_row, head);
+        // Lane 16kg + c writes dims 8c..8c+7 of the heads its lane group holds.
+        const int c = t.lane & 15;
+    #pragma unroll
+        for (int e = 0; e < kE; ++e) {
+    #pragma unroll
+            for (int g = 0; g < G; ++g) {
+                if (g != head[e])
+                    continue;
+                const int64_t row = (int64_t)t.b * a.num_q_heads + t.kvh * G + g;
+                if (t.nsplit == 1) {
+                    const float inv = 1.0f / l_row[e];
+                    uint4 o;
+                    o.x = f32_to_bf16(acc[g][0] * inv) | (f32_to_bf16(acc[g][1] * inv) << 16);
+                    o.y = f32_to_bf16(acc[g][2] * inv) | (f32_to_bf16(acc[g][3] * inv) << 16);
+                    o.z = f32_to_bf16(acc[g][4] * inv) | (f32_to_bf16(acc[g][5] * inv) << 16);
+                    o.w = f32_to_bf16(acc[g][6] * inv) | (f32_to_bf16(acc[g][7] * inv) << 16);
+                    *reinterpret_cast<uint4*>(a.out + row * kHeadDim + 8 * c) = o;
+                } else {
+                    const int64_t part = row * a.num_splits + t.s;
+                    float4* dst = reinterpret_cast<float4*>(a.ws_acc + part * kHeadDim + 8 * c);
+                    dst[0] = make_float4(acc[g][0], acc[g][1], acc[g][2], acc[g][3]);
+                    dst[1] = make_float4(acc[g][4], acc[g][5], acc[g][6], acc[g][7]);
+                    if (c == 0)
+                        *reinterpret_cast<float2*>(a.ws_ml + part * 2) = make_float2(m[e], l_row[e]);
+                }
             }
         }
-    }
+    };
+    const int groups = a.num_kv_heads / a.heads_per_unit;
+    if (PERSISTENT)
+        run_persistent(a, groups, plan, unit);
+    else  // one split per sequence: unit (b, head group) = blockIdx.x
+        unit(a, blockIdx.x / groups, blockIdx.x % groups, 0, true);
 }
 
 // ------------------------------------------- split kernel, VALU dot2 QK ---
@@ -758,137 +1026,144 @@ __attribute__((amdgpu_waves_per_eu(2))) void split_mfma_hp(SplitArgs a)
 // lanes of the row with DPP; each row r keeps its own online softmax over its
 // tokens and the four rows are merged with the log-sum-exp rule at the end.
 
-template <int G, bool CHECKED, bool ORDERED>
+template <int G, bool CHECKED, bool PERSISTENT>
 __global__ __launch_bounds__(kWave * kUnitWaves) void split_valu_bf16(SplitArgs a)
 {
     __shared__ __attribute__((aligned(16))) UnitShared<G> sh;
+    extern __shared__ int plan[];
 
-    WaveTask t;
-    int32_t my_page;
-    if (!begin_task<CHECKED, ORDERED>(a, t, my_page)) {
-        write_zero_rows<G>(a, t);
-        return;
-    }
+    auto unit = [&](const SplitArgs& a, int b, int kvh, int s, bool owner) {
+        WaveTask t;
+        int32_t my_page;
+        if (!begin_unit<CHECKED>(a, t, my_page, b, kvh, s, owner)) {
+            write_zero_rows<G>(a, t);
+            return;
+        }
 
-    const int lane = t.lane;
-    const int r = lane >> 4, c = lane & 15;
-    const int h0 = t.kvh * G;
+        const int lane = t.lane;
+        const int r = lane >> 4, c = lane & 15;
+        const int h0 = t.kvh * G;
 
-    uint4 qv[G];
-#pragma unroll
-    for (int g = 0; g < G; ++g)
-        qv[g] = *reinterpret_cast<const uint4*>(
-            a.q + ((int64_t)t.b * a.num_q_heads + h0 + g) * kHeadDim + 8 * c);
-
-    float m[G], l[G], acc[G][8];
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-        m[g] = -INFINITY;
-        l[g] = 0.0f;
-#pragma unroll
-        for (int d = 0; d < 8; ++d)
-            acc[g][d] = 0.0f;
-    }
-
-    const int off = r * a.row_bytes + 16 * c;
-    const int step = 4 * a.row_bytes;
-    auto issue = [&](KvBf16::Buf& buf, int i) {
-        const int64_t page = __builtin_amdgcn_readlane(my_page, i);
-        const uint8_t* ks = slab_base(a, a.k_pool, page, t.kvh);
-        const uint8_t* vs = slab_base(a, a.v_pool, page, t.kvh);
-#pragma unroll
-        for (int k = 0; k < 4; ++k)
-            buf.k[k] = load_stream16(ks + step * k + off);
-#pragma unroll
-        for (int k = 0; k < 4; ++k)
-            buf.v[k] = load_stream16(vs + step * k + off);
-    };
-
-    auto consume = [&](KvBf16::Buf& buf, int i) {
-        uint4 (&kbuf)[4] = buf.k;
-        uint4 (&vbuf)[4] = buf.v;
-        const int valid = t.seq_len - task_page(t, i) * kPageSize;
-        float sc[G][4];
-#pragma unroll
+        uint4 qv[G];
+    #pragma unroll
         for (int g = 0; g < G; ++g)
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                float x = dot2_bf16(qv[g].x, kbuf[k].x, 0.0f);
-                x = dot2_bf16(qv[g].y, kbuf[k].y, x);
-                x = dot2_bf16(qv[g].z, kbuf[k].z, x);
-                x = dot2_bf16(qv[g].w, kbuf[k].w, x);
-                x = row16_sum(x) * a.scale_log2;
-                sc[g][k] = (4 * k + r < valid) ? x : -INFINITY;
-            }
+            qv[g] = *reinterpret_cast<const uint4*>(
+                a.q + ((int64_t)t.b * a.num_q_heads + h0 + g) * kHeadDim + 8 * c);
 
-        float p[G][4];
-#pragma unroll
+        float m[G], l[G], acc[G][8];
+    #pragma unroll
         for (int g = 0; g < G; ++g) {
-            const float mx = fmaxf(fmaxf(sc[g][0], sc[g][1]), fmaxf(sc[g][2], sc[g][3]));
-            const float m_new = fmaxf(m[g], mx);
-            // A row may see no valid token of a short last page: keep it empty.
-            const bool empty = m_new == -INFINITY;
-            const float alpha = empty ? 1.0f : exp2_fast(m[g] - m_new);
-            float sum = 0.0f;
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                p[g][k] = empty ? 0.0f : exp2_fast(sc[g][k] - m_new);
-                sum += p[g][k];
-            }
-            l[g] = l[g] * alpha + sum;
-            m[g] = m_new;
-#pragma unroll
+            m[g] = -INFINITY;
+            l[g] = 0.0f;
+    #pragma unroll
             for (int d = 0; d < 8; ++d)
-                acc[g][d] *= alpha;
+                acc[g][d] = 0.0f;
         }
 
-        if (valid < kPageSize) {
-#pragma unroll
+        const int off = r * a.row_bytes + 16 * c;
+        const int step = 4 * a.row_bytes;
+        auto issue = [&](KvBf16::Buf& buf, int i) {
+            const int64_t page = __builtin_amdgcn_readlane(my_page, i);
+            const uint8_t* ks = slab_base(a, a.k_pool, page, t.kvh);
+            const uint8_t* vs = slab_base(a, a.v_pool, page, t.kvh);
+    #pragma unroll
             for (int k = 0; k < 4; ++k)
-                if (4 * k + r >= valid)
-                    vbuf[k] = make_uint4(0, 0, 0, 0);
-        }
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            float v[8];
-            unpack8(vbuf[k], v);
-#pragma unroll
+                buf.k[k] = load_stream16(ks + step * k + off);
+    #pragma unroll
+            for (int k = 0; k < 4; ++k)
+                buf.v[k] = load_stream16(vs + step * k + off);
+        };
+
+        auto consume = [&](KvBf16::Buf& buf, int i) {
+            uint4 (&kbuf)[4] = buf.k;
+            uint4 (&vbuf)[4] = buf.v;
+            const int valid = t.seq_len - task_page(t, i) * kPageSize;
+            float sc[G][4];
+    #pragma unroll
             for (int g = 0; g < G; ++g)
-#pragma unroll
+    #pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    float x = dot2_bf16(qv[g].x, kbuf[k].x, 0.0f);
+                    x = dot2_bf16(qv[g].y, kbuf[k].y, x);
+                    x = dot2_bf16(qv[g].z, kbuf[k].z, x);
+                    x = dot2_bf16(qv[g].w, kbuf[k].w, x);
+                    x = row16_sum(x) * a.scale_log2;
+                    sc[g][k] = (4 * k + r < valid) ? x : -INFINITY;
+                }
+
+            float p[G][4];
+    #pragma unroll
+            for (int g = 0; g < G; ++g) {
+                const float mx = fmaxf(fmaxf(sc[g][0], sc[g][1]), fmaxf(sc[g][2], sc[g][3]));
+                const float m_new = fmaxf(m[g], mx);
+                // A row may see no valid token of a short last page: keep it empty.
+                const bool empty = m_new == -INFINITY;
+                const float alpha = empty ? 1.0f : exp2_fast(m[g] - m_new);
+                float sum = 0.0f;
+    #pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    p[g][k] = empty ? 0.0f : exp2_fast(sc[g][k] - m_new);
+                    sum += p[g][k];
+                }
+                l[g] = l[g] * alpha + sum;
+                m[g] = m_new;
+    #pragma unroll
                 for (int d = 0; d < 8; ++d)
-                    acc[g][d] = fmaf(p[g][k], v[d], acc[g][d]);
+                    acc[g][d] *= alpha;
+            }
+
+            if (valid < kPageSize) {
+    #pragma unroll
+                for (int k = 0; k < 4; ++k)
+                    if (4 * k + r >= valid)
+                        vbuf[k] = make_uint4(0, 0, 0, 0);
+            }
+    #pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                float v[8];
+                unpack8(vbuf[k], v);
+    #pragma unroll
+                for (int g = 0; g < G; ++g)
+    #pragma unroll
+                    for (int d = 0; d < 8; ++d)
+                        acc[g][d] = fmaf(p[g][k], v[d], acc[g][d]);
+            }
+        };
+
+        KvBf16::Buf buf_a, buf_b;
+        stream_pages(t.count, buf_a, buf_b, issue, consume);
+
+        // Merge the four rows: rescale each to the common max, then add.  A
+        // wavefront without pages keeps m = -inf, l = 0, acc = 0.
+    #pragma unroll
+        for (int g = 0; g < G; ++g) {
+            float M = fmaxf(m[g], __shfl_xor(m[g], 16));
+            M = fmaxf(M, __shfl_xor(M, 32));
+            const float w = (m[g] == -INFINITY) ? 0.0f : exp2_fast(m[g] - M);
+            float lw = l[g] * w;
+            lw += __shfl_xor(lw, 16);
+            lw += __shfl_xor(lw, 32);
+            l[g] = lw;
+            m[g] = M;
+    #pragma unroll
+            for (int d = 0; d < 8; ++d) {
+                float v = acc[g][d] * w;
+                v += __shfl_xor(v, 16);
+                v += __shfl_xor(v, 32);
+                acc[g][d] = v;
+            }
         }
+    #pragma unroll
+        for (int g = 0; g < G; ++g)
+            if ((g & 3) == r)
+                stash_state<G>(sh, t.wave, g, c, acc[g], m[g], l[g]);
+        __syncthreads();
+        merge_unit<G>(a, t, sh);
     };
-
-    KvBf16::Buf buf_a, buf_b;
-    stream_pages(t.count, buf_a, buf_b, issue, consume);
-
-    // Merge the four rows: rescale each to the common max, then add.  A
-    // wavefront without pages keeps m = -inf, l = 0, acc = 0.
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-        float M = fmaxf(m[g], __shfl_xor(m[g], 16));
-        M = fmaxf(M, __shfl_xor(M, 32));
-        const float w = (m[g] == -INFINITY) ? 0.0f : exp2_fast(m[g] - M);
-        float lw = l[g] * w;
-        lw += __shfl_xor(lw, 16);
-        lw += __shfl_xor(lw, 32);
-        l[g] = lw;
-        m[g] = M;
-#pragma unroll
-        for (int d = 0; d < 8; ++d) {
-            float v = acc[g][d] * w;
-            v += __shfl_xor(v, 16);
-            v += __shfl_xor(v, 32);
-            acc[g][d] = v;
-        }
-    }
-#pragma unroll
-    for (int g = 0; g < G; ++g)
-        if ((g & 3) == r)
-            stash_state<G>(sh, t.wave, g, c, acc[g], m[g], l[g]);
-    __syncthreads();
-    merge_unit<G>(a, t, sh);
+    if (PERSISTENT)
+        run_persistent(a, a.num_kv_heads, plan, unit);
+    else  // one split per sequence: unit (b, kv head) = blockIdx.x
+        unit(a, blockIdx.x / a.num_kv_heads, blockIdx.x % a.num_kv_heads, 0, true);
 }
 
 // -------------------------------------------------------- merge kernel ---
@@ -961,39 +1236,41 @@ __global__ __launch_bounds__(kWave * kMergeWaves) void merge_splits(MergeArgs a)
 
 typedef void (*SplitKernel)(SplitArgs);
 
-// ORDERED: the split-level unit order for runs with more than one split
-// (four-wavefront units only).
-template <int G, bool CHECKED, bool ORDERED>
+// PERSISTENT: the kernel for runs with more than one split (persistent
+// work-groups taking units from the queue).
+template <int G, bool CHECKED, bool PERSISTENT>
 SplitKernel pick(bool fp8, bool mfma, bool hp)
 {
     if (hp)
-        return fp8 ? split_mfma_hp<G, CHECKED, KvFp8> : split_mfma_hp<G, CHECKED, KvBf16>;
+        return fp8 ? split_mfma_hp<G, CHECKED, KvFp8, PERSISTENT>
+                   : split_mfma_hp<G, CHECKED, KvBf16, PERSISTENT>;
     if (fp8)
-        return split_mfma<G, CHECKED, KvFp8, ORDERED>;  // fp8 pools: MFMA score tile only
+        return split_mfma<G, CHECKED, KvFp8, PERSISTENT>;  // fp8 pools: MFMA score tile only
     if (mfma)
-        return split_mfma<G, CHECKED, KvBf16, ORDERED>;
-    return split_valu_bf16<G, CHECKED, ORDERED>;
+        return split_mfma<G, CHECKED, KvBf16, PERSISTENT>;
+    return split_valu_bf16<G, CHECKED, PERSISTENT>;
 }
 
-template <bool CHECKED, bool ORDERED>
+template <bool CHECKED, bool PERSISTENT>
 SplitKernel select_for_group(int G, bool fp8, bool mfma, bool hp)
 {
     switch (G) {
-    case 1: return pick<1, CHECKED, ORDERED>(fp8, mfma, hp);
-    case 2: return pick<2, CHECKED, ORDERED>(fp8, mfma, hp);
-    case 4: return pick<4, CHECKED, ORDERED>(fp8, mfma, hp);
-    case 8: return pick<8, CHECKED, ORDERED>(fp8, mfma, hp);
+    case 1: return pick<1, CHECKED, PERSISTENT>(fp8, mfma, hp);
+    case 2: return pick<2, CHECKED, PERSISTENT>(fp8, mfma, hp);
+    case 4: return pick<4, CHECKED, PERSISTENT>(fp8, mfma, hp);
+    case 8: return pick<8, CHECKED, PERSISTENT>(fp8, mfma, hp);
     default: return nullptr;
     }
 }
 
-SplitKernel select_split_kernel(int G, bool checked, bool fp8, bool mfma, bool hp, bool ordered)
+SplitKernel select_split_kernel(int G, bool checked, bool fp8, bool mfma, bool hp,
+                               bool persistent)
 {
     if (checked)
-        return ordered ? select_for_group<true, true>(G, fp8, mfma, hp)
-                       : select_for_group<true, false>(G, fp8, mfma, hp);
-    return ordered ? select_for_group<false, true>(G, fp8, mfma, hp)
-                   : select_for_group<false, false>(G, fp8, mfma, hp);
+        return persistent ? select_for_group<true, true>(G, fp8, mfma, hp)
+                          : select_for_group<true, false>(G, fp8, mfma, hp);
+    return persistent ? select_for_group<false, true>(G, fp8, mfma, hp)
+                      : select_for_group<false, false>(G, fp8, mfma, hp);
 }
 
 // kv heads per head-parallel work-group: the largest divisor of Hkv up to 8
@@ -1028,13 +1305,16 @@ struct rl_decode_attn {
     bool use_mfma;
     bool head_parallel;
     int heads_per_unit;
-    SplitKernel split_kernel;          // runs with one split per sequence
-    SplitKernel split_kernel_ordered;  // runs with more
+    SplitKernel split_kernel;             // runs with one split per sequence
+    SplitKernel split_kernel_persistent;  // runs with more
+    int persistent_grid;                  // persistent work-groups resident at once
+    int static_slots;                     // one-unit work-groups resident at once
     void* workspace;
     size_t workspace_bytes;
     float* ws_acc;
     float* ws_ml;
     int32_t* dev_error;
+    int32_t* queue;  // persistent runs: next unit, finished work-groups
     hipEvent_t ev_split_begin;
     hipEvent_t ev_split_end;
 };
@@ -1091,7 +1371,8 @@ rl_da_status check_config(const rl_da_config* cfg, int* split_tokens, int* split
 }
 
 // Workspace: per-split partial accumulators and (m, l) pairs, then one
-// 256-byte block for the device error word.
+// 256-byte block for the device error word (offset 0) and the persistent
+// launch's unit queue (offset 128).
 size_t partials_bytes(const rl_da_config* cfg, int max_splits)
 {
     const size_t rows = (size_t)cfg->max_batch * (size_t)cfg->num_q_heads * (size_t)max_splits;
@@ -1153,13 +1434,37 @@ rl_da_status rl_decode_attn_create(const rl_da_config* cfg, rl_decode_attn** out
     h->use_mfma = (cfg->flags & RL_DA_SCORES_ON_VALU) == 0;
     h->head_parallel = uses_head_parallel(cfg);
     h->heads_per_unit = h->head_parallel ? heads_per_unit_for(cfg->num_kv_heads) : 1;
-    for (int ordered = 0; ordered < 2; ++ordered)
-        (ordered ? h->split_kernel_ordered : h->split_kernel) = select_split_kernel(
+    for (int persistent = 0; persistent < 2; ++persistent)
+        (persistent ? h->split_kernel_persistent : h->split_kernel) = select_split_kernel(
             G, (cfg->flags & RL_DA_CHECKED) != 0, cfg->kv_dtype == RL_DA_KV_FP8_E4M3, h->use_mfma,
-            h->head_parallel, ordered != 0);
+            h->head_parallel, persistent != 0);
     if (hipGetDevice(&h->device) != hipSuccess) {
         free(h);
         return RL_DA_ERR_HIP;
+    }
+    // One persistent work-group per slot that can be resident with the
+    // largest plan this handle can need; and how many one-unit work-groups
+    // the static grid keeps resident.
+    {
+        const int threads = h->head_parallel ? kWave * h->heads_per_unit : kWave * kUnitWaves;
+        const int plan_batch = cfg->max_batch < kMaxPlanBatch ? cfg->max_batch : kMaxPlanBatch;
+        const size_t lds = (size_t)plan_ints(plan_batch) * sizeof(int);
+        int per_cu = 0, static_per_cu = 0, cus = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                &per_cu, reinterpret_cast<const void*>(h->split_kernel_persistent), threads,
+                lds) != hipSuccess ||
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                &static_per_cu, reinterpret_cast<const void*>(h->split_kernel), threads, 0) !=
+                hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device) !=
+                hipSuccess ||
+            per_cu < 1 || static_per_cu < 1 || cus < 1) {
+            (void)hipGetLastError();
+            free(h);
+            return RL_DA_ERR_HIP;
+        }
+        h->persistent_grid = per_cu * cus;
+        h->static_slots = static_per_cu * cus;
     }
     h->workspace_bytes = workspace_bytes_for(cfg, ms);
     if (hipMalloc(&h->workspace, h->workspace_bytes) != hipSuccess) {
@@ -1171,7 +1476,8 @@ rl_da_status rl_decode_attn_create(const rl_da_config* cfg, rl_decode_attn** out
     h->ws_acc = (float*)h->workspace;
     h->ws_ml = h->ws_acc + rows * kHeadDim;
     h->dev_error = (int32_t*)((char*)h->workspace + h->workspace_bytes - 256);
-    if (hipMemset(h->dev_error, 0, sizeof(int32_t)) != hipSuccess) {
+    h->queue = h->dev_error + 32;
+    if (hipMemset(h->dev_error, 0, 256) != hipSuccess) {
         (void)hipFree(h->workspace);
         free(h);
         return RL_DA_ERR_HIP;
@@ -1229,8 +1535,17 @@ rl_da_status rl_decode_attn_run(rl_decode_attn* h, const void* q, const void* k_
 
     const int num_splits = (max_pages + h->split_pages - 1) / h->split_pages;
     const int64_t units = (int64_t)batch * (cfg.num_kv_heads / h->heads_per_unit) * num_splits;
-    if (units > INT32_MAX)
+    if (units + h->persistent_grid > INT32_MAX)
         return RL_DA_ERR_UNSUPPORTED;
+    // One split: the one-unit kernel, one work-group per unit.  Several
+    // splits: the multi-split kernel -- one work-group per unit when the chip
+    // holds every unit at once (the order cannot matter then), else
+    // persistent work-groups taking units longest first (in sequence order
+    // when the batch is too large for the plan).
+    const bool persistent = num_splits > 1;
+    const Schedule schedule = units <= h->static_slots ? kOnePerGroup
+                              : batch <= kMaxPlanBatch ? kQueuePlanned
+                                                       : kQueueInOrder;
 
     SplitArgs sa;
     sa.q = (const uint16_t*)q;
@@ -1255,16 +1570,27 @@ rl_da_status rl_decode_attn_run(rl_decode_attn* h, const void* q, const void* k_
     sa.max_pages = max_pages;
     sa.split_pages = h->split_pages;
     sa.num_splits = num_splits;
-    sa.units_per_level = (int32_t)(units / num_splits);
     sa.heads_per_unit = h->heads_per_unit;
+    sa.batch = batch;
+    sa.schedule = schedule;
+    sa.queue = h->queue;
     sa.scale_log2 = scale * kLog2e;
 
     hipStream_t st = (hipStream_t)stream;
     if (h->ev_split_begin != nullptr && hipEventRecord(h->ev_split_begin, st) != hipSuccess)
         return RL_DA_ERR_HIP;
     const int threads = h->head_parallel ? kWave * h->heads_per_unit : kWave * kUnitWaves;
-    hipLaunchKernelGGL(num_splits > 1 ? h->split_kernel_ordered : h->split_kernel,
-                       dim3((unsigned)units), dim3(threads), 0, st, sa);
+    if (persistent) {
+        const int64_t grid = schedule == kOnePerGroup || units <= h->persistent_grid
+                                 ? units
+                                 : h->persistent_grid;
+        const size_t lds =
+            schedule == kQueuePlanned ? (size_t)plan_ints(batch) * sizeof(int) : 0;
+        hipLaunchKernelGGL(h->split_kernel_persistent, dim3((unsigned)grid), dim3(threads), lds,
+                           st, sa);
+    } else {
+        hipLaunchKernelGGL(h->split_kernel, dim3((unsigned)units), dim3(threads), 0, st, sa);
+    }
     if (hipGetLastError() != hipSuccess)
         return RL_DA_ERR_HIP;
     if (h->ev_split_end != nullptr && hipEventRecord(h->ev_split_end, st) != hipSuccess)
