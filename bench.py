@@ -562,6 +562,7 @@ def main():
     attn = binding.DecodeAttention.for_problem(base, flags=flags,
                                                split_tokens=args.split_tokens)
     split_tokens, num_splits = attn.split_info(base.max_pages)
+    unit_heads = attn.unit_heads()
     stream = torch.cuda.current_stream()
 
     nev = args.steps
@@ -622,8 +623,8 @@ def main():
             "page_size": base.page_size, "seq_len_mean": float(base.lengths().mean()),
             "split_tokens": split_tokens, "num_splits": num_splits,
             "scores": args.scores, "replicas": len(replicas), "layout": base.layout,
-            "units": "per-head" if (args.per_head_units or base.layout == "hnd")
-                     else "head-parallel",
+            "units": "per-head" if unit_heads == 1
+                     else "head-parallel (%d kv heads)" % unit_heads,
         },
         "query_tokens_per_s": round(base.batch / (ms_per_step / 1e3), 1),
         "kv_bytes_per_step": kv_bytes,

@@ -90,13 +90,16 @@ typedef enum { RL_DA_LAYOUT_HND = 0, RL_DA_LAYOUT_NHD = 1 } rl_da_layout;
  * ALUs instead of packing the query group into an MFMA tile (same results up
  * to fp32 rounding; kept to measure one path against the other). */
 #define RL_DA_SCORES_ON_VALU 0x2u
-/* create() flag for token-major (RL_DA_LAYOUT_NHD) pools.  By default such a
- * handle runs one work-group per (sequence, split, group of up to 8 kv
- * heads), one wavefront per kv head, so the group reads each page's token
- * rows together; with this flag it runs the head-major pools' units instead
- * (four wavefronts per (sequence, kv head, split) sharing its pages), which
- * balance better when lengths have a long tail.  No effect on head-major
- * pools, with RL_DA_SCORES_ON_VALU, or with one kv head per group. */
+/* create() flag for token-major (RL_DA_LAYOUT_NHD) pools.  Such a handle
+ * runs head-parallel units -- one work-group per (sequence, split, group of
+ * up to 8 kv heads), one wavefront per kv head, so the group reads each
+ * page's token rows together -- when its full-capacity batch cut into
+ * four-wavefront units would fit on the device at once (768 work-groups);
+ * a larger handle runs the head-major pools' units (four wavefronts per
+ * (sequence, kv head, split)), which the persistent longest-first schedule
+ * balances.  This flag always selects the four-wavefront units.  No effect
+ * on head-major pools, with RL_DA_SCORES_ON_VALU, or with one kv head per
+ * group (rl_decode_attn_unit_heads reports the choice). */
 #define RL_DA_PER_HEAD_UNITS 0x4u
 
 /* Device error word bits reported by rl_decode_attn_check_error(). */
@@ -166,6 +169,11 @@ rl_da_status rl_decode_attn_check_error(rl_decode_attn* h, int32_t* device_error
  * block table of max_pages columns is divided into. */
 rl_da_status rl_decode_attn_split_info(const rl_decode_attn* h, int32_t max_pages,
                                        int32_t* split_tokens, int32_t* num_splits);
+
+/* Work-unit family of a handle (host only): *kv_heads_per_unit = 1 for the
+ * four-wavefront units of one kv head, or the number of kv heads of a
+ * head-parallel unit (token-major pools). */
+rl_da_status rl_decode_attn_unit_heads(const rl_decode_attn* h, int32_t* kv_heads_per_unit);
 
 /*
  * Extend (prefill) attention: causal attention of several new tokens per

@@ -42,6 +42,7 @@ EXPORTED = [
     "rl_decode_attn_workspace_size",
     "rl_decode_attn_check_error",
     "rl_decode_attn_split_info",
+    "rl_decode_attn_unit_heads",
     "rl_extend_attn",
     "rl_kv_append",
     "rl_decode_attn_set_timing_events",
@@ -129,6 +130,8 @@ def load_library():
     lib.rl_decode_attn_check_error.restype = ctypes.c_int
     lib.rl_decode_attn_split_info.argtypes = [vp, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)]
     lib.rl_decode_attn_split_info.restype = ctypes.c_int
+    lib.rl_decode_attn_unit_heads.argtypes = [vp, ctypes.POINTER(i32)]
+    lib.rl_decode_attn_unit_heads.restype = ctypes.c_int
     lib.rl_extend_attn.argtypes = [vp, vp, i32, vp, vp, vp, vp, i64, vp, i32, vp, i32, i32, i32,
                                    i32, i32, i32, i32, ctypes.c_float, vp, vp]
     lib.rl_extend_attn.restype = ctypes.c_int
@@ -232,6 +235,12 @@ def rl_decode_attn_split_info(h, max_pages):
     rc = load_library().rl_decode_attn_split_info(h, int(max_pages), ctypes.byref(st),
                                                   ctypes.byref(ns))
     return rc, st.value, ns.value
+
+
+def rl_decode_attn_unit_heads(h):
+    v = ctypes.c_int32()
+    rc = load_library().rl_decode_attn_unit_heads(h, ctypes.byref(v))
+    return rc, v.value
 
 
 def rl_extend_attn(q, q_start, max_q_per_seq, k_pool, v_pool, k_scale, v_scale, num_pages,
@@ -433,6 +442,13 @@ class DecodeAttention:
         if rc != RL_DA_OK:
             raise RLDecodeAttnError(rc, "rl_decode_attn_split_info")
         return st, ns
+
+    def unit_heads(self):
+        """kv heads per work unit: 1 (four-wavefront units) or a head group."""
+        rc, v = rl_decode_attn_unit_heads(self.handle)
+        if rc != RL_DA_OK:
+            raise RLDecodeAttnError(rc, "rl_decode_attn_unit_heads")
+        return v
 
     def check_error(self):
         rc, v = rl_decode_attn_check_error(self.handle)

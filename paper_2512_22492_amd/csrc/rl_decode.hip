@@ -48,6 +48,10 @@ constexpr int kMaxSplitTokens = kWave * kUnitWaves * kPageSize;
 // every wavefront walks all pages of its split
 constexpr int kMaxHeadsPerUnit = 8;
 constexpr int kMaxSplitTokensHp = 4096;
+// Four-wavefront work-groups the chip holds at once with three per CU
+// (MI355X: 256 CUs); the unit-family choice for token-major pools compares
+// a handle's capacity with it.
+constexpr int64_t kResidentUnits = 256 * 3;
 // Launches with more than one split run persistent work-groups that take
 // units longest first from a plan built in LDS; batches above this size
 // take the units in sequence order instead (the plan would not fit).
@@ -1282,14 +1286,41 @@ int heads_per_unit_for(int num_kv_heads)
     return 1;
 }
 
+// The default split: the longest of kDefaultSplitTokens, half, ... (down to
+// kMinDefaultSplitTokens) that cuts a full-capacity batch into at least
+// kMinDefaultUnits work units of units_per_split per (sequence, split).  It
+// depends on the handle's capacity only, never on a run's batch.
+int default_split_tokens(const rl_da_config* cfg, int64_t units_per_split)
+{
+    int st = kDefaultSplitTokens;
+    while (st > kMinDefaultSplitTokens) {
+        const int64_t splits = ((int64_t)cfg->max_pages_per_seq * kPageSize + st - 1) / st;
+        if ((int64_t)cfg->max_batch * units_per_split * splits >= kMinDefaultUnits)
+            break;
+        st /= 2;
+    }
+    return st;
+}
+
 // Token-major pools with at least two kv heads per work-group take the
-// head-parallel units (MFMA scores only) unless the caller asks for the
-// four-wavefront units; everything else the four-wavefront units.
+// head-parallel units (MFMA scores only) when the handle's full-capacity
+// batch, cut into four-wavefront units, would fit on the chip at once
+// (kResidentUnits); a larger capacity takes the four-wavefront units, which
+// the persistent longest-first schedule balances (on lengths with a tail
+// that beats the head-parallel units by 8-15%; on uniform lengths the
+// head-parallel units stay ahead).  RL_DA_PER_HEAD_UNITS or
+// RL_DA_SCORES_ON_VALU always take the four-wavefront units, and so does
+// everything on head-major pools.
 bool uses_head_parallel(const rl_da_config* cfg)
 {
-    return cfg->layout == RL_DA_LAYOUT_NHD &&
-           (cfg->flags & (RL_DA_SCORES_ON_VALU | RL_DA_PER_HEAD_UNITS)) == 0 &&
-           heads_per_unit_for(cfg->num_kv_heads) >= 2;
+    if (cfg->layout != RL_DA_LAYOUT_NHD ||
+        (cfg->flags & (RL_DA_SCORES_ON_VALU | RL_DA_PER_HEAD_UNITS)) != 0 ||
+        heads_per_unit_for(cfg->num_kv_heads) < 2)
+        return false;
+    const int st = cfg->split_tokens != 0 ? cfg->split_tokens
+                                          : default_split_tokens(cfg, cfg->num_kv_heads);
+    const int64_t splits = ((int64_t)cfg->max_pages_per_seq * kPageSize + st - 1) / st;
+    return (int64_t)cfg->max_batch * cfg->num_kv_heads * splits <= kResidentUnits;
 }
 
 }  // namespace
@@ -1350,18 +1381,8 @@ rl_da_status check_config(const rl_da_config* cfg, int* split_tokens, int* split
     // work units per (sequence, split)
     const int64_t units_per_split =
         hp ? cfg->num_kv_heads / heads_per_unit_for(cfg->num_kv_heads) : cfg->num_kv_heads;
-    int st = cfg->split_tokens;
-    if (st == 0) {
-        // depends on the handle's capacity only, never on a run's batch
-        st = kDefaultSplitTokens;
-        while (st > kMinDefaultSplitTokens) {
-            const int64_t splits =
-                ((int64_t)cfg->max_pages_per_seq * kPageSize + st - 1) / st;
-            if ((int64_t)cfg->max_batch * units_per_split * splits >= kMinDefaultUnits)
-                break;
-            st /= 2;
-        }
-    }
+    const int st =
+        cfg->split_tokens != 0 ? cfg->split_tokens : default_split_tokens(cfg, units_per_split);
     if (st % kPageSize != 0 || st > (hp ? kMaxSplitTokensHp : kMaxSplitTokens))
         return RL_DA_ERR_UNSUPPORTED;
     *split_tokens = st;
@@ -1542,7 +1563,12 @@ rl_da_status rl_decode_attn_run(rl_decode_attn* h, const void* q, const void* k_
     // holds every unit at once (the order cannot matter then), else
     // persistent work-groups taking units longest first (in sequence order
     // when the batch is too large for the plan).
-    const bool persistent = num_splits > 1;
+    // (Four-wavefront units on token-major pools run persistent with one
+    // split too: their static grid balances badly there, 590 -> 463 us on the
+    // fp8 large batch; on head-major pools the static grid is as good.)
+    const bool persistent =
+        num_splits > 1 || (cfg.layout == RL_DA_LAYOUT_NHD && !h->head_parallel &&
+                           units > h->static_slots);
     const Schedule schedule = units <= h->static_slots ? kOnePerGroup
                               : batch <= kMaxPlanBatch ? kQueuePlanned
                                                        : kQueueInOrder;
@@ -1610,6 +1636,14 @@ rl_da_status rl_decode_attn_run(rl_decode_attn* h, const void* q, const void* k_
         if (hipGetLastError() != hipSuccess)
             return RL_DA_ERR_HIP;
     }
+    return RL_DA_OK;
+}
+
+rl_da_status rl_decode_attn_unit_heads(const rl_decode_attn* h, int32_t* kv_heads_per_unit)
+{
+    if (h == nullptr || kv_heads_per_unit == nullptr)
+        return RL_DA_ERR_INVALID_ARG;
+    *kv_heads_per_unit = h->head_parallel ? h->heads_per_unit : 1;
     return RL_DA_OK;
 }
 
