@@ -26,8 +26,10 @@ namespace {
 // product running over keys in the order (4g..4g+3, 16+4g..16+4g+3) for lane
 // group g, and V^T read from LDS in the same order.  Row max, rescale and sum
 // are therefore lane-local but for two shuffles per 64 keys.  P enters the
-// PV product as two bf16 terms (hi + lo), so the value sum keeps fp32-level
-// accuracy; l sums the same fp32 probabilities.
+// PV product rounded to bf16 (relative error at most 2^-8 per weight, as in
+// common flash-attention kernels; an earlier two-term hi + lo split kept
+// fp32-level accuracy at a third more MFMAs and conversion work); l sums the
+// unrounded fp32 probabilities.
 
 constexpr int kRowBlocks = 2;                      // 16-row blocks per wavefront
 constexpr int kTileRows = kUnitWaves * kRowBlocks * 16;
@@ -243,25 +245,49 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
         // position; rows past the tile's tokens score 0 and stay finite) and
         // O^T += V^T P^T: lane holds dims 16db + 4g4 + jj of row i16.
         const bool masked = j >= first_masked_stage;
-        // Scaled scores (log2 units; the mask after the scale, so that any
-        // scale, 0 or negative included, leaves masked keys at -inf) and
-        // their row max over the stage for both row blocks (lane-local over
-        // 16 keys, then the two other lane groups of the row).
+        // Row max of the scaled scores (log2 units) over the stage for both
+        // row blocks (lane-local over 16 keys, then the two other lane groups
+        // of the row).  With every page's multiplier positive (the usual
+        // case) the multiply folds into the exponent, p = 2^(raw * mult - m),
+        // and the max is each page's multiplier times its raw max; a zero or
+        // negative multiplier takes the general path -- scale, then mask, so
+        // that masked keys stay at -inf for any scale -- with mult 1.
+        bool positive = true;
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+            positive &= sl[kb] > 0.0f;
+        float mult[4];
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+            mult[kb] = positive ? sl[kb] : 1.0f;
         float sc[kRowBlocks][4][4], mx[kRowBlocks];
+        auto stage_max = [&](auto pre_scaled) {
 #pragma unroll
-        for (int rb = 0; rb < kRowBlocks; ++rb) {
-            mx[rb] = -INFINITY;
+            for (int rb = 0; rb < kRowBlocks; ++rb) {
+                mx[rb] = -INFINITY;
 #pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
+                for (int kb = 0; kb < 4; ++kb) {
+                    float pm = -INFINITY;
 #pragma unroll
-                for (int jj = 0; jj < 4; ++jj) {
-                    float x = sacc[rb][kb][jj] * sl[kb];
-                    if (masked)
-                        x = j * kStageKeys + 16 * kb + 4 * g4 + jj <= row_pos[rb] ? x : -INFINITY;
-                    sc[rb][kb][jj] = x;
-                    mx[rb] = fmaxf(mx[rb], x);
+                    for (int jj = 0; jj < 4; ++jj) {
+                        float x = sacc[rb][kb][jj];
+                        if (decltype(pre_scaled)::value)
+                            x *= sl[kb];
+                        if (masked)
+                            x = j * kStageKeys + 16 * kb + 4 * g4 + jj <= row_pos[rb] ? x
+                                                                                  : -INFINITY;
+                        sc[rb][kb][jj] = x;
+                        pm = fmaxf(pm, x);
+                    }
+                    // mult > 0 in the folded form: -inf stays -inf
+                    mx[rb] = fmaxf(mx[rb], decltype(pre_scaled)::value ? pm : pm * sl[kb]);
                 }
-        }
+            }
+        };
+        if (positive)
+            stage_max(std::false_type{});
+        else
+            stage_max(std::true_type{});
 #pragma unroll
         for (int rb = 0; rb < kRowBlocks; ++rb)
             mx[rb] = fmaxf(mx[rb], __shfl_xor(mx[rb], 16));
@@ -286,34 +312,29 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
                         o[rb][db][jj] *= alpha;
             }
         }
-        // Probabilities as P^T operands: [rb][key half][hi, lo] bf16 x 8.
-        uint4 pt[kRowBlocks][2][2];
+        // Probabilities as P^T operands: [rb][key half] bf16 x 8 (round to
+        // nearest even; the normaliser sums the unrounded values).
+        uint4 pt[kRowBlocks][2];
 #pragma unroll
         for (int rb = 0; rb < kRowBlocks; ++rb) {
-            uint32_t hi[4][2], lo[4][2];
+            uint32_t pk[4][2];
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
                 for (int jp = 0; jp < 2; ++jp) {
-                    float p0 = exp2_fast(sc[rb][kb][2 * jp] - m_run[rb]);
-                    float p1 = exp2_fast(sc[rb][kb][2 * jp + 1] - m_run[rb]);
+                    float p0 = exp2_fast(fmaf(sc[rb][kb][2 * jp], mult[kb], -m_run[rb]));
+                    float p1 = exp2_fast(fmaf(sc[rb][kb][2 * jp + 1], mult[kb], -m_run[rb]));
                     lsum[rb] += p0 + p1;
                     if (FP8) {
                         p0 *= vsc[kb];
                         p1 *= vsc[kb];
                     }
-                    const uint32_t h = pack_bf16x2(p0, p1);
-                    hi[kb][jp] = h;
-                    lo[kb][jp] = pack_bf16x2(p0 - __uint_as_float(h << 16),
-                                             p1 - __uint_as_float(h & 0xffff0000u));
+                    pk[kb][jp] = pack_bf16x2(p0, p1);
                 }
 #pragma unroll
-            for (int kh = 0; kh < 2; ++kh) {
-                pt[rb][kh][0] = make_uint4(hi[2 * kh][0], hi[2 * kh][1], hi[2 * kh + 1][0],
-                                           hi[2 * kh + 1][1]);
-                pt[rb][kh][1] = make_uint4(lo[2 * kh][0], lo[2 * kh][1], lo[2 * kh + 1][0],
-                                           lo[2 * kh + 1][1]);
-            }
+            for (int kh = 0; kh < 2; ++kh)
+                pt[rb][kh] = make_uint4(pk[2 * kh][0], pk[2 * kh][1], pk[2 * kh + 1][0],
+                                        pk[2 * kh + 1][1]);
         }
         // O^T += V^T P^T: lane holds dims 16db + 4g4 + jj of row i16.  The V^T
         // operand of the next (db, kh) is read before this one's MFMAs.
@@ -340,10 +361,7 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
 #pragma unroll
             for (int rb = 0; rb < kRowBlocks; ++rb) {
                 o[rb][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                    __builtin_bit_cast(bf16x8_t, vt), __builtin_bit_cast(bf16x8_t, pt[rb][kh][0]),
-                    o[rb][db], 0, 0, 0);
-                o[rb][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                    __builtin_bit_cast(bf16x8_t, vt), __builtin_bit_cast(bf16x8_t, pt[rb][kh][1]),
+                    __builtin_bit_cast(bf16x8_t, vt), __builtin_bit_cast(bf16x8_t, pt[rb][kh]),
                     o[rb][db], 0, 0, 0);
             }
         }

@@ -34,17 +34,17 @@ def run_extend(p, q, q_start, max_new):
 
 
 def p_split_bound(p):
-    """The PV MFMA takes each probability as two bf16 terms, so every weight
-    carries up to 2^-18 relative error and the normalisation up to another
-    2^-18: the output may move by 2^-17 * max|V| beyond the bf16 rounding
-    (V decoded with its slab scales for e4m3 pools)."""
+    """The PV MFMA takes each probability rounded to bf16 (relative error at
+    most 2^-8 per weight) while the normaliser sums the unrounded values: the
+    output may move by 2^-8 * max|V| beyond the bf16 output rounding (V
+    decoded with its slab scales for e4m3 pools)."""
     if p.kv_dtype == "bf16":
         vmax = float(p.v_pool.float().abs().max())
     else:
         codes = p.v_pool.view(torch.float8_e4m3fn).float().abs()
         dims = (2, 3) if p.layout == "hnd" else (1, 3)   # slot and dim axes
         vmax = float((codes.amax(dim=dims) * p.v_scale).max())
-    return 2.0 ** -17 * vmax
+    return 2.0 ** -8 * vmax
 
 
 def oracle_extend(p, q, q_start):

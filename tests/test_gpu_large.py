@@ -75,7 +75,8 @@ def test_extend_and_append_beyond_4gib(layout):
                                   q_start.cpu().numpy(), h["k_pool"], h["v_pool"],
                                   h["block_table"], h["seq_lens"], num_kv_heads=8,
                                   scale=p.scale, layout=layout)
-    extra = 2.0 ** -17 * float(p.v_pool.float().abs().max())
+    # the P.V product takes P rounded to bf16: 2^-8 max|V| on top of one ulp
+    extra = 2.0 ** -8 * float(p.v_pool.float().abs().max())
     print(check_close(bf16_to_f64(out), ref, "extend > 4 GiB " + layout, extra_abs=extra))
 
 
