@@ -134,12 +134,19 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
     const int64_t st_off = (int64_t)kvh * a.head_bytes + kElt * (16 * st_c);
     const int npages = (L + kPageSize - 1) / kPageSize;
     uint4 kr[2][2], vr[2][2];  // [key of the pair][half of the 16 dims] (bf16)
-    auto fetch = [&](int stage) {
+    // The block-table entry of the thread's key pair (both keys share a
+    // page) is read one stage ahead, so a stage's K/V loads do not wait on
+    // a table load.
+    auto stage_page = [&](int stage) {
+        const int key = stage * kStageKeys + 2 * st_kp;
+        return key < L ? bt[key / kPageSize] : 0;
+    };
+    auto fetch = [&](int stage, int page) {
 #pragma unroll
         for (int e = 0; e < 2; ++e) {
             const int key = stage * kStageKeys + 2 * st_kp + e;
             if (key < L) {  // pages past the sequence are never read
-                const int64_t off = bt[key / kPageSize] * a.page_bytes + st_off +
+                const int64_t off = (int64_t)page * a.page_bytes + st_off +
                                     (int64_t)(key % kPageSize) * a.row_bytes;
                 kr[e][0] = load_stream16(a.k_pool + off);
                 vr[e][0] = load_stream16(a.v_pool + off);
@@ -193,12 +200,15 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
         }
     };
 
-    fetch(0);
+    fetch(0, stage_page(0));
+    int next_page = stage_page(1);
     for (int j = 0; j < nstages; ++j) {
         const int buf = j & 1;
         stash(buf);
-        if (j + 1 < nstages)
-            fetch(j + 1);
+        if (j + 1 < nstages) {
+            fetch(j + 1, next_page);
+            next_page = stage_page(j + 2);
+        }
         __syncthreads();
 
         // Score multiplier (scale * log2 e, times k_scale) and value scale
