@@ -43,19 +43,48 @@ def short_lengths(n, seed, hi=300):
     return [int(x) for x in L]
 
 
+@pytest.mark.parametrize("flags", [0, B.RL_DA_CHECKED])
 @pytest.mark.parametrize("batch", [PLAN_BATCH_LIMIT, PLAN_BATCH_LIMIT + 4])
 @pytest.mark.parametrize("hq,hkv", [(8, 2), (16, 2)])
-def test_large_batches_with_and_without_the_plan(batch, hq, hkv):
+def test_large_batches_with_and_without_the_plan(batch, hq, hkv, flags):
     """At the plan's batch limit the plan is largest; one past it the units
     run in sequence order.  Both match the oracle, and a sub-batch (always
     planned) gives the same bits for its sequences."""
-    print("case batch", batch, "hq", hq, "hkv", hkv, flush=True)
+    print("case batch", batch, "hq", hq, "hkv", hkv, "flags", flags, flush=True)
     p = problem(hq, hkv, short_lengths(batch, seed=batch + hq), seed=batch + hq)
-    got = run_gpu(p, split_tokens=64)
+    got = run_gpu(p, split_tokens=64, flags=flags)
     print(check_close(bf16_to_f64(got), oracle_ref(p), "batch %d G=%d" % (batch, hq // hkv)))
     rows = list(range(0, batch, 7))
-    part = run_gpu(sub_problem(p, rows), split_tokens=64)
+    part = run_gpu(sub_problem(p, rows), split_tokens=64, flags=flags)
     assert torch.equal(part.view(torch.int16), got[rows].view(torch.int16))
+
+
+@pytest.mark.parametrize("kv,layout", [("bf16", "hnd"), ("fp8_e4m3", "hnd"), ("bf16", "nhd")])
+def test_checked_mode_on_the_persistent_schedule(kv, layout):
+    """A checked handle on a launch with many units (longest-first plan): a
+    block-table entry out of range and a sequence longer than its table row
+    are reported without a fault, and every other sequence's output keeps its
+    bits."""
+    lengths = [1000 + 37 * (i % 11) for i in range(300)]
+    p = problem(8, 2, lengths, seed=71, kv=kv, layout=layout)
+    with B.DecodeAttention.for_problem(p, flags=B.RL_DA_CHECKED, split_tokens=64) as attn:
+        assert attn.unit_heads() == 1 and attn.split_info(p.max_pages)[1] > 1
+        good = run_gpu(p, attn=attn)
+        assert attn.check_error() == 0
+        print(check_close(bf16_to_f64(good), oracle_ref(p), "checked persistent " + kv + layout))
+        others = [b for b in range(len(lengths)) if b not in (5, 123)]
+        bad_table = p.block_table.clone()
+        bad_table[123, 7] = p.num_pages + 5        # inside sequence 123
+        q = workloads.DecodeProblem(**{**p.__dict__, "block_table": bad_table})
+        got = run_gpu(q, attn=attn)
+        assert attn.check_error() & B.RL_DA_DEVERR_PAGE_OUT_OF_RANGE
+        assert torch.equal(got[others].view(torch.int16), good[others].view(torch.int16))
+        long_lens = p.seq_lens.clone()
+        long_lens[5] = p.max_pages * 16 + 1        # longer than its table row
+        q = workloads.DecodeProblem(**{**p.__dict__, "seq_lens": long_lens})
+        got = run_gpu(q, attn=attn)
+        assert attn.check_error() & B.RL_DA_DEVERR_LENGTH_TOO_LONG
+        assert torch.equal(got[others].view(torch.int16), good[others].view(torch.int16))
 
 
 @pytest.mark.parametrize("kv,layout,flags", [
