@@ -37,15 +37,18 @@ def bench_kernels():
     vp, sz, i32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32
     lib.rl_bench_copy.argtypes = [vp, vp, sz, vp]
     lib.rl_bench_stream_read.argtypes = [vp, sz, vp, ctypes.c_int, vp]
-    lib.rl_bench_page_read.argtypes = [vp, vp, vp, i32, vp, i32, i32, i32, i32, vp, vp]
+    lib.rl_bench_page_read.argtypes = [vp, vp, vp, i32, vp, ctypes.c_int64, i32, i32, i32,
+                                       i32, vp, vp]
     for f in (lib.rl_bench_copy, lib.rl_bench_stream_read, lib.rl_bench_page_read):
         f.restype = ctypes.c_int
     return lib
 
 
-def read_ceilings(p, split_pages, stream):
+def read_ceilings(p, stream):
     """Achievable read bandwidth: a contiguous 4 GiB stream, and the decode
-    step's own K/V page reads with no arithmetic.  Best of several runs."""
+    step's own K/V page reads with no arithmetic, divided evenly over the
+    work-groups (64 pages of one kv head each).  Best of several runs."""
+    import numpy as np
     import torch
     lib = bench_kernels()
     s = stream.cuda_stream
@@ -63,8 +66,13 @@ def read_ceilings(p, split_pages, stream):
             if it:
                 best_stream = max(best_stream, nbytes / (e0.elapsed_time(e1) / 1e3) / 1e9)
     del buf
-    units = p.batch * p.num_kv_heads * ((p.max_pages + split_pages - 1) // split_pages)
-    sink = torch.empty(units * 256, dtype=torch.int32, device="cuda")
+    unit_pages = 64
+    pages = (np.clip(p.lengths(), 0, p.max_pages * p.page_size) + p.page_size - 1) // p.page_size
+    prefix = np.concatenate([[0], np.cumsum(pages)]).astype(np.int32)
+    total_pages = int(prefix[-1])
+    prefix_dev = torch.from_numpy(prefix).to("cuda")
+    units = p.num_kv_heads * ((total_pages + unit_pages - 1) // unit_pages)
+    sink = torch.empty(max(units, 1) * 256, dtype=torch.int32, device="cuda")
     best_page = 0.0
     kv = p.kv_bytes()
     slab = p.page_size * p.head_dim * (2 if p.kv_dtype == "bf16" else 1)
@@ -73,8 +81,9 @@ def read_ceilings(p, split_pages, stream):
         e0.record(stream)
         assert lib.rl_bench_page_read(p.k_pool.data_ptr(), p.v_pool.data_ptr(),
                                       p.block_table.data_ptr(), p.max_pages,
-                                      p.seq_lens.data_ptr(), p.batch, p.num_kv_heads,
-                                      split_pages, slab, sink.data_ptr(), s) == 0
+                                      prefix_dev.data_ptr(), total_pages, p.batch,
+                                      p.num_kv_heads, unit_pages, slab, sink.data_ptr(),
+                                      s) == 0
         e1.record(stream)
         e1.synchronize()
         if it:
@@ -648,7 +657,7 @@ def main():
     attn.close()
     if not args.no_ceilings:
         print("bench: measuring read ceilings", file=sys.stderr, flush=True)
-        ceil = read_ceilings(base, split_tokens // base.page_size, stream)
+        ceil = read_ceilings(base, stream)
         record["read_ceiling"] = ceil
         if "roofline" in record:
             record["roofline"]["frac_of_stream_read"] = round(

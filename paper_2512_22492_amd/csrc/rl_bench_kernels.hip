@@ -6,11 +6,12 @@
 //                         traffic counters.
 //   rl_bench_stream_read  contiguous read of a buffer, one contiguous share per
 //                         work-group: the achievable HBM read bandwidth.
-//   rl_bench_page_read    reads exactly the K/V bytes one decode step reads, in
-//                         the same work units (four wavefronts per (sequence,
-//                         kv head, split), pages taken in turn) and the same
-//                         per-lane non-temporal load pattern as the split-K
-//                         attention kernel, with no arithmetic: the ceiling of
+//   rl_bench_page_read    reads exactly the K/V bytes one decode step reads, with
+//                         the split-K attention kernel's per-lane non-temporal
+//                         load pattern (head-major slabs) and no arithmetic,
+//                         the step's pages divided evenly over the work-groups
+//                         (four wavefronts per (64 consecutive pages of the
+//                         batch, kv head), kv heads adjacent): the ceiling of
 //                         that access pattern.
 //
 // All pointers are device pointers owned by the caller.  Each function
@@ -73,57 +74,68 @@ struct PageReadArgs {
     const uint8_t* k_pool;
     const uint8_t* v_pool;
     const int32_t* block_table;
-    const int32_t* seq_lens;
+    const int32_t* page_prefix;  // [batch + 1]: pages of the sequences before b
     uint32_t* sink;
+    int64_t total_pages;         // page_prefix[batch]
     int32_t num_kv_heads;
     int32_t max_pages;
-    int32_t split_pages;
-    int32_t num_splits;
-    int32_t slab_bytes;  // 4096 (bf16) or 2048 (e4m3)
+    int32_t batch;
+    int32_t unit_pages;
+    int32_t slab_bytes;          // 4096 (bf16) or 2048 (e4m3)
 };
 
 __global__ __launch_bounds__(64 * kUnitWaves) void page_read_kernel(PageReadArgs a)
 {
-    const int unit = blockIdx.x;
-    const int s = unit % a.num_splits;
-    const int bk = unit / a.num_splits;
-    const int kvh = bk % a.num_kv_heads;
-    const int b = bk / a.num_kv_heads;
+    const int kvh = blockIdx.x % a.num_kv_heads;
+    const int64_t i0 = (int64_t)(blockIdx.x / a.num_kv_heads) * a.unit_pages;
+    const int64_t i1 = min(i0 + (int64_t)a.unit_pages, a.total_pages);
     const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
-    const int L = min(a.seq_lens[b], a.max_pages * 16);
-    const int npages = L > 0 ? (L + 15) / 16 : 0;
-    const int p0 = s * a.split_pages;
-    const int p1 = min(p0 + a.split_pages, npages);
+    int64_t i = i0 + wave;
+    // sequence of page i: page_prefix[b] <= i < page_prefix[b + 1]
+    int b = 0;
+    if (i < i1) {
+        int hi = a.batch;  // page_prefix[hi] = total_pages > i
+        while (hi - b > 1) {
+            const int mid = (b + hi) >> 1;
+            if (a.page_prefix[mid] <= i)
+                b = mid;
+            else
+                hi = mid;
+        }
+    }
     uint32_t acc = 0;
     const int koff = (lane & 15) * 256 + 16 * (lane >> 4);
     const int voff = lane * 16;
-    for (int j = p0 + wave; j < p1; j += kUnitWaves) {
+    for (; i < i1; i += kUnitWaves) {
+        while (a.page_prefix[b + 1] <= i)  // ends: page_prefix[batch] > i
+            ++b;
+        const int j = (int)(i - a.page_prefix[b]);
         const int64_t page = a.block_table[(int64_t)b * a.max_pages + j];
         const int64_t slab = (page * a.num_kv_heads + kvh) * a.slab_bytes;
         if (a.slab_bytes == 4096) {
             uint4 k[4], v[4];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                k[i] = load_stream16(a.k_pool + slab + koff + 64 * i);
-                v[i] = load_stream16(a.v_pool + slab + voff + 1024 * i);
+            for (int r = 0; r < 4; ++r) {
+                k[r] = load_stream16(a.k_pool + slab + koff + 64 * r);
+                v[r] = load_stream16(a.v_pool + slab + voff + 1024 * r);
             }
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-                acc ^= k[i].x ^ k[i].y ^ k[i].z ^ k[i].w ^ v[i].x ^ v[i].y ^ v[i].z ^ v[i].w;
+            for (int r = 0; r < 4; ++r)
+                acc ^= k[r].x ^ k[r].y ^ k[r].z ^ k[r].w ^ v[r].x ^ v[r].y ^ v[r].z ^ v[r].w;
         } else {
             const int koff8 = (lane & 15) * 128 + 16 * (lane >> 4);
             uint4 k[2], v[2];
 #pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                k[i] = load_stream16(a.k_pool + slab + koff8 + 64 * i);
-                v[i] = load_stream16(a.v_pool + slab + voff + 1024 * i);
+            for (int r = 0; r < 2; ++r) {
+                k[r] = load_stream16(a.k_pool + slab + koff8 + 64 * r);
+                v[r] = load_stream16(a.v_pool + slab + voff + 1024 * r);
             }
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
-                acc ^= k[i].x ^ k[i].y ^ k[i].z ^ k[i].w ^ v[i].x ^ v[i].y ^ v[i].z ^ v[i].w;
+            for (int r = 0; r < 2; ++r)
+                acc ^= k[r].x ^ k[r].y ^ k[r].z ^ k[r].w ^ v[r].x ^ v[r].y ^ v[r].z ^ v[r].w;
         }
     }
-    a.sink[(size_t)unit * 64 * kUnitWaves + threadIdx.x] = acc;
+    a.sink[(size_t)blockIdx.x * 64 * kUnitWaves + threadIdx.x] = acc;
 }
 
 }  // namespace
@@ -153,28 +165,36 @@ int rl_bench_stream_read(const void* src, size_t bytes, uint32_t* sink, int grid
 }
 
 // Pools [P][Hkv][16][128] of 2-byte (slab_bytes 4096) or 1-byte (2048)
-// elements; sink must hold batch*num_kv_heads*num_splits*256 words.
+// elements; block_table [batch][max_pages].
+// page_prefix: device int32 [batch + 1], page_prefix[b] = pages of sequences
+// 0 .. b-1 (each sequence's ceil(min(len, 16 * max_pages) / 16)); total_pages
+// = page_prefix[batch].  sink: grid * 256 words, grid = num_kv_heads *
+// ceil(total_pages / unit_pages).
 int rl_bench_page_read(const void* k_pool, const void* v_pool, const int32_t* block_table,
-                       int32_t max_pages, const int32_t* seq_lens, int32_t batch,
-                       int32_t num_kv_heads, int32_t split_pages, int32_t slab_bytes,
-                       uint32_t* sink, void* stream)
+                       int32_t max_pages, const int32_t* page_prefix, int64_t total_pages,
+                       int32_t batch, int32_t num_kv_heads, int32_t unit_pages,
+                       int32_t slab_bytes, uint32_t* sink, void* stream)
 {
     if (k_pool == nullptr || v_pool == nullptr || block_table == nullptr ||
-        seq_lens == nullptr || sink == nullptr || batch <= 0 || num_kv_heads <= 0 ||
-        max_pages <= 0 || split_pages <= 0 || (slab_bytes != 4096 && slab_bytes != 2048))
+        page_prefix == nullptr || sink == nullptr || batch <= 0 || num_kv_heads <= 0 ||
+        max_pages <= 0 || unit_pages <= 0 || total_pages < 0 ||
+        (slab_bytes != 4096 && slab_bytes != 2048))
         return -1;
+    if (total_pages == 0)
+        return 0;
     PageReadArgs a;
     a.k_pool = (const uint8_t*)k_pool;
     a.v_pool = (const uint8_t*)v_pool;
     a.block_table = block_table;
-    a.seq_lens = seq_lens;
+    a.page_prefix = page_prefix;
     a.sink = sink;
+    a.total_pages = total_pages;
     a.num_kv_heads = num_kv_heads;
     a.max_pages = max_pages;
-    a.split_pages = split_pages;
-    a.num_splits = (max_pages + split_pages - 1) / split_pages;
+    a.batch = batch;
+    a.unit_pages = unit_pages;
     a.slab_bytes = slab_bytes;
-    const int64_t units = (int64_t)batch * num_kv_heads * a.num_splits;
+    const int64_t units = (int64_t)num_kv_heads * ((total_pages + unit_pages - 1) / unit_pages);
     hipLaunchKernelGGL(page_read_kernel, dim3((unsigned)units), dim3(64 * kUnitWaves), 0,
                        (hipStream_t)stream, a);
     return (int)hipGetLastError();
