@@ -15,8 +15,9 @@ namespace {
 // wavefronts for (sequence b, kv head, tile of 128/G new tokens): 128 query
 // rows, row r = (token r / G, head r % G); wavefront w owns rows 32w..32w+31 as
 // two blocks of 16.  The keys the tile can see pass through LDS 64 at a time
-// (four pages: K as [key][dim], V transposed to [dim][key]), double-buffered
-// with one barrier per stage.
+// (four pages, K and V both as [key][dim] rows), double-buffered with one
+// barrier per stage; the next stage's loads are in flight during the current
+// stage's products.
 //
 // Both products run transposed so that every lane keeps one query row from
 // the scores to the output.  S^T = K Q^T (v_mfma_f32_16x16x32_bf16, A = 16
@@ -24,24 +25,37 @@ namespace {
 // l%16 and keys 4(l/16)+j of each 16-key block; O^T += V^T P^T (same MFMA,
 // 32 keys) takes P^T straight from those registers, with the k index of the
 // product running over keys in the order (4g..4g+3, 16+4g..16+4g+3) for lane
-// group g, and V^T read from LDS in the same order.  Row max, rescale and sum
-// are therefore lane-local but for two shuffles per 64 keys.  P enters the
-// PV product rounded to bf16 (relative error at most 2^-8 per weight, as in
-// common flash-attention kernels; an earlier two-term hi + lo split kept
-// fp32-level accuracy at a third more MFMAs and conversion work); l sums the
-// unrounded fp32 probabilities.
+// group g; the V^T operand in that order comes from the [key][dim] rows by
+// the LDS transpose read.  Row max, rescale and sum are therefore lane-local
+// but for two shuffles per 64 keys.  P enters the PV product rounded to bf16
+// (relative error at most 2^-8 per weight, as in common flash-attention
+// kernels; an earlier two-term hi + lo split kept fp32-level accuracy at a
+// third more MFMAs and conversion work); l sums the unrounded fp32
+// probabilities.
+//
+// Work-group order: consecutive work-groups go to the eight XCDs in turn,
+// and the tiles of one (sequence, kv head) read the same keys, so they are
+// placed on one XCD (one L2) -- see the unit mapping in the kernel.
 
 constexpr int kRowBlocks = 2;                      // 16-row blocks per wavefront
 constexpr int kTileRows = kUnitWaves * kRowBlocks * 16;
 constexpr int kStageKeys = 64;                     // keys per LDS stage (4 pages)
 constexpr int kStagePages = kStageKeys / kPageSize;
-constexpr int kKRow = kHeadDim + 8;                // K [key][dim] row, padded (bf16)
-constexpr int kVtRow = kStageKeys + 4;             // V^T [dim][key] row, padded (bf16)
+constexpr int kKRow = kHeadDim + 8;                // K and V [key][dim] row, padded (bf16)
 
-// Column of key k in V^T row `dim`: keys are XORed with 8 * (dim / 16 % 8), so
-// that the staging writes of one instruction (8 dim blocks x 4 key pairs)
-// fall in 32 different banks; runs of 4 keys stay contiguous for the reads.
-__device__ __forceinline__ int vt_col(int dim, int key) { return key ^ (8 * ((dim >> 4) & 7)); }
+typedef short short4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) short4_t lds_short4_t;
+
+// Four bf16 of one dim from four consecutive key rows of a [key][dim] LDS
+// tile (ds_read_b64_tr_b16).  Within each 16-lane group, lane j receives
+// element j % 4 of the 8-byte chunks addressed by lanes j / 4 + 4e, e = 0..3:
+// when lane s addresses row (base + s / 4), dims (d0 + 4 (s % 4)) .. +3, lane
+// j gets rows base .. base + 3 of dim d0 + j.
+__device__ __forceinline__ uint2 lds_read_transposed(const uint16_t* p)
+{
+    const short4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_t*)p);
+    return __builtin_bit_cast(uint2, v);
+}
 
 struct ExtendArgs {
     const uint16_t* q;          // bf16 [T][Hq][D]
@@ -73,10 +87,26 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
     static_assert(G >= 1 && G <= 16 && 16 % G == 0, "16-row blocks hold whole groups");
     constexpr int kTileTok = kTileRows / G;
     __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][kStageKeys][kKRow];
-    __shared__ __attribute__((aligned(16))) uint16_t vt_lds[2][kHeadDim][kVtRow];
+    __shared__ __attribute__((aligned(16))) uint16_t v_lds[2][kStageKeys][kKRow];
+    // e4m3 pools: (k_scale, v_scale) of the stage's four pages
+    __shared__ __attribute__((aligned(16))) float2 scale_lds[2][kStagePages];
 
-    const int tile = blockIdx.x % a.num_tiles;
-    const int bk = blockIdx.x / a.num_tiles;
+    // Work-group g runs on XCD g % 8.  Pairs (sequence, kv head) are dealt
+    // to the XCDs in turn, pair p to XCD p % 8 with all its tiles, so the
+    // tiles that read the same keys share an L2 and every XCD takes every
+    // eighth pair of the batch; pairs past the last whole eight follow in
+    // grid order.
+    const int T = a.num_tiles;
+    const int g = blockIdx.x;
+    const int main_units = (int)(gridDim.x / T / 8) * 8 * T;
+    int bk, tile;
+    if (g < main_units) {
+        bk = (g / 8 / T) * 8 + g % 8;
+        tile = (g / 8) % T;
+    } else {
+        bk = g / T;
+        tile = g % T;
+    }
     const int kvh = bk % a.num_kv_heads;
     const int b = bk / a.num_kv_heads;
     const int q0 = a.q_start[b];
@@ -132,8 +162,9 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
     const int32_t* bt = a.block_table + (int64_t)b * a.max_pages;
     constexpr int kElt = FP8 ? 1 : 2;
     const int64_t st_off = (int64_t)kvh * a.head_bytes + kElt * (16 * st_c);
-    const int npages = (L + kPageSize - 1) / kPageSize;
-    uint4 kr[2][2], vr[2][2];  // [key of the pair][half of the 16 dims] (bf16)
+    uint4 kr[2][2], vr[2][2];  // bf16: [key of the pair][half of the 16 dims]
+    uint4 kc[2], vc[2];        // e4m3: the codes of the pair's 16 dims
+    float ksr = 0.0f, vsr = 0.0f;  // e4m3: scales of the thread's page
     // The block-table entry of the thread's key pair (both keys share a
     // page) is read one stage ahead, so a stage's K/V loads do not wait on
     // a table load.
@@ -141,21 +172,32 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
         const int key = stage * kStageKeys + 2 * st_kp;
         return key < L ? bt[key / kPageSize] : 0;
     };
+    // Loads are unconditional, so that nothing between a load and the
+    // staging of its data waits for it: a key past the sequence end reads its
+    // slot in page 0, which every pool has (stage_page gives page 0 there),
+    // and is discarded at staging (its value row and, for a page wholly past
+    // the end, its scales are overwritten; its scores are masked to -inf).
+    bool live[2];
     auto fetch = [&](int stage, int page) {
+        if (FP8) {
+            const int64_t slab = (int64_t)page * a.num_kv_heads + kvh;
+            ksr = a.k_scale[slab];
+            vsr = a.v_scale[slab];
+        }
 #pragma unroll
         for (int e = 0; e < 2; ++e) {
             const int key = stage * kStageKeys + 2 * st_kp + e;
-            if (key < L) {  // pages past the sequence are never read
-                const int64_t off = (int64_t)page * a.page_bytes + st_off +
-                                    (int64_t)(key % kPageSize) * a.row_bytes;
+            live[e] = key < L;
+            const int64_t off = (int64_t)page * a.page_bytes + st_off +
+                                (int64_t)(key % kPageSize) * a.row_bytes;
+            if (FP8) {
+                kc[e] = load_stream16(a.k_pool + off);
+                vc[e] = load_stream16(a.v_pool + off);
+            } else {
                 kr[e][0] = load_stream16(a.k_pool + off);
                 vr[e][0] = load_stream16(a.v_pool + off);
-                if (!FP8) {
-                    kr[e][1] = load_stream16(a.k_pool + off + 16);
-                    vr[e][1] = load_stream16(a.v_pool + off + 16);
-                }
-            } else {  // slots past the sequence end may hold NaN: stage zeros
-                kr[e][0] = kr[e][1] = vr[e][0] = vr[e][1] = make_uint4(0, 0, 0, 0);
+                kr[e][1] = load_stream16(a.k_pool + off + 16);
+                vr[e][1] = load_stream16(a.v_pool + off + 16);
             }
         }
     };
@@ -171,32 +213,41 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
         hi = make_uint4(cvt(c.z, F{}), cvt(c.z, T{}), cvt(c.w, F{}), cvt(c.w, T{}));
     };
     auto stash = [&](int buf) {
-        if (FP8) {
+        uint4 ks[2][2], vs[2][2];
 #pragma unroll
-            for (int e = 0; e < 2; ++e) {
-                const uint4 kc = kr[e][0], vc = vr[e][0];
-                widen(kc, kr[e][0], kr[e][1]);
-                widen(vc, vr[e][0], vr[e][1]);
+        for (int e = 0; e < 2; ++e) {
+            if (FP8) {
+                widen(kc[e], ks[e][0], ks[e][1]);
+                widen(vc[e], vs[e][0], vs[e][1]);
+            } else {
+                ks[e][0] = kr[e][0];
+                ks[e][1] = kr[e][1];
+                vs[e][0] = vr[e][0];
+                vs[e][1] = vr[e][1];
             }
         }
 #pragma unroll
         for (int e = 0; e < 2; ++e) {
             uint4* krow = reinterpret_cast<uint4*>(&k_lds[buf][2 * st_kp + e][16 * st_c]);
-            krow[0] = kr[e][0];
-            krow[1] = kr[e][1];
+            krow[0] = ks[e][0];
+            krow[1] = ks[e][1];
         }
-        // V^T: dims 16c..16c+15, the key pair as one 32-bit word per dim
-        const uint32_t w0[8] = {vr[0][0].x, vr[0][0].y, vr[0][0].z, vr[0][0].w,
-                                vr[0][1].x, vr[0][1].y, vr[0][1].z, vr[0][1].w};
-        const uint32_t w1[8] = {vr[1][0].x, vr[1][0].y, vr[1][0].z, vr[1][0].w,
-                                vr[1][1].x, vr[1][1].y, vr[1][1].z, vr[1][1].w};
-        const int col = vt_col(16 * st_c, 2 * st_kp);  // same swizzle for all 16 dims
 #pragma unroll
-        for (int d = 0; d < 8; ++d) {
-            *reinterpret_cast<uint32_t*>(&vt_lds[buf][16 * st_c + 2 * d][col]) =
-                (w0[d] & 0xffffu) | (w1[d] << 16);
-            *reinterpret_cast<uint32_t*>(&vt_lds[buf][16 * st_c + 2 * d + 1][col]) =
-                (w0[d] >> 16) | (w1[d] & 0xffff0000u);
+        for (int e = 0; e < 2; ++e) {
+            uint4* vrow = reinterpret_cast<uint4*>(&v_lds[buf][2 * st_kp + e][16 * st_c]);
+            vrow[0] = vs[e][0];
+            vrow[1] = vs[e][1];
+            if (!live[e]) {  // slots past the sequence end may hold NaN
+                vrow[0] = make_uint4(0, 0, 0, 0);
+                vrow[1] = make_uint4(0, 0, 0, 0);
+            }
+        }
+        // The first key of each page carries the page's scales; a page
+        // wholly past the end takes 1 (its keys are masked, its values zero).
+        if (FP8 && st_c == 0 && st_kp % (kPageSize / 2) == 0) {
+            scale_lds[buf][st_kp / (kPageSize / 2)] = make_float2(ksr, vsr);
+            if (!live[0])
+                scale_lds[buf][st_kp / (kPageSize / 2)] = make_float2(1.0f, 1.0f);
         }
     };
 
@@ -220,12 +271,9 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
             sl[kb] = a.scale_log2;
             vsc[kb] = 1.0f;
             if (FP8) {
-                const int pg = j * kStagePages + kb;
-                if (pg < npages) {
-                    const int64_t slab = (int64_t)bt[pg] * a.num_kv_heads + kvh;
-                    sl[kb] *= a.k_scale[slab];
-                    vsc[kb] = a.v_scale[slab];
-                }
+                const float2 ps = scale_lds[buf][kb];
+                sl[kb] *= ps.x;
+                vsc[kb] = ps.y;
             }
         }
 
@@ -350,12 +398,9 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
         // operand of the next (db, kh) is read before this one's MFMAs.
         auto vt_operand = [&](int step) {
             const int db = step >> 1, kh = step & 1;
-            const int dim = 16 * db + i16;
-            const uint16_t* vrow = &vt_lds[buf][dim][0];
-            const uint2 va =
-                *reinterpret_cast<const uint2*>(vrow + vt_col(dim, 32 * kh + 4 * g4));
-            const uint2 vb =
-                *reinterpret_cast<const uint2*>(vrow + vt_col(dim, 32 * kh + 16 + 4 * g4));
+            const uint16_t* vp = &v_lds[buf][32 * kh + 4 * g4 + (i16 >> 2)][16 * db + 4 * (i16 & 3)];
+            const uint2 va = lds_read_transposed(vp);
+            const uint2 vb = lds_read_transposed(vp + 16 * kKRow);
             return make_uint4(va.x, va.y, vb.x, vb.y);
         };
         uint4 vt_next = vt_operand(0);

@@ -121,6 +121,45 @@ def test_extend_ignores_unread_memory_and_is_causal():
     assert torch.equal(moved[20:].view(torch.int16), base[20:].view(torch.int16))
 
 
+@pytest.mark.parametrize("kv,layout", [("bf16", "hnd"), ("fp8_e4m3", "hnd"), ("bf16", "nhd"),
+                                       ("fp8_e4m3", "nhd")])
+def test_extend_ignores_page_zero_and_the_table_tail(kv, layout):
+    """Keys past a sequence's end are staged from page 0 and discarded; table
+    entries past a sequence's pages are never read.  With page 0 out of use
+    and filled with NaN (codes and, for e4m3 pools, scales) and every table
+    row's tail out of range, each output keeps its bits."""
+    new, prior = [37, 1, 64, 20, 9], [70, 0, 130, 300, 7]   # partial pages and stages
+    p, q, q_start = extend_problem(new, prior, seed=44, hq=16, hkv=4, layout=layout, kv=kv)
+    bt = p.block_table.clone()
+    pages = [(int(L) + 15) // 16 for L in p.seq_lens.cpu()]
+    used = {int(x) for b, n in enumerate(pages) for x in bt[b, :n].cpu()}
+    if 0 in used:  # move page 0's tokens to a spare page
+        spare = next(x for x in range(1, p.num_pages) if x not in used)
+        for t in (p.k_pool, p.v_pool) + ((p.k_scale, p.v_scale) if kv != "bf16" else ()):
+            t[spare] = t[0]
+        for b, n in enumerate(pages):
+            row = bt[b, :n]
+            row[row == 0] = spare
+    p = workloads.DecodeProblem(**{**p.__dict__, "block_table": bt})
+    base = run_extend(p, q, q_start, max(new))
+    print(check_close(bf16_to_f64(base), oracle_extend(p, q, q_start), "page 0 " + kv + layout,
+                      extra_abs=p_split_bound(p)))
+    if kv == "bf16":
+        p.k_pool[0] = float("nan")
+        p.v_pool[0] = float("nan")
+    else:
+        p.k_pool[0] = 0x7F   # e4m3 NaN
+        p.v_pool[0] = 0x7F
+        p.k_scale[0] = float("nan")
+        p.v_scale[0] = float("nan")
+    tail = bt.clone()
+    for b, n in enumerate(pages):
+        tail[b, n:] = 1 << 30
+    got = run_extend(workloads.DecodeProblem(**{**p.__dict__, "block_table": tail}),
+                     q, q_start, max(new))
+    assert torch.equal(got.view(torch.int16), base.view(torch.int16))
+
+
 def test_extend_argument_validation():
     p, q, q_start = extend_problem([3, 2], [4, 4], seed=42)
     out = torch.empty_like(q)
