@@ -27,7 +27,7 @@ namespace {
 // product running over keys in the order (4g..4g+3, 16+4g..16+4g+3) for lane
 // group g; the V^T operand in that order comes from the [key][dim] rows by
 // the LDS transpose read.  Row max, rescale and sum are therefore lane-local
-// but for two shuffles per 64 keys.  P enters the PV product rounded to bf16
+// but for two lane swaps per 64 keys.  P enters the PV product rounded to bf16
 // (relative error at most 2^-8 per weight, as in common flash-attention
 // kernels; an earlier two-term hi + lo split kept fp32-level accuracy at a
 // third more MFMAs and conversion work); l sums the unrounded fp32
@@ -55,6 +55,36 @@ __device__ __forceinline__ uint2 lds_read_transposed(const uint16_t* p)
 {
     const short4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_t*)p);
     return __builtin_bit_cast(uint2, v);
+}
+
+// A lane's value and that of lane l ^ 16 (permlane16_swap exchanges 16-lane
+// rows 1 <-> 0 and 3 <-> 2 between its two operands: with both equal to v,
+// lane l receives v of lanes l & ~16 and l | 16), or of lane l ^ 32
+// (permlane32_swap, the two halves).  Vector-ALU operations, no LDS round
+// trip.
+__device__ __forceinline__ float max_lanes_xor16(float v)
+{
+    const auto s = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v),
+                                                    false, false);
+    return fmaxf(__uint_as_float(s[0]), __uint_as_float(s[1]));
+}
+__device__ __forceinline__ float max_lanes_xor32(float v)
+{
+    const auto s = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v),
+                                                    false, false);
+    return fmaxf(__uint_as_float(s[0]), __uint_as_float(s[1]));
+}
+__device__ __forceinline__ float sum_lanes_xor16(float v)
+{
+    const auto s = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v),
+                                                    false, false);
+    return __uint_as_float(s[0]) + __uint_as_float(s[1]);
+}
+__device__ __forceinline__ float sum_lanes_xor32(float v)
+{
+    const auto s = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v),
+                                                    false, false);
+    return __uint_as_float(s[0]) + __uint_as_float(s[1]);
 }
 
 struct ExtendArgs {
@@ -253,7 +283,10 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
 
     fetch(0, stage_page(0));
     int next_page = stage_page(1);
-    for (int j = 0; j < nstages; ++j) {
+    // One stage; stages that cannot cross a query position (all but the
+    // last one or two of a tile) are compiled without the causal mask.
+    auto stage = [&](const int j, auto masked_t) {
+        constexpr bool masked = decltype(masked_t)::value;
         const int buf = j & 1;
         stash(buf);
         if (j + 1 < nstages) {
@@ -302,7 +335,6 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
         // Probabilities (masked only in stages that can cross a query
         // position; rows past the tile's tokens score 0 and stay finite) and
         // O^T += V^T P^T: lane holds dims 16db + 4g4 + jj of row i16.
-        const bool masked = j >= first_masked_stage;
         // Row max of the scaled scores (log2 units) over the stage for both
         // row blocks (lane-local over 16 keys, then the two other lane groups
         // of the row).  With every page's multiplier positive (the usual
@@ -348,10 +380,10 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
             stage_max(std::true_type{});
 #pragma unroll
         for (int rb = 0; rb < kRowBlocks; ++rb)
-            mx[rb] = fmaxf(mx[rb], __shfl_xor(mx[rb], 16));
+            mx[rb] = max_lanes_xor16(mx[rb]);
 #pragma unroll
         for (int rb = 0; rb < kRowBlocks; ++rb)
-            mx[rb] = fmaxf(mx[rb], __shfl_xor(mx[rb], 32));  // finite: key 0 is visible
+            mx[rb] = max_lanes_xor32(mx[rb]);  // finite: key 0 is visible
         bool grow = false;
 #pragma unroll
         for (int rb = 0; rb < kRowBlocks; ++rb)
@@ -420,14 +452,17 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
                     o[rb][db], 0, 0, 0);
             }
         }
-    }
+    };
+    int j = 0;
+    for (; j < min(first_masked_stage, nstages); ++j)
+        stage(j, std::false_type{});
+    for (; j < nstages; ++j)
+        stage(j, std::true_type{});
 
     // out[row] = O[row] / l[row]; lane holds row i16, dims 16db + 4g4 + jj.
 #pragma unroll
     for (int rb = 0; rb < kRowBlocks; ++rb) {
-        float l = lsum[rb];
-        l += __shfl_xor(l, 16);
-        l += __shfl_xor(l, 32);
+        const float l = sum_lanes_xor32(sum_lanes_xor16(lsum[rb]));
         if (!row_real[rb])
             continue;
         const int r = wave * (kRowBlocks * 16) + rb * 16 + i16;
