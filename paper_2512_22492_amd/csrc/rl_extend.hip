@@ -318,7 +318,11 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
 #pragma unroll
             for (int rb = 0; rb < kRowBlocks; ++rb)
                 sacc[rb][kb] = floatx4_t{0.0f, 0.0f, 0.0f, 0.0f};
-        // dims outermost: eight independent accumulators between dependent MFMAs
+        // dims outermost: eight independent accumulators between dependent MFMAs.
+        // The two product phases run at raised wave priority: of the two
+        // wavefronts on a SIMD, one starting its products issues ahead of
+        // one in its softmax, which keeps the MFMA unit fed.
+        __builtin_amdgcn_s_setprio(1);
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks) {
 #pragma unroll
@@ -332,6 +336,7 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
                         sacc[rb][kb], 0, 0, 0);
             }
         }
+        __builtin_amdgcn_s_setprio(0);
         // Probabilities (masked only in stages that can cross a query
         // position; rows past the tile's tokens score 0 and stay finite) and
         // O^T += V^T P^T: lane holds dims 16db + 4g4 + jj of row i16.
@@ -435,6 +440,7 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
             const uint2 vb = lds_read_transposed(vp + 16 * kKRow);
             return make_uint4(va.x, va.y, vb.x, vb.y);
         };
+        __builtin_amdgcn_s_setprio(1);
         uint4 vt_next = vt_operand(0);
 #pragma unroll
         for (int step = 0; step < 16; ++step) {
@@ -452,6 +458,7 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
                     o[rb][db], 0, 0, 0);
             }
         }
+        __builtin_amdgcn_s_setprio(0);
     };
     int j = 0;
     for (; j < min(first_masked_stage, nstages); ++j)
