@@ -17,7 +17,7 @@ namespace {
 // two blocks of 16.  The keys the tile can see pass through LDS 64 at a time
 // (four pages, K and V both as [key][dim] rows), double-buffered with one
 // barrier per stage; the next stage's loads are in flight during the current
-// stage's products.
+// stage's products.  bf16 pages are staged 16 threads per whole key row.
 //
 // Both products run transposed so that every lane keeps one query row from
 // the scores to the output.  S^T = K Q^T (v_mfma_f32_16x16x32_bf16, A = 16
@@ -41,7 +41,10 @@ constexpr int kRowBlocks = 2;                      // 16-row blocks per wavefron
 constexpr int kTileRows = kUnitWaves * kRowBlocks * 16;
 constexpr int kStageKeys = 64;                     // keys per LDS stage (4 pages)
 constexpr int kStagePages = kStageKeys / kPageSize;
-constexpr int kKRow = kHeadDim + 8;                // K and V [key][dim] row, padded (bf16)
+// K and V [key][dim] rows padded to 288 bytes: the 16-byte K operand reads
+// and the transposed V reads of an instruction then meet no bank conflict
+// (measured: half the LDS cycles of 272-byte rows).
+constexpr int kKRow = kHeadDim + 16;
 
 typedef short short4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) short4_t lds_short4_t;
@@ -186,49 +189,63 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
             o[rb][db] = floatx4_t{0.0f, 0.0f, 0.0f, 0.0f};
     }
 
-    // Staging: thread t moves keys 2(t/8) and 2(t/8)+1, dims 16(t%8)..+15, of
-    // K and of V (two 16-byte loads each, one for e4m3).
-    const int st_kp = threadIdx.x / 8, st_c = threadIdx.x % 8;
-    const int32_t* bt = a.block_table + (int64_t)b * a.max_pages;
+    // Staging.  bf16 pools: thread t moves dims 8(t%16) .. +7 of key rows
+    // t/16 + 16r, r = 0..3 (slot t/16 of page r of the stage): 16 threads per
+    // whole key row, so that each staging write instruction covers four whole
+    // rows (every LDS bank once per row).  e4m3 pools (128-byte rows): thread
+    // t moves the codes of dims 16(t%8) .. +15 of keys 2(t/8) and 2(t/8) + 1
+    // (16-byte loads; whole-row staging would take 8-byte ones), widened to
+    // bf16 as they are staged.
+    //
+    // Loads are unconditional, so that nothing between a load and the staging
+    // of its data waits for it: page indices past the sequence are clamped to
+    // its last page, so a key past the end reads a slot of a page the sequence
+    // owns and is discarded (its value row is overwritten with zeros, its
+    // scores are masked to -inf; the clamped page's scales are finite).
+    constexpr int kRowsPerThread = FP8 ? 2 : kStagePages;
+    const int st_row = FP8 ? 2 * (threadIdx.x / 8) : threadIdx.x / 16;  // first key row
+    const int st_col = FP8 ? 16 * (threadIdx.x % 8) : 8 * (threadIdx.x % 16);  // first dim
+    const int npages = (L + kPageSize - 1) / kPageSize;  // >= 1 here
+    // The table row's address is uniform; held in vector registers, its
+    // loads are vector loads, counted with the K/V loads and waited for at
+    // the staging, instead of scalar loads, which share a counter with LDS
+    // accesses and would be waited for at the next barrier and LDS read.
+    typedef __attribute__((address_space(1))) const int32_t global_i32;
+    global_i32* bt = (global_i32*)(a.block_table + (int64_t)b * a.max_pages);
+    asm volatile("" : "+v"(bt));
     constexpr int kElt = FP8 ? 1 : 2;
-    const int64_t st_off = (int64_t)kvh * a.head_bytes + kElt * (16 * st_c);
-    uint4 kr[2][2], vr[2][2];  // bf16: [key of the pair][half of the 16 dims]
-    uint4 kc[2], vc[2];        // e4m3: the codes of the pair's 16 dims
-    float ksr = 0.0f, vsr = 0.0f;  // e4m3: scales of the thread's page
-    // The block-table entry of the thread's key pair (both keys share a
-    // page) is read one stage ahead, so a stage's K/V loads do not wait on
-    // a table load.
-    auto stage_page = [&](int stage) {
-        const int key = stage * kStageKeys + 2 * st_kp;
-        return key < L ? bt[key / kPageSize] : 0;
+    const int64_t st_off = (int64_t)kvh * a.head_bytes + kElt * st_col;
+    uint4 kr[kRowsPerThread], vr[kRowsPerThread];  // bf16 dims or e4m3 codes
+    float ksr = 1.0f, vsr = 1.0f;                  // e4m3: scales of page t % 4
+    // Key row of staging slot r and its page within the stage.
+    auto slot_row = [&](int r) { return FP8 ? st_row + r : r * kPageSize + st_row; };
+    // The table entries of a stage are read one stage ahead, so that its K/V
+    // loads do not wait on a table load: bf16, page r of the stage for slot
+    // r; e4m3, the page of the thread's key pair (and page t % 4 for the
+    // scales).
+    int pages_next[kStagePages];
+    auto stage_pages = [&](int stage, int* pg) {
+#pragma unroll
+        for (int r = 0; r < kStagePages; ++r) {
+            const int idx = FP8 ? (r == 0 ? st_row / kPageSize : (threadIdx.x & 3)) : r;
+            pg[r] = FP8 && r > 1 ? 0 : bt[min(stage * kStagePages + idx, npages - 1)];
+        }
     };
-    // Loads are unconditional, so that nothing between a load and the
-    // staging of its data waits for it: a key past the sequence end reads its
-    // slot in page 0, which every pool has (stage_page gives page 0 there),
-    // and is discarded at staging (its value row and, for a page wholly past
-    // the end, its scales are overwritten; its scores are masked to -inf).
-    bool live[2];
-    auto fetch = [&](int stage, int page) {
+    bool live[kRowsPerThread];
+    auto fetch = [&](int stage, const int* pg) {
+#pragma unroll
+        for (int r = 0; r < kRowsPerThread; ++r) {
+            const int row = slot_row(r);
+            live[r] = stage * kStageKeys + row < L;
+            const int64_t off = (int64_t)(FP8 ? pg[0] : pg[r]) * a.page_bytes + st_off +
+                                (int64_t)(row % kPageSize) * a.row_bytes;
+            kr[r] = load_stream16(a.k_pool + off);
+            vr[r] = load_stream16(a.v_pool + off);
+        }
         if (FP8) {
-            const int64_t slab = (int64_t)page * a.num_kv_heads + kvh;
+            const int64_t slab = (int64_t)pg[1] * a.num_kv_heads + kvh;
             ksr = a.k_scale[slab];
             vsr = a.v_scale[slab];
-        }
-#pragma unroll
-        for (int e = 0; e < 2; ++e) {
-            const int key = stage * kStageKeys + 2 * st_kp + e;
-            live[e] = key < L;
-            const int64_t off = (int64_t)page * a.page_bytes + st_off +
-                                (int64_t)(key % kPageSize) * a.row_bytes;
-            if (FP8) {
-                kc[e] = load_stream16(a.k_pool + off);
-                vc[e] = load_stream16(a.v_pool + off);
-            } else {
-                kr[e][0] = load_stream16(a.k_pool + off);
-                vr[e][0] = load_stream16(a.v_pool + off);
-                kr[e][1] = load_stream16(a.k_pool + off + 16);
-                vr[e][1] = load_stream16(a.v_pool + off + 16);
-            }
         }
     };
     // 16 e4m3 codes to 16 bf16 (exact), in order.
@@ -243,46 +260,37 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
         hi = make_uint4(cvt(c.z, F{}), cvt(c.z, T{}), cvt(c.w, F{}), cvt(c.w, T{}));
     };
     auto stash = [&](int buf) {
-        uint4 ks[2][2], vs[2][2];
 #pragma unroll
-        for (int e = 0; e < 2; ++e) {
+        for (int r = 0; r < kRowsPerThread; ++r) {
+            const int row = slot_row(r);
+            uint4* krow = reinterpret_cast<uint4*>(&k_lds[buf][row][st_col]);
+            uint4* vrow = reinterpret_cast<uint4*>(&v_lds[buf][row][st_col]);
             if (FP8) {
-                widen(kc[e], ks[e][0], ks[e][1]);
-                widen(vc[e], vs[e][0], vs[e][1]);
+                uint4 lo, hi;
+                widen(kr[r], lo, hi);
+                krow[0] = lo;
+                krow[1] = hi;
+                widen(vr[r], lo, hi);
+                vrow[0] = lo;
+                vrow[1] = hi;
+                if (!live[r]) {  // slots past the sequence end may hold NaN
+                    vrow[0] = make_uint4(0, 0, 0, 0);
+                    vrow[1] = make_uint4(0, 0, 0, 0);
+                }
             } else {
-                ks[e][0] = kr[e][0];
-                ks[e][1] = kr[e][1];
-                vs[e][0] = vr[e][0];
-                vs[e][1] = vr[e][1];
+                krow[0] = kr[r];
+                vrow[0] = vr[r];
+                if (!live[r])  // slots past the sequence end may hold NaN
+                    vrow[0] = make_uint4(0, 0, 0, 0);
             }
         }
-#pragma unroll
-        for (int e = 0; e < 2; ++e) {
-            uint4* krow = reinterpret_cast<uint4*>(&k_lds[buf][2 * st_kp + e][16 * st_c]);
-            krow[0] = ks[e][0];
-            krow[1] = ks[e][1];
-        }
-#pragma unroll
-        for (int e = 0; e < 2; ++e) {
-            uint4* vrow = reinterpret_cast<uint4*>(&v_lds[buf][2 * st_kp + e][16 * st_c]);
-            vrow[0] = vs[e][0];
-            vrow[1] = vs[e][1];
-            if (!live[e]) {  // slots past the sequence end may hold NaN
-                vrow[0] = make_uint4(0, 0, 0, 0);
-                vrow[1] = make_uint4(0, 0, 0, 0);
-            }
-        }
-        // The first key of each page carries the page's scales; a page
-        // wholly past the end takes 1 (its keys are masked, its values zero).
-        if (FP8 && st_c == 0 && st_kp % (kPageSize / 2) == 0) {
-            scale_lds[buf][st_kp / (kPageSize / 2)] = make_float2(ksr, vsr);
-            if (!live[0])
-                scale_lds[buf][st_kp / (kPageSize / 2)] = make_float2(1.0f, 1.0f);
-        }
+        if (FP8 && threadIdx.x < kStagePages)
+            scale_lds[buf][threadIdx.x] = make_float2(ksr, vsr);
     };
 
-    fetch(0, stage_page(0));
-    int next_page = stage_page(1);
+    stage_pages(0, pages_next);
+    fetch(0, pages_next);
+    stage_pages(1, pages_next);
     // One stage; stages that cannot cross a query position (all but the
     // last one or two of a tile) are compiled without the causal mask.
     auto stage = [&](const int j, auto masked_t) {
@@ -290,8 +298,8 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
         const int buf = j & 1;
         stash(buf);
         if (j + 1 < nstages) {
-            fetch(j + 1, next_page);
-            next_page = stage_page(j + 2);
+            fetch(j + 1, pages_next);
+            stage_pages(j + 2, pages_next);
         }
         __syncthreads();
 

@@ -123,15 +123,17 @@ def test_extend_ignores_unread_memory_and_is_causal():
 
 @pytest.mark.parametrize("kv,layout", [("bf16", "hnd"), ("fp8_e4m3", "hnd"), ("bf16", "nhd"),
                                        ("fp8_e4m3", "nhd")])
-def test_extend_ignores_page_zero_and_the_table_tail(kv, layout):
-    """Keys past a sequence's end are staged from page 0 and discarded; table
-    entries past a sequence's pages are never read.  With page 0 out of use
-    and filled with NaN (codes and, for e4m3 pools, scales) and every table
-    row's tail out of range, each output keeps its bits."""
+def test_extend_ignores_unstaged_memory_and_the_table_tail(kv, layout):
+    """Keys past a sequence's end are read from a slot of its last page and
+    discarded; table entries past a sequence's pages are never read; pages
+    no sequence uses are never read.  With the slots past each sequence's end
+    NaN, an unused page 0 NaN (codes and, for e4m3 pools, scales) and every
+    table row's tail out of range, each output keeps its bits."""
     new, prior = [37, 1, 64, 20, 9], [70, 0, 130, 300, 7]   # partial pages and stages
     p, q, q_start = extend_problem(new, prior, seed=44, hq=16, hkv=4, layout=layout, kv=kv)
     bt = p.block_table.clone()
-    pages = [(int(L) + 15) // 16 for L in p.seq_lens.cpu()]
+    lens = [int(L) for L in p.seq_lens.cpu()]
+    pages = [(L + 15) // 16 for L in lens]
     used = {int(x) for b, n in enumerate(pages) for x in bt[b, :n].cpu()}
     if 0 in used:  # move page 0's tokens to a spare page
         spare = next(x for x in range(1, p.num_pages) if x not in used)
@@ -142,14 +144,19 @@ def test_extend_ignores_page_zero_and_the_table_tail(kv, layout):
             row[row == 0] = spare
     p = workloads.DecodeProblem(**{**p.__dict__, "block_table": bt})
     base = run_extend(p, q, q_start, max(new))
-    print(check_close(bf16_to_f64(base), oracle_extend(p, q, q_start), "page 0 " + kv + layout,
+    print(check_close(bf16_to_f64(base), oracle_extend(p, q, q_start), "unstaged " + kv + layout,
                       extra_abs=p_split_bound(p)))
-    if kv == "bf16":
-        p.k_pool[0] = float("nan")
-        p.v_pool[0] = float("nan")
-    else:
-        p.k_pool[0] = 0x7F   # e4m3 NaN
-        p.v_pool[0] = 0x7F
+    nan_code = float("nan") if kv == "bf16" else 0x7F   # e4m3 NaN
+    for pool in (p.k_pool, p.v_pool):
+        pool[0] = nan_code
+        for b, L in enumerate(lens):
+            last, tail = int(bt[b, (L - 1) // 16]), L % 16
+            if tail:
+                if layout == "hnd":
+                    pool[last, :, tail:, :] = nan_code
+                else:
+                    pool[last, tail:, :, :] = nan_code
+    if kv != "bf16":
         p.k_scale[0] = float("nan")
         p.v_scale[0] = float("nan")
     tail = bt.clone()
