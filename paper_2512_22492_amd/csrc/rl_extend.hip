@@ -35,7 +35,9 @@ namespace {
 //
 // Work-group order: consecutive work-groups go to the eight XCDs in turn,
 // and the tiles of one (sequence, kv head) read the same keys, so they are
-// placed on one XCD (one L2) -- see the unit mapping in the kernel.
+// placed on one XCD (one L2) -- see the unit mapping in the kernel.  The
+// sequences are taken longest first (by length class), so that the longest
+// tiles do not start last and set the end of the launch.
 
 constexpr int kRowBlocks = 2;                      // 16-row blocks per wavefront
 constexpr int kTileRows = kUnitWaves * kRowBlocks * 16;
@@ -90,6 +92,70 @@ __device__ __forceinline__ float sum_lanes_xor32(float v)
     return __uint_as_float(s[0]) + __uint_as_float(s[1]);
 }
 
+// Length classes for the work-group order, longest first: class 0 holds
+// lengths of 2^15 and more, class c lengths in [2^(15-c), 2^(16-c)), class 7
+// everything below 2^9.
+constexpr int kLengthClasses = 8;
+__device__ __forceinline__ int length_class(int L)
+{
+    const int lg = 31 - __builtin_clz((unsigned)max(L, 1));
+    return min(max(15 - lg, 0), kLengthClasses - 1);
+}
+
+// The sequence at place `rank` of the batch in longest-first order (length
+// classes descending, sequence order within a class).  Every work-group
+// derives the same order from the lengths (the counts do not depend on the
+// order of the LDS atomics); called by all threads of the work-group.
+// `classes` is LDS scratch of `capacity` bytes that keeps each sequence's
+// class between the two passes (larger batches read the lengths again).
+__device__ int sequence_at_rank(const int32_t* seq_lens, int cap, int batch, int rank,
+                                uint8_t* classes, int capacity)
+{
+    __shared__ int count[kLengthClasses];
+    __shared__ int wave_hits[kUnitWaves];
+    __shared__ int pick;
+    const int t = threadIdx.x, lane = t % kWave, w = t / kWave;
+    if (t < kLengthClasses)
+        count[t] = 0;
+    __syncthreads();
+    for (int i = t; i < batch; i += kWave * kUnitWaves) {
+        const int cl = length_class(min(seq_lens[i], cap));
+        if (i < capacity)
+            classes[i] = (uint8_t)cl;
+        atomicAdd(&count[cl], 1);
+    }
+    __syncthreads();
+    int c = 0, k = rank;  // rank < batch, so some class holds it
+    while (c < kLengthClasses - 1 && k >= count[c])
+        k -= count[c++];
+    if (count[c] == batch)  // one class: sequence order
+        return rank;
+    // the k-th sequence of class c, one chunk of 256 sequences at a time
+    for (int base = 0; base < batch; base += kWave * kUnitWaves) {
+        const int i = base + t;
+        const bool hit =
+            i < batch &&
+            (i < capacity ? (int)classes[i] : length_class(min(seq_lens[i], cap))) == c;
+        const uint64_t m = __ballot(hit);
+        if (lane == 0)
+            wave_hits[w] = __popcll(m);
+        __syncthreads();
+        int before = 0, total = 0;
+#pragma unroll
+        for (int v = 0; v < kUnitWaves; ++v) {
+            before += v < w ? wave_hits[v] : 0;
+            total += wave_hits[v];
+        }
+        if (hit && before + __popcll(m & ((1ull << lane) - 1)) == k)
+            pick = i;
+        __syncthreads();
+        if (k < total)
+            break;
+        k -= total;
+    }
+    return pick;
+}
+
 struct ExtendArgs {
     const uint16_t* q;          // bf16 [T][Hq][D]
     const int32_t* q_start;     // [B+1]
@@ -140,8 +206,13 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
         bk = g / T;
         tile = g % T;
     }
+    // Pairs are taken longest sequence first, so that the longest tiles do
+    // not start last and set the end of the launch.
     const int kvh = bk % a.num_kv_heads;
-    const int b = bk / a.num_kv_heads;
+    // (the K staging buffer is free until the first stage is staged)
+    const int b = sequence_at_rank(a.seq_lens, a.max_pages * kPageSize,
+                                   (int)(gridDim.x / T / a.num_kv_heads), bk / a.num_kv_heads,
+                                   reinterpret_cast<uint8_t*>(&k_lds[0][0][0]), (int)sizeof(k_lds));
     const int q0 = a.q_start[b];
     // lengths clamped to what the table row can hold, new tokens to the length
     const int L = min(a.seq_lens[b], a.max_pages * kPageSize);

@@ -167,6 +167,33 @@ def test_extend_ignores_unstaged_memory_and_the_table_tail(kv, layout):
     assert torch.equal(got.view(torch.int16), base.view(torch.int16))
 
 
+def test_extend_longest_first_order_on_a_large_batch():
+    """Work-groups take the sequences longest first; every work-group derives
+    the order from the lengths, keeping each sequence's length class in LDS
+    for the first 36864 sequences and reading the lengths again past that.
+    A batch of 37000 sequences, nearly all empty, with real ones of six
+    length classes on both sides of that index: their rows match the oracle."""
+    batch = 37000
+    real = {5: (3000, 40), 300: (20, 5), 9000: (33000, 17), 36863: (700, 64),
+            36864: (5000, 33), 36999: (100, 1), 20000: (1, 1), 15000: (12000, 2)}
+    prior = [0] * batch
+    new = [0] * batch
+    for b, (pre, n) in real.items():
+        prior[b], new[b] = pre, n
+    p, q, q_start = extend_problem(new, prior, seed=45, hq=4, hkv=1)
+    got = run_extend(p, q, q_start, max(new))
+    rows = sorted(real)
+    sub = workloads.DecodeProblem(**{**p.__dict__, "batch": len(rows),
+                                     "block_table": p.block_table[rows].contiguous(),
+                                     "seq_lens": p.seq_lens[rows].contiguous()})
+    qs = q_start.cpu().numpy()
+    sub_q = torch.cat([q[qs[b]:qs[b + 1]] for b in rows])
+    sub_start = torch.tensor(np.concatenate([[0], np.cumsum([new[b] for b in rows])]),
+                             dtype=torch.int32, device=q.device)
+    print(check_close(bf16_to_f64(got), oracle_extend(sub, sub_q, sub_start),
+                      "longest-first, 37000 sequences", extra_abs=p_split_bound(p)))
+
+
 def test_extend_argument_validation():
     p, q, q_start = extend_problem([3, 2], [4, 4], seed=42)
     out = torch.empty_like(q)
