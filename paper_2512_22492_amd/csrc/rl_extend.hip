@@ -288,7 +288,7 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
     const int64_t st_off = (int64_t)kvh * a.head_bytes + kElt * st_col;
     uint4 kr[kRowsPerThread], vr[kRowsPerThread];  // bf16 dims or e4m3 codes
     float ksr = 1.0f, vsr = 1.0f;                  // e4m3: scales of page t % 4
-    // Key row of staging slot r and its page within the stage.
+    // Key row (within the stage) of the thread's staging slot r.
     auto slot_row = [&](int r) { return FP8 ? st_row + r : r * kPageSize + st_row; };
     // The table entries of a stage are read one stage ahead, so that its K/V
     // loads do not wait on a table load: bf16, page r of the stage for slot
