@@ -28,10 +28,13 @@ namespace {
 // group g; the V^T operand in that order comes from the [key][dim] rows by
 // the LDS transpose read.  Row max, rescale and sum are therefore lane-local
 // but for two lane swaps per 64 keys.  P enters the PV product rounded to bf16
-// (relative error at most 2^-8 per weight, as in common flash-attention
+// (relative error at most 2^-9 per weight, as in common flash-attention
 // kernels; an earlier two-term hi + lo split kept fp32-level accuracy at a
-// third more MFMAs and conversion work); l sums the unrounded fp32
-// probabilities.
+// third more MFMAs and conversion work).  For bf16 pools l is the sum of the
+// same rounded weights, taken by the PV product against a block of ones, so
+// the output is a convex combination of the values with weights off by at
+// most 2^-8 relative in total; for e4m3 pools (whose packed weights carry the
+// page's v_scale) l sums the unrounded fp32 probabilities.
 //
 // Work-group order: consecutive work-groups go to the eight XCDs in turn,
 // and the tiles of one (sequence, kv head) read the same keys, so they are
@@ -250,11 +253,19 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
     const int first_masked_stage = (base_pos + tok0) / kStageKeys;
 
     float m_run[kRowBlocks], lsum[kRowBlocks];
+    // bf16 pools: the row sums come from the PV product itself -- a block of
+    // all-ones "values" against the same bf16 probabilities -- so they sum
+    // exactly the weights the numerator uses (every lane of a row block holds
+    // its row's sum in each element).  e4m3 pools sum in lsum: their packed
+    // probabilities carry the page's v_scale.
+    floatx4_t lacc[kRowBlocks];
+    const uint4 ones_bf16 = make_uint4(0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u);
     floatx4_t o[kRowBlocks][8];
 #pragma unroll
     for (int rb = 0; rb < kRowBlocks; ++rb) {
         m_run[rb] = -INFINITY;
         lsum[rb] = 0.0f;
+        lacc[rb] = floatx4_t{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
         for (int db = 0; db < 8; ++db)
             o[rb][db] = floatx4_t{0.0f, 0.0f, 0.0f, 0.0f};
@@ -480,6 +491,9 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
                 m_run[rb] = m_new;
                 lsum[rb] *= alpha;
 #pragma unroll
+                for (int jj = 0; jj < 4; ++jj)
+                    lacc[rb][jj] *= alpha;
+#pragma unroll
                 for (int db = 0; db < 8; ++db)
 #pragma unroll
                     for (int jj = 0; jj < 4; ++jj)
@@ -498,7 +512,8 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
                 for (int jp = 0; jp < 2; ++jp) {
                     float p0 = exp2_fast(fmaf(sc[rb][kb][2 * jp], mult[kb], -m_run[rb]));
                     float p1 = exp2_fast(fmaf(sc[rb][kb][2 * jp + 1], mult[kb], -m_run[rb]));
-                    lsum[rb] += p0 + p1;
+                    if (FP8)
+                        lsum[rb] += p0 + p1;
                     if (FP8) {
                         p0 *= vsc[kb];
                         p1 *= vsc[kb];
@@ -537,6 +552,15 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
                     o[rb][db], 0, 0, 0);
             }
         }
+        if (!FP8) {
+#pragma unroll
+            for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+                for (int rb = 0; rb < kRowBlocks; ++rb)
+                    lacc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        __builtin_bit_cast(bf16x8_t, ones_bf16),
+                        __builtin_bit_cast(bf16x8_t, pt[rb][kh]), lacc[rb], 0, 0, 0);
+        }
         __builtin_amdgcn_s_setprio(0);
     };
     int j = 0;
@@ -548,7 +572,7 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
     // out[row] = O[row] / l[row]; lane holds row i16, dims 16db + 4g4 + jj.
 #pragma unroll
     for (int rb = 0; rb < kRowBlocks; ++rb) {
-        const float l = sum_lanes_xor32(sum_lanes_xor16(lsum[rb]));
+        const float l = FP8 ? sum_lanes_xor32(sum_lanes_xor16(lsum[rb])) : lacc[rb][0];
         if (!row_real[rb])
             continue;
         const int r = wave * (kRowBlocks * 16) + rb * 16 + i16;

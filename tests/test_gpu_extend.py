@@ -35,7 +35,9 @@ def run_extend(p, q, q_start, max_new):
 
 def p_split_bound(p):
     """The PV MFMA takes each probability rounded to bf16 (relative error at
-    most 2^-8 per weight) while the normaliser sums the unrounded values: the
+    most 2^-9 per weight).  bf16 pools normalise by the sum of the rounded
+    weights (the weights of the convex combination then move by at most 2^-8
+    in total), e4m3 pools by the sum of the unrounded ones: either way the
     output may move by 2^-8 * max|V| beyond the bf16 output rounding (V
     decoded with its slab scales for e4m3 pools)."""
     if p.kv_dtype == "bf16":
