@@ -102,6 +102,45 @@ def test_extend_qwen3_8b_shapes_sampled():
                     extra_abs=p_split_bound(p))
 
 
+@pytest.mark.parametrize("config,n", [("qwen3_8b_step", 512), ("fp8_large_batch", 128)])
+def test_extend_bench_workloads_sampled(config, n):
+    """The inputs `bench.py --op extend` times, built the same way (every
+    sequence gets n new tokens after its drawn length), in the same launch:
+    new tokens 0, n/2 and n-1 of the longest, the shortest and two other
+    sequences match the oracle, each as a decode query over its visible
+    prefix."""
+    cfg = dict(workloads.CONFIGS[config])
+    seed = cfg.pop("seed")
+    prior = workloads.draw_lengths(np.random.default_rng(seed), cfg["batch"], cfg["lengths"])
+    cfg["lengths"] = [int(x) + n for x in prior]
+    p = workloads.make_problem(config + "+extend", seed=seed, device=device(), **cfg)
+    T = n * p.batch
+    gen = torch.Generator(device=device()).manual_seed(seed + 1)
+    q = torch.randn((T, p.num_q_heads, p.head_dim), generator=gen,
+                    device=device()).to(torch.bfloat16)
+    q_start = torch.arange(0, T + 1, n, dtype=torch.int32, device=device())
+    got = run_extend(p, q, q_start, n)
+    assert torch.isfinite(got.float()).all()
+    h = p.host_arrays()
+    kw = {}
+    if p.kv_dtype != "bf16":
+        kw = dict(kv_dtype=oracle.KV_FP8_E4M3, k_scale=h["k_scale"], v_scale=h["v_scale"])
+    order = np.argsort(np.asarray(prior), kind="stable")
+    seqs = sorted({int(order[-1]), int(order[0]), int(order[len(order) // 3]),
+                   int(order[2 * len(order) // 3])})
+    q_bits = q.cpu().view(torch.int16).numpy().view(np.uint16)
+    for b in seqs:
+        for i in sorted({0, n // 2, n - 1}):
+            lens = h["seq_lens"].copy()
+            lens[b] = int(prior[b]) + i + 1
+            qrow = np.repeat(q_bits[b * n + i:b * n + i + 1], p.batch, axis=0)
+            ref = oracle.decode_attention(qrow, h["k_pool"], h["v_pool"], h["block_table"], lens,
+                                          num_kv_heads=p.num_kv_heads, scale=p.scale,
+                                          rows=[[b, hh] for hh in range(p.num_q_heads)], **kw)
+            check_close(bf16_to_f64(got[b * n + i]), ref, "%s b=%d i=%d" % (config, b, i),
+                        extra_abs=p_split_bound(p))
+
+
 def test_extend_ignores_unread_memory_and_is_causal():
     new, prior = [20, 5], [13, 40]
     p, q, q_start = extend_problem(new, prior, seed=41)
