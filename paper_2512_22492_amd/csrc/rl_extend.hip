@@ -386,8 +386,9 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
         __syncthreads();
 
         // Score multiplier (scale * log2 e, times k_scale) and value scale
-        // of the stage's four pages; pages past the sequence get 1 (their
-        // keys are masked and their values staged as zeros).
+        // of the stage's four pages; a page past the sequence carries the
+        // finite scales of the page its index was clamped to (its keys are
+        // masked and its values staged as zeros).
         float sl[4], vsc[4];
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb) {
