@@ -5,10 +5,12 @@ A step is one rl_decode_attn_run() (split-K kernel + merge kernel) over one
 batch.  Inputs are seeded synthetic tensors resident in HBM before timing
 starts.  Prints one JSON line:
   value      = KV bytes read per step / step time  (GB/s, the metric's unit)
-  roofline   = the split-K kernel's achieved bytes/s against 8 TB/s, timed
-               live with HIP events recorded around each of its launches in
-               a second pass of K steps (the events stay out of the first)
+  roofline   = the split-K kernel's achieved bytes/s against 8 TB/s: the
+               step's algorithmic bytes over the kernel's mean duration, from
+               HIP events attached to each of its launches in a second pass
+               of K steps (the first pass, which gives value, has none)
   cpu_baseline = the fp64 oracle timed on the host on a sample of the step
+  parity     = the GPU output of that sample against the oracle's
 """
 import argparse
 import json
@@ -195,14 +197,16 @@ def summarize_pmc(fetch_csv, write_csv, config, op="attention"):
 
 
 def algorithmic_bytes(p):
-    """Bytes the split-K kernel must move: K and V of every cached token (plus
-    fp8 slab scales), the queries, the used block-table entries, seq_lens."""
+    """Bytes one decode step must move: K and V of every cached token (plus
+    fp8 slab scales), the queries, the outputs, the used block-table entries
+    and seq_lens.  Returns (total, KV part)."""
     import numpy as np
     L = np.clip(p.lengths(), 0, None)
     pages = (L + p.page_size - 1) // p.page_size
     kv = p.kv_bytes()
     q = p.batch * p.num_q_heads * p.head_dim * 2
-    return kv + q + int(pages.sum()) * 4 + p.batch * 4, kv
+    out = q
+    return kv + q + out + int(pages.sum()) * 4 + p.batch * 4, kv
 
 
 def load_traffic(config, kernel_source_sha):
@@ -227,9 +231,47 @@ def kernel_source_sha(op="attention"):
     return h.hexdigest()
 
 
-def cpu_baseline(p, min_seconds=10.0):
-    """Times the oracle on the host.  The sample is the whole step (every
-    (sequence, head) row) when that is bounded, else the first sequences."""
+def _bf16_ulp(x):
+    """Spacing of bf16 numbers at |x| (8 significant bits)."""
+    import numpy as np
+    a = np.abs(x)
+    with np.errstate(divide="ignore"):
+        e = np.floor(np.log2(np.where(a > 0, a, 1.0)))
+    return np.where(a > 0, np.exp2(np.maximum(e, -126) - 7), 0.0)
+
+
+def parity_stats(got, ref):
+    """Error of the GPU's bf16 output against the fp64 oracle: the official
+    bound (|err| <= 1e-2 + 1e-2 |ref|), max |err|, max error in bf16 ulps of
+    the reference, the fraction of elements equal to the correctly rounded
+    reference, and the relative RMS error."""
+    import numpy as np
+    import torch
+    err = np.abs(got - ref)
+    ulp = _bf16_ulp(ref)
+    with np.errstate(invalid="ignore", divide="ignore"):
+        ulps = np.where(ulp > 0, err / ulp, 0.0)
+    rne = torch.from_numpy(ref).float().to(torch.bfloat16).double().numpy()
+    rms = float(np.sqrt(np.mean(ref * ref)))
+    return {
+        "elements": int(err.size),
+        "official_bound_holds": bool(np.all(err <= 1e-2 + 1e-2 * np.abs(ref))),
+        "max_abs_err": float(err.max()),
+        "max_ulp": round(float(ulps.max()), 4),
+        "frac_rne_equal": round(float(np.mean(got == rne)), 6),
+        "rel_rms_err": float(np.sqrt(np.mean(err * err))) / rms if rms > 0 else 0.0,
+    }
+
+
+def cpu_baseline(p, gpu_out, min_seconds=10.0):
+    """Times the oracle on the host, built for this host (-O3 -march=native,
+    no FMA contraction: the same results as the test build).  The sample is
+    the whole step (every (sequence, head) row) when that is bounded, else
+    the first sequences.  The oracle's output of the sample also gives the
+    GPU output's error statistics."""
+    import shutil
+    import tempfile
+
     import numpy as np
     import oracle
     kv_code = oracle.KV_BF16 if p.kv_dtype == "bf16" else oracle.KV_FP8_E4M3
@@ -241,26 +283,38 @@ def cpu_baseline(p, min_seconds=10.0):
     nseq = max(1, min(p.batch, nseq))
     rows = np.array([(b, hh) for b in range(nseq) for hh in range(p.num_q_heads)],
                     dtype=np.int32)
-    # repeat the sample until about min_seconds of CPU work have been timed
-    reps, dt = 0, 0.0
-    while reps == 0 or dt < min_seconds:
-        t0 = time.perf_counter()
-        oracle.decode_attention(kv_dtype=kv_code, rows=rows, **h)
-        dt += time.perf_counter() - t0
-        reps += 1
+    tmp = tempfile.mkdtemp(prefix="oracle_native_")
+    try:
+        try:
+            lib, build = oracle.build_native(tmp), "gcc -O3 -march=native -ffp-contract=off -fopenmp"
+        except Exception as e:  # no compiler on this host: the portable build
+            print("bench: native oracle build failed (%s); timing the portable build" % e,
+                  file=sys.stderr, flush=True)
+            lib, build = oracle.LIB_PATH, "gcc -O2 -ffp-contract=off -fopenmp (portable)"
+        with oracle.using_library(lib):
+            # repeat the sample until about min_seconds of CPU work have been timed
+            reps, dt, ref = 0, 0.0, None
+            while reps == 0 or dt < min_seconds:
+                t0 = time.perf_counter()
+                ref = oracle.decode_attention(kv_dtype=kv_code, rows=rows, **h)
+                dt += time.perf_counter() - t0
+                reps += 1
+            cores = oracle.max_threads()
+            # one thread, on the first sequence's rows (a few seconds)
+            rows1 = rows[:p.num_q_heads]
+            oracle.set_threads(1)
+            try:
+                t0 = time.perf_counter()
+                oracle.decode_attention(kv_dtype=kv_code, rows=rows1, **h)
+                dt1 = time.perf_counter() - t0
+            finally:
+                oracle.set_threads(cores)
+    finally:
+        shutil.rmtree(tmp, ignore_errors=True)
     elt = 2 if p.kv_dtype == "bf16" else 1
     kv = int(L[:nseq].sum()) * p.num_kv_heads * p.head_dim * 2 * elt * reps
-    cores = oracle.max_threads()
-    # one thread, on the first sequence's rows (a few seconds)
-    rows1 = rows[:p.num_q_heads]
-    oracle.set_threads(1)
-    try:
-        t0 = time.perf_counter()
-        oracle.decode_attention(kv_dtype=kv_code, rows=rows1, **h)
-        dt1 = time.perf_counter() - t0
-    finally:
-        oracle.set_threads(cores)
     kv1 = int(L[0]) * p.num_kv_heads * p.head_dim * 2 * elt
+    got = gpu_out[:nseq].float().cpu().numpy().astype(np.float64).reshape(ref.shape)
     return {
         "value": kv / dt / 1e9,
         "unit": "GB/s",
@@ -269,21 +323,37 @@ def cpu_baseline(p, min_seconds=10.0):
         "sample": "%d of %d sequences (%d query-head rows, all tokens), fp64, %d passes "
                   "in %.2f s; %.1f query-tokens/s" % (nseq, p.batch, len(rows), reps, dt,
                                                      nseq * reps / dt),
+        "build": build,
         "single_thread_GBs": round(kv1 / dt1 / 1e9, 4),
+        "single_thread_sample": "sequence 0 (%d tokens, %d query heads), 1 pass"
+                                % (int(L[0]), p.num_q_heads),
         "cpu_model": _cpu_model(),
         "seconds": dt,
-    }
+    }, parity_stats(got, ref)
 
 
 def _cpu_model():
+    """The host CPU as /proc/cpuinfo names it: model name, family, model,
+    stepping, and the logical CPUs this process may run on."""
+    info = {}
     try:
         with open("/proc/cpuinfo") as f:
             for line in f:
-                if line.startswith("model name"):
-                    return line.split(":", 1)[1].strip()
+                if ":" not in line:
+                    if info:
+                        break
+                    continue
+                k, v = (x.strip() for x in line.split(":", 1))
+                if k in ("vendor_id", "model name", "cpu family", "model", "stepping",
+                         "cpu MHz") and k not in info:
+                    info[k] = v
     except OSError:
-        pass
-    return None
+        return None
+    try:
+        info["usable_cpus"] = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        info["usable_cpus"] = os.cpu_count()
+    return info
 
 
 def input_digests(p):
@@ -596,22 +666,27 @@ def main():
     torch.cuda.synchronize()
     t1 = time.perf_counter()
 
-    # Second timed pass of K steps with HIP events recorded on the stream just
-    # before and after every split-kernel launch (the events cost a few us per
-    # step, so they stay out of the first pass).
+    # Second timed pass of K steps whose split-kernel launches carry HIP
+    # events attached to the launch itself (hipExtLaunchKernel): each pair
+    # holds that kernel's own start and end.  Its wall time bounds the sum of
+    # the kernel times from above.
     split_ms = None
+    pass2_ms = None
     if not args.no_kernel_events:
+        t2 = time.perf_counter()
         for i in range(args.steps):
             binding.rl_decode_attn_set_timing_events(attn.handle, ev_b[i].cuda_event,
                                                      ev_e[i].cuda_event)
             attn.run_problem(replicas[i % len(replicas)], out, stream)
         torch.cuda.synchronize()
+        pass2_ms = (time.perf_counter() - t2) * 1e3 / args.steps
         binding.rl_decode_attn_set_timing_events(attn.handle, None, None)
         split_ms = np.array([b.elapsed_time(e) for b, e in zip(ev_b, ev_e)])
 
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     alg_bytes, kv_bytes = algorithmic_bytes(base)
     value = kv_bytes / (ms_per_step / 1e3) / 1e9
+    seed = workloads.CONFIGS[args.config]["seed"]
     record = {
         "metric": "decode-attention KV-read GB/s (fraction of HBM peak) + query-tokens/s, 1 GPU",
         "value": round(value, 2),
@@ -627,6 +702,7 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": "%s: %s" % (args.config, workloads.describe(args.config)),
+            "seed": seed,
             "batch": base.batch, "num_q_heads": base.num_q_heads,
             "num_kv_heads": base.num_kv_heads, "head_dim": base.head_dim,
             "page_size": base.page_size, "seq_len_mean": float(base.lengths().mean()),
@@ -643,6 +719,9 @@ def main():
         record["config"]["input_sha256_16"] = input_digests(base)
     if split_ms is not None:
         avg = float(split_ms.mean())
+        # every kernel runs inside its step, so the mean kernel time cannot
+        # exceed the pass's mean step time
+        assert avg <= pass2_ms * (1 + 1e-6), (avg, pass2_ms)
         achieved = alg_bytes / (avg / 1e3) / 1e9
         record["roofline"] = {
             "bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
@@ -652,6 +731,8 @@ def main():
             "min_us": round(float(split_ms.min()) * 1e3, 2),
             "p10_p50_p90_us": [round(float(x) * 1e3, 2)
                                for x in np.percentile(split_ms, [10, 50, 90])],
+            "step_us_same_pass": round(pass2_ms * 1e3, 2),
+            "avg_le_ms_per_step": bool(avg <= ms_per_step),
             "bytes_per_launch": alg_bytes,
         }
     attn.close()
@@ -666,10 +747,15 @@ def main():
                 record["roofline"]["achieved"] / ceil["page_read_GBs"], 4)
     if not args.no_cpu_baseline:
         print("bench: timing the CPU oracle", file=sys.stderr, flush=True)
-        record["cpu_baseline"] = cpu_baseline(base)
+        # the output of the last timed step, from the first replica's inputs
+        attn = binding.DecodeAttention.for_problem(base, flags=flags,
+                                                   split_tokens=args.split_tokens)
+        attn.run_problem(base, out, stream)
+        torch.cuda.synchronize()
+        attn.close()
+        record["cpu_baseline"], record["parity"] = cpu_baseline(base, out)
         del record["cpu_baseline"]["seconds"]
     print(json.dumps(record), flush=True)
-
 
 if __name__ == "__main__":
     main()

@@ -31,16 +31,26 @@
  * Execution.  run() enqueues its kernels on the caller's HIP stream and
  * returns without synchronising; the result is ready when the stream has
  * reached that point.  run() never allocates: the handle owns a workspace
- * sized at create() for max_batch and max_pages_per_seq.  One handle must not
- * be used by two runs that can overlap (two streams); use one handle per
- * stream.  Results are deterministic: no atomics take part in any reduction,
- * the split size is fixed per handle and partial results merge in a fixed
- * order, so a sequence's output does not depend on the rest of the batch or
- * on where its pages sit in the pool.  With several splits per sequence and
- * more work units than the device holds at once, the split kernel runs
- * persistent work-groups that take units, longest first, from a counter in
- * the handle's workspace (the last work-group resets it); which work-group
+ * sized at create() for max_batch and max_pages_per_seq.  Results are
+ * deterministic: no atomics take part in any reduction, the split size is
+ * fixed per handle and partial results merge in a fixed order, so a
+ * sequence's output does not depend on the rest of the batch or on where its
+ * pages sit in the pool.  With several splits per sequence and more work
+ * units than the device holds at once, the split kernel runs persistent
+ * work-groups that take units, longest first, from a counter in the handle's
+ * workspace (the last work-group of each launch resets it); which work-group
  * computes a unit never changes a result.
+ *
+ * Concurrency.  The runs of one handle share its workspace: the per-split
+ * partial results, the persistent schedule's unit counter and the error
+ * word.  They must therefore be ordered on one stream (or otherwise never
+ * overlap); two runs of one handle that overlap on two streams race on all
+ * three and give wrong outputs without any error.  Use one handle per
+ * stream; different handles never share state.  A run that returned
+ * RL_DA_ERR_HIP, or whose stream later reports an error, may have stopped
+ * with the unit counter not reset: destroy the handle and create a new one
+ * before running again (after a device fault the HIP context itself is
+ * unusable and must be re-created first).
  *
  * Errors.  Every entry point returns an rl_da_status; nothing is thrown
  * across the interface.  run() checks its host-visible arguments and returns
@@ -159,8 +169,10 @@ rl_da_status rl_decode_attn_workspace_size(const rl_da_config* cfg,
                                            size_t* bytes);
 
 /*
- * Checked handles only: synchronises the device, stores the accumulated
- * RL_DA_DEVERR_* bits in *device_error and clears them.  UNSUPPORTED for a
+ * Checked handles only: waits for the stream of the handle's latest run()
+ * (only that stream; other work on the device is not waited for), stores the
+ * RL_DA_DEVERR_* bits accumulated since the previous call in *device_error
+ * and clears them with a kernel enqueued on that stream.  UNSUPPORTED for a
  * handle created without RL_DA_CHECKED.
  */
 rl_da_status rl_decode_attn_check_error(rl_decode_attn* h, int32_t* device_error);
@@ -243,10 +255,12 @@ rl_da_status rl_kv_append(const void* k_new, const void* v_new, void* k_pool, vo
 
 /*
  * Measurement hook (no counterpart in the paper): with both events non-NULL,
- * every later run() records split_begin on its stream just before the split-K
- * kernel and split_end just after it, so hipEventElapsedTime gives that
- * kernel's duration.  Events are hipEvent_t owned by the caller; NULL, NULL
- * turns recording off.  INVALID_ARG if exactly one event is NULL.
+ * every later run() launches its split-K kernel with split_begin and
+ * split_end attached to the launch itself (hipExtLaunchKernel), so they take
+ * that kernel's start and end timestamps and hipEventElapsedTime gives its
+ * duration, with nothing inserted between the launches of a step.  Events
+ * are hipEvent_t owned by the caller; NULL, NULL turns recording off.
+ * INVALID_ARG if exactly one event is NULL.
  */
 rl_da_status rl_decode_attn_set_timing_events(rl_decode_attn* h, void* split_begin,
                                               void* split_end);

@@ -52,6 +52,38 @@ def build(force: bool = True) -> str:
     return LIB_PATH
 
 
+def build_native(directory: str) -> str:
+    """Compile the same source with -O3 -march=native (still no FMA
+    contraction, so every result is bit-identical to the portable build) into
+    `directory`, for timing the oracle on the host it runs on.  Returns the
+    library path."""
+    os.makedirs(directory, exist_ok=True)
+    path = os.path.join(directory, "libdecode_attn_oracle_native.so")
+    cmd = ["gcc", "-O3", "-march=native", "-std=c11", "-Wall", "-Wextra", "-fopenmp",
+           "-ffp-contract=off", "-fPIC", "-shared", _SRC, "-o", path, "-lm"]
+    subprocess.run(cmd, check=True)
+    return path
+
+
+class using_library:
+    """Context manager: oracle calls inside it go to the library at `path`
+    (for instance a build_native() build)."""
+
+    def __init__(self, path: str):
+        self.path = path
+        self.saved = None
+
+    def __enter__(self):
+        self.saved = _lib
+        _load_path(self.path)
+        return self
+
+    def __exit__(self, *exc):
+        global _lib
+        _lib = self.saved
+        return False
+
+
 class _Append(ctypes.Structure):
     _fields_ = [
         ("batch", ctypes.c_int32),
@@ -106,25 +138,32 @@ def _load():
         path = os.environ.get("RL_ORACLE_LIB") or LIB_PATH
         if path == LIB_PATH and not os.path.exists(LIB_PATH):
             build()
-        lib = ctypes.CDLL(path)
-        lib.rl_oracle_decode_attn.argtypes = [
-            ctypes.POINTER(_Problem), ctypes.c_void_p, ctypes.c_int64,
-            ctypes.c_void_p]
-        lib.rl_oracle_decode_attn.restype = ctypes.c_int
-        lib.rl_oracle_e4m3_to_double.argtypes = [ctypes.c_uint8]
-        lib.rl_oracle_e4m3_to_double.restype = ctypes.c_double
-        lib.rl_oracle_bf16_to_double.argtypes = [ctypes.c_uint16]
-        lib.rl_oracle_bf16_to_double.restype = ctypes.c_double
-        lib.rl_oracle_extend_attn.argtypes = [ctypes.POINTER(_Problem), ctypes.c_void_p,
-                                              ctypes.c_void_p]
-        lib.rl_oracle_extend_attn.restype = ctypes.c_int
-        lib.rl_oracle_kv_append.argtypes = [ctypes.POINTER(_Append)]
-        lib.rl_oracle_kv_append.restype = ctypes.c_int
-        lib.rl_oracle_e4m3_encode.argtypes = [ctypes.c_float]
-        lib.rl_oracle_e4m3_encode.restype = ctypes.c_uint8
-        lib.rl_oracle_max_threads.argtypes = []
-        lib.rl_oracle_max_threads.restype = ctypes.c_int
-        _lib = lib
+        _load_path(path)
+    return _lib
+
+
+def _load_path(path):
+    """Loads the oracle library at `path` as the one later calls use."""
+    global _lib
+    lib = ctypes.CDLL(path)
+    lib.rl_oracle_decode_attn.argtypes = [
+        ctypes.POINTER(_Problem), ctypes.c_void_p, ctypes.c_int64,
+        ctypes.c_void_p]
+    lib.rl_oracle_decode_attn.restype = ctypes.c_int
+    lib.rl_oracle_e4m3_to_double.argtypes = [ctypes.c_uint8]
+    lib.rl_oracle_e4m3_to_double.restype = ctypes.c_double
+    lib.rl_oracle_bf16_to_double.argtypes = [ctypes.c_uint16]
+    lib.rl_oracle_bf16_to_double.restype = ctypes.c_double
+    lib.rl_oracle_extend_attn.argtypes = [ctypes.POINTER(_Problem), ctypes.c_void_p,
+                                          ctypes.c_void_p]
+    lib.rl_oracle_extend_attn.restype = ctypes.c_int
+    lib.rl_oracle_kv_append.argtypes = [ctypes.POINTER(_Append)]
+    lib.rl_oracle_kv_append.restype = ctypes.c_int
+    lib.rl_oracle_e4m3_encode.argtypes = [ctypes.c_float]
+    lib.rl_oracle_e4m3_encode.restype = ctypes.c_uint8
+    lib.rl_oracle_max_threads.argtypes = []
+    lib.rl_oracle_max_threads.restype = ctypes.c_int
+    _lib = lib
     return _lib
 
 

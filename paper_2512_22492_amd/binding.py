@@ -184,6 +184,65 @@ def _stream(s):
     return s.cuda_stream
 
 
+def _pool_shape(layout, num_pages, num_kv_heads, page_size, head_dim):
+    if layout == "nhd":
+        return (num_pages, page_size, num_kv_heads, head_dim)
+    return (num_pages, num_kv_heads, page_size, head_dim)
+
+
+def _check_tensor(name, t, *, dtype=None, shape=None, ndim=None, device=None):
+    """Raises ValueError unless t is a contiguous torch tensor of the given
+    dtype, shape (None entries match anything) and device."""
+    if not hasattr(t, "data_ptr") or not hasattr(t, "is_contiguous"):
+        raise ValueError("%s must be a torch tensor" % name)
+    if dtype is not None and t.dtype not in (dtype if isinstance(dtype, tuple) else (dtype,)):
+        raise ValueError("%s has dtype %s, expected %s" % (name, t.dtype, dtype))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError("%s must have %d dimensions, has shape %s" % (name, ndim, tuple(t.shape)))
+    if shape is not None:
+        if t.dim() != len(shape) or any(w is not None and int(d) != int(w)
+                                        for d, w in zip(t.shape, shape)):
+            raise ValueError("%s has shape %s, expected %s"
+                             % (name, tuple(t.shape), tuple("*" if w is None else w
+                                                            for w in shape)))
+    if device is not None and t.device != device:
+        raise ValueError("%s is on %s, expected %s" % (name, t.device, device))
+
+
+def _check_pools(k_pool, v_pool, k_scale, v_scale, *, kv_dtype, layout, num_kv_heads,
+                 head_dim, page_size, device):
+    """The pools' dtype (bf16 or uint8 e4m3 codes), layout shape and device;
+    fp32 [num_pages, num_kv_heads] scales exactly for e4m3.  Returns num_pages."""
+    import torch
+    elt = torch.bfloat16 if kv_dtype == RL_DA_KV_BF16 else torch.uint8
+    _check_tensor("k_pool", k_pool, dtype=elt, ndim=4, device=device)
+    P = int(k_pool.shape[0])
+    want = _pool_shape("nhd" if layout == RL_DA_LAYOUT_NHD else "hnd", P, num_kv_heads,
+                       page_size, head_dim)
+    _check_tensor("k_pool", k_pool, shape=want)
+    _check_tensor("v_pool", v_pool, dtype=elt, shape=want, device=device)
+    if kv_dtype == RL_DA_KV_BF16:
+        if k_scale is not None or v_scale is not None:
+            raise ValueError("bf16 pools take no k_scale / v_scale")
+    else:
+        _check_tensor("k_scale", k_scale, dtype=torch.float32, shape=(P, num_kv_heads),
+                      device=device)
+        _check_tensor("v_scale", v_scale, dtype=torch.float32, shape=(P, num_kv_heads),
+                      device=device)
+    return P
+
+
+def _check_table(block_table, seq_lens, batch, device):
+    import torch
+    _check_tensor("block_table", block_table, dtype=torch.int32, ndim=2, device=device)
+    if int(block_table.shape[0]) != batch:
+        raise ValueError("block_table has %d rows for a batch of %d"
+                         % (block_table.shape[0], batch))
+    _check_tensor("seq_lens", seq_lens, dtype=torch.int32, shape=(batch,), device=device)
+
+
 def make_config(num_q_heads, num_kv_heads, max_batch, max_pages_per_seq, *,
                 head_dim=128, page_size=16, kv_dtype=RL_DA_KV_BF16,
                 layout=RL_DA_LAYOUT_HND, split_tokens=0, flags=0) -> rl_da_config:
@@ -257,7 +316,17 @@ def rl_extend_attn(q, q_start, max_q_per_seq, k_pool, v_pool, k_scale, v_scale, 
 def extend_attention(p, q, q_start, max_q_per_seq, out, stream=None):
     """Extend attention of new tokens q [T, Hq, D] (rows q_start[b]..) over
     problem p's cache (p.seq_lens include the new tokens); raises on error."""
+    import torch
     dt = RL_DA_KV_BF16 if p.kv_dtype == "bf16" else RL_DA_KV_FP8_E4M3
+    dev = p.k_pool.device
+    _check_tensor("q", q, dtype=torch.bfloat16, shape=(None, p.num_q_heads, p.head_dim),
+                  device=dev)
+    _check_tensor("out", out, dtype=torch.bfloat16, shape=tuple(q.shape), device=dev)
+    _check_tensor("q_start", q_start, dtype=torch.int32, shape=(p.batch + 1,), device=dev)
+    _check_pools(p.k_pool, p.v_pool, p.k_scale, p.v_scale, kv_dtype=dt,
+                 layout=LAYOUTS[p.layout], num_kv_heads=p.num_kv_heads, head_dim=p.head_dim,
+                 page_size=p.page_size, device=dev)
+    _check_table(p.block_table, p.seq_lens, p.batch, dev)
     rc = rl_extend_attn(q, q_start, max_q_per_seq, p.k_pool, p.v_pool, p.k_scale, p.v_scale,
                         p.num_pages, p.block_table, p.max_pages, p.seq_lens, p.batch,
                         p.num_q_heads, p.num_kv_heads, p.head_dim, p.page_size, dt,
@@ -280,7 +349,18 @@ def rl_kv_append(k_new, v_new, k_pool, v_pool, k_scale, v_scale, num_pages, bloc
 def kv_append(p, k_new, v_new, device_error=None, stream=None):
     """Appends k_new/v_new [B, Hkv, D] (bf16 tensors) to problem p's pools at
     positions p.seq_lens; raises on a bad status."""
+    import torch
     dt = RL_DA_KV_BF16 if p.kv_dtype == "bf16" else RL_DA_KV_FP8_E4M3
+    dev = p.k_pool.device
+    want = (p.batch, p.num_kv_heads, p.head_dim)
+    _check_tensor("k_new", k_new, dtype=torch.bfloat16, shape=want, device=dev)
+    _check_tensor("v_new", v_new, dtype=torch.bfloat16, shape=want, device=dev)
+    _check_pools(p.k_pool, p.v_pool, p.k_scale, p.v_scale, kv_dtype=dt,
+                 layout=LAYOUTS[p.layout], num_kv_heads=p.num_kv_heads, head_dim=p.head_dim,
+                 page_size=p.page_size, device=dev)
+    _check_table(p.block_table, p.seq_lens, p.batch, dev)
+    if device_error is not None:
+        _check_tensor("device_error", device_error, dtype=torch.int32, device=dev)
     rc = rl_kv_append(k_new, v_new, p.k_pool, p.v_pool, p.k_scale, p.v_scale, p.num_pages,
                       p.block_table, p.max_pages, p.seq_lens, p.batch, p.num_kv_heads,
                       p.head_dim, p.page_size, dt, LAYOUTS[p.layout], device_error, stream)
@@ -417,6 +497,9 @@ class DecodeAttention:
         if rc != RL_DA_OK:
             raise RLDecodeAttnError(rc, "rl_decode_attn_create")
         self.handle = h
+        import torch
+        # the library creates the handle on the current device
+        self.device = torch.device("cuda", torch.cuda.current_device())
 
     @classmethod
     def for_problem(cls, p, **kw):
@@ -425,6 +508,18 @@ class DecodeAttention:
 
     def run(self, q, k_pool, v_pool, k_scale, v_scale, block_table, seq_lens, scale, out,
             stream=None):
+        """Checks every tensor (dtype, contiguity, device, shapes that agree
+        with the handle) before the C call; raises ValueError otherwise."""
+        import torch
+        c = self.cfg
+        dev = self.device
+        _check_tensor("q", q, dtype=torch.bfloat16, shape=(None, c.num_q_heads, c.head_dim),
+                      device=dev)
+        _check_tensor("out", out, dtype=torch.bfloat16, shape=tuple(q.shape), device=dev)
+        _check_pools(k_pool, v_pool, k_scale, v_scale, kv_dtype=c.kv_dtype, layout=c.layout,
+                     num_kv_heads=c.num_kv_heads, head_dim=c.head_dim,
+                     page_size=c.page_size, device=dev)
+        _check_table(block_table, seq_lens, int(q.shape[0]), dev)
         rc = rl_decode_attn_run(self.handle, q, k_pool, v_pool, k_scale, v_scale,
                                 k_pool.shape[0], block_table, block_table.shape[1],
                                 seq_lens, q.shape[0], scale, out, stream)

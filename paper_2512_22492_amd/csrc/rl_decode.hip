@@ -1346,6 +1346,7 @@ struct rl_decode_attn {
     float* ws_ml;
     int32_t* dev_error;
     int32_t* queue;  // persistent runs: next unit, finished work-groups
+    hipStream_t last_stream;  // stream of the latest run (check_error waits on it)
     hipEvent_t ev_split_begin;
     hipEvent_t ev_split_end;
 };
@@ -1392,8 +1393,11 @@ rl_da_status check_config(const rl_da_config* cfg, int* split_tokens, int* split
 }
 
 // Workspace: per-split partial accumulators and (m, l) pairs, then one
-// 256-byte block for the device error word (offset 0) and the persistent
-// launch's unit queue (offset 128).
+// 256-byte control block: the device error word (offset 0) and the
+// persistent launch's unit queue (offset 128).
+constexpr size_t kControlBytes = 256;
+constexpr int kQueueWord = 32;  // int32 index of the queue in the control block
+
 size_t partials_bytes(const rl_da_config* cfg, int max_splits)
 {
     const size_t rows = (size_t)cfg->max_batch * (size_t)cfg->num_q_heads * (size_t)max_splits;
@@ -1404,49 +1408,26 @@ size_t partials_bytes(const rl_da_config* cfg, int max_splits)
 
 size_t workspace_bytes_for(const rl_da_config* cfg, int max_splits)
 {
-    return partials_bytes(cfg, max_splits) + 256;
+    return partials_bytes(cfg, max_splits) + kControlBytes;
 }
 
-}  // namespace
-
-extern "C" {
-
-const char* rl_da_status_string(rl_da_status s)
+// Zeroes n int32 words on a stream (a kernel rather than a memset node, so
+// that the clear can sit in a captured graph).
+__global__ __launch_bounds__(64) void clear_words(int32_t* p, int n)
 {
-    switch (s) {
-    case RL_DA_OK: return "ok";
-    case RL_DA_ERR_INVALID_ARG: return "invalid argument";
-    case RL_DA_ERR_UNSUPPORTED: return "unsupported configuration";
-    case RL_DA_ERR_OUT_OF_MEMORY: return "out of device memory";
-    case RL_DA_ERR_HIP: return "HIP runtime error";
-    }
-    return "unknown status";
+    for (int i = threadIdx.x; i < n; i += blockDim.x)
+        p[i] = 0;
 }
 
-rl_da_status rl_decode_attn_workspace_size(const rl_da_config* cfg, size_t* bytes)
+// Everything a handle holds except its workspace: the validated
+// configuration, the split geometry, the kernels and their resident
+// work-group counts on the current device.  Allocates nothing.
+rl_da_status init_handle(rl_decode_attn* h, const rl_da_config* cfg)
 {
-    int st, sp, ms;
-    if (bytes == nullptr)
-        return RL_DA_ERR_INVALID_ARG;
-    const rl_da_status rc = check_config(cfg, &st, &sp, &ms);
-    if (rc != RL_DA_OK)
-        return rc;
-    *bytes = workspace_bytes_for(cfg, ms);
-    return RL_DA_OK;
-}
-
-rl_da_status rl_decode_attn_create(const rl_da_config* cfg, rl_decode_attn** out)
-{
-    if (out == nullptr)
-        return RL_DA_ERR_INVALID_ARG;
-    *out = nullptr;
     int st, sp, ms;
     const rl_da_status rc = check_config(cfg, &st, &sp, &ms);
     if (rc != RL_DA_OK)
         return rc;
-    rl_decode_attn* h = (rl_decode_attn*)calloc(1, sizeof(rl_decode_attn));
-    if (h == nullptr)
-        return RL_DA_ERR_OUT_OF_MEMORY;
     h->cfg = *cfg;
     h->split_tokens = st;
     h->split_pages = sp;
@@ -1459,83 +1440,68 @@ rl_da_status rl_decode_attn_create(const rl_da_config* cfg, rl_decode_attn** out
         (persistent ? h->split_kernel_persistent : h->split_kernel) = select_split_kernel(
             G, (cfg->flags & RL_DA_CHECKED) != 0, cfg->kv_dtype == RL_DA_KV_FP8_E4M3, h->use_mfma,
             h->head_parallel, persistent != 0);
-    if (hipGetDevice(&h->device) != hipSuccess) {
-        free(h);
+    if (hipGetDevice(&h->device) != hipSuccess)
         return RL_DA_ERR_HIP;
-    }
     // One persistent work-group per slot that can be resident with the
     // largest plan this handle can need; and how many one-unit work-groups
     // the static grid keeps resident.
-    {
-        const int threads = h->head_parallel ? kWave * h->heads_per_unit : kWave * kUnitWaves;
-        const int plan_batch = cfg->max_batch < kMaxPlanBatch ? cfg->max_batch : kMaxPlanBatch;
-        const size_t lds = (size_t)plan_ints(plan_batch) * sizeof(int);
-        int per_cu = 0, static_per_cu = 0, cus = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                &per_cu, reinterpret_cast<const void*>(h->split_kernel_persistent), threads,
-                lds) != hipSuccess ||
-            hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                &static_per_cu, reinterpret_cast<const void*>(h->split_kernel), threads, 0) !=
-                hipSuccess ||
-            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device) !=
-                hipSuccess ||
-            per_cu < 1 || static_per_cu < 1 || cus < 1) {
-            (void)hipGetLastError();
-            free(h);
-            return RL_DA_ERR_HIP;
-        }
-        h->persistent_grid = per_cu * cus;
-        h->static_slots = static_per_cu * cus;
-    }
-    h->workspace_bytes = workspace_bytes_for(cfg, ms);
-    if (hipMalloc(&h->workspace, h->workspace_bytes) != hipSuccess) {
+    const int threads = h->head_parallel ? kWave * h->heads_per_unit : kWave * kUnitWaves;
+    const int plan_batch = cfg->max_batch < kMaxPlanBatch ? cfg->max_batch : kMaxPlanBatch;
+    const size_t lds = (size_t)plan_ints(plan_batch) * sizeof(int);
+    int per_cu = 0, static_per_cu = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &per_cu, reinterpret_cast<const void*>(h->split_kernel_persistent), threads, lds) !=
+            hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &static_per_cu, reinterpret_cast<const void*>(h->split_kernel), threads, 0) !=
+            hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device) !=
+            hipSuccess ||
+        per_cu < 1 || static_per_cu < 1 || cus < 1) {
         (void)hipGetLastError();
-        free(h);
-        return RL_DA_ERR_OUT_OF_MEMORY;
-    }
-    const size_t rows = (size_t)cfg->max_batch * (size_t)cfg->num_q_heads * (size_t)ms;
-    h->ws_acc = (float*)h->workspace;
-    h->ws_ml = h->ws_acc + rows * kHeadDim;
-    h->dev_error = (int32_t*)((char*)h->workspace + h->workspace_bytes - 256);
-    h->queue = h->dev_error + 32;
-    if (hipMemset(h->dev_error, 0, 256) != hipSuccess) {
-        (void)hipFree(h->workspace);
-        free(h);
         return RL_DA_ERR_HIP;
     }
-    *out = h;
+    h->persistent_grid = per_cu * cus;
+    h->static_slots = static_per_cu * cus;
+    h->workspace_bytes = workspace_bytes_for(cfg, ms);
     return RL_DA_OK;
 }
 
-rl_da_status rl_decode_attn_destroy(rl_decode_attn* h)
+// Points the handle at a workspace of h->workspace_bytes bytes.
+void bind_workspace(rl_decode_attn* h, void* ws)
 {
-    if (h == nullptr)
-        return RL_DA_OK;
-    const hipError_t e = hipFree(h->workspace);
-    free(h);
-    return e == hipSuccess ? RL_DA_OK : RL_DA_ERR_HIP;
+    const size_t rows =
+        (size_t)h->cfg.max_batch * (size_t)h->cfg.num_q_heads * (size_t)h->max_splits;
+    h->workspace = ws;
+    h->ws_acc = (float*)ws;
+    h->ws_ml = h->ws_acc + rows * kHeadDim;
+    h->dev_error = (int32_t*)((char*)ws + h->workspace_bytes - kControlBytes);
+    h->queue = h->dev_error + kQueueWord;
 }
 
-rl_da_status rl_decode_attn_split_info(const rl_decode_attn* h, int32_t max_pages,
-                                       int32_t* split_tokens, int32_t* num_splits)
+// Launches the split kernel, with the handle's timing events attached to the
+// kernel itself when they are set (their timestamps are the kernel's own
+// start and end, with no marker packets between launches).
+hipError_t launch_split(const rl_decode_attn* h, SplitKernel k, int64_t grid, int threads,
+                        size_t lds, hipStream_t st, SplitArgs& sa)
 {
-    if (h == nullptr || split_tokens == nullptr || num_splits == nullptr || max_pages < 1 ||
-        max_pages > h->cfg.max_pages_per_seq)
-        return RL_DA_ERR_INVALID_ARG;
-    *split_tokens = h->split_tokens;
-    *num_splits = (max_pages + h->split_pages - 1) / h->split_pages;
-    return RL_DA_OK;
+    if (h->ev_split_begin != nullptr) {
+        void* args[] = {&sa};
+        return hipExtLaunchKernel(reinterpret_cast<const void*>(k), dim3((unsigned)grid),
+                                  dim3(threads), args, lds, st, h->ev_split_begin,
+                                  h->ev_split_end, 0);
+    }
+    hipLaunchKernelGGL(k, dim3((unsigned)grid), dim3(threads), lds, st, sa);
+    return hipGetLastError();
 }
 
-rl_da_status rl_decode_attn_run(rl_decode_attn* h, const void* q, const void* k_pool,
-                                const void* v_pool, const float* k_scale,
-                                const float* v_scale, int64_t num_pages,
-                                const int32_t* block_table, int32_t max_pages,
-                                const int32_t* seq_lens, int32_t batch, float scale, void* out,
-                                void* stream)
+// Enqueues one decode step with the handle's kernels and workspace.
+rl_da_status enqueue_run(rl_decode_attn* h, const void* q, const void* k_pool,
+                         const void* v_pool, const float* k_scale, const float* v_scale,
+                         int64_t num_pages, const int32_t* block_table, int32_t max_pages,
+                         const int32_t* seq_lens, int32_t batch, float scale, void* out,
+                         hipStream_t st, bool clear_queue)
 {
-    if (h == nullptr)
-        return RL_DA_ERR_INVALID_ARG;
     const rl_da_config& cfg = h->cfg;
     if (batch < 0 || batch > cfg.max_batch)
         return RL_DA_ERR_INVALID_ARG;
@@ -1602,25 +1568,26 @@ rl_da_status rl_decode_attn_run(rl_decode_attn* h, const void* q, const void* k_
     sa.queue = h->queue;
     sa.scale_log2 = scale * kLog2e;
 
-    hipStream_t st = (hipStream_t)stream;
-    if (h->ev_split_begin != nullptr && hipEventRecord(h->ev_split_begin, st) != hipSuccess)
-        return RL_DA_ERR_HIP;
+    h->last_stream = st;
     const int threads = h->head_parallel ? kWave * h->heads_per_unit : kWave * kUnitWaves;
     if (persistent) {
+        if (clear_queue && schedule != kOnePerGroup) {
+            hipLaunchKernelGGL(clear_words, dim3(1), dim3(64), 0, st, h->queue, 2);
+            if (hipGetLastError() != hipSuccess)
+                return RL_DA_ERR_HIP;
+        }
         const int64_t grid = schedule == kOnePerGroup || units <= h->persistent_grid
                                  ? units
                                  : h->persistent_grid;
         const size_t lds =
             schedule == kQueuePlanned ? (size_t)plan_ints(batch) * sizeof(int) : 0;
-        hipLaunchKernelGGL(h->split_kernel_persistent, dim3((unsigned)grid), dim3(threads), lds,
-                           st, sa);
+        if (launch_split(h, h->split_kernel_persistent, grid, threads, lds, st, sa) !=
+            hipSuccess)
+            return RL_DA_ERR_HIP;
     } else {
-        hipLaunchKernelGGL(h->split_kernel, dim3((unsigned)units), dim3(threads), 0, st, sa);
+        if (launch_split(h, h->split_kernel, units, threads, 0, st, sa) != hipSuccess)
+            return RL_DA_ERR_HIP;
     }
-    if (hipGetLastError() != hipSuccess)
-        return RL_DA_ERR_HIP;
-    if (h->ev_split_end != nullptr && hipEventRecord(h->ev_split_end, st) != hipSuccess)
-        return RL_DA_ERR_HIP;
     if (num_splits > 1) {
         MergeArgs ma;
         ma.seq_lens = seq_lens;
@@ -1637,6 +1604,100 @@ rl_da_status rl_decode_attn_run(rl_decode_attn* h, const void* q, const void* k_
             return RL_DA_ERR_HIP;
     }
     return RL_DA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* rl_da_status_string(rl_da_status s)
+{
+    switch (s) {
+    case RL_DA_OK: return "ok";
+    case RL_DA_ERR_INVALID_ARG: return "invalid argument";
+    case RL_DA_ERR_UNSUPPORTED: return "unsupported configuration";
+    case RL_DA_ERR_OUT_OF_MEMORY: return "out of device memory";
+    case RL_DA_ERR_HIP: return "HIP runtime error";
+    }
+    return "unknown status";
+}
+
+rl_da_status rl_decode_attn_workspace_size(const rl_da_config* cfg, size_t* bytes)
+{
+    int st, sp, ms;
+    if (bytes == nullptr)
+        return RL_DA_ERR_INVALID_ARG;
+    const rl_da_status rc = check_config(cfg, &st, &sp, &ms);
+    if (rc != RL_DA_OK)
+        return rc;
+    *bytes = workspace_bytes_for(cfg, ms);
+    return RL_DA_OK;
+}
+
+rl_da_status rl_decode_attn_create(const rl_da_config* cfg, rl_decode_attn** out)
+{
+    if (out == nullptr)
+        return RL_DA_ERR_INVALID_ARG;
+    *out = nullptr;
+    int st, sp, ms;
+    rl_da_status rc = check_config(cfg, &st, &sp, &ms);
+    if (rc != RL_DA_OK)
+        return rc;
+    rl_decode_attn* h = (rl_decode_attn*)calloc(1, sizeof(rl_decode_attn));
+    if (h == nullptr)
+        return RL_DA_ERR_OUT_OF_MEMORY;
+    rc = init_handle(h, cfg);
+    if (rc != RL_DA_OK) {
+        free(h);
+        return rc;
+    }
+    void* ws = nullptr;
+    if (hipMalloc(&ws, h->workspace_bytes) != hipSuccess) {
+        (void)hipGetLastError();
+        free(h);
+        return RL_DA_ERR_OUT_OF_MEMORY;
+    }
+    bind_workspace(h, ws);
+    if (hipMemset(h->dev_error, 0, kControlBytes) != hipSuccess) {
+        (void)hipFree(ws);
+        free(h);
+        return RL_DA_ERR_HIP;
+    }
+    *out = h;
+    return RL_DA_OK;
+}
+
+rl_da_status rl_decode_attn_destroy(rl_decode_attn* h)
+{
+    if (h == nullptr)
+        return RL_DA_OK;
+    const hipError_t e = hipFree(h->workspace);
+    free(h);
+    return e == hipSuccess ? RL_DA_OK : RL_DA_ERR_HIP;
+}
+
+rl_da_status rl_decode_attn_split_info(const rl_decode_attn* h, int32_t max_pages,
+                                       int32_t* split_tokens, int32_t* num_splits)
+{
+    if (h == nullptr || split_tokens == nullptr || num_splits == nullptr || max_pages < 1 ||
+        max_pages > h->cfg.max_pages_per_seq)
+        return RL_DA_ERR_INVALID_ARG;
+    *split_tokens = h->split_tokens;
+    *num_splits = (max_pages + h->split_pages - 1) / h->split_pages;
+    return RL_DA_OK;
+}
+
+rl_da_status rl_decode_attn_run(rl_decode_attn* h, const void* q, const void* k_pool,
+                                const void* v_pool, const float* k_scale,
+                                const float* v_scale, int64_t num_pages,
+                                const int32_t* block_table, int32_t max_pages,
+                                const int32_t* seq_lens, int32_t batch, float scale, void* out,
+                                void* stream)
+{
+    if (h == nullptr)
+        return RL_DA_ERR_INVALID_ARG;
+    return enqueue_run(h, q, k_pool, v_pool, k_scale, v_scale, num_pages, block_table,
+                       max_pages, seq_lens, batch, scale, out, (hipStream_t)stream, false);
 }
 
 rl_da_status rl_decode_attn_unit_heads(const rl_decode_attn* h, int32_t* kv_heads_per_unit)
@@ -1663,12 +1724,16 @@ rl_da_status rl_decode_attn_check_error(rl_decode_attn* h, int32_t* device_error
         return RL_DA_ERR_INVALID_ARG;
     if ((h->cfg.flags & RL_DA_CHECKED) == 0)
         return RL_DA_ERR_UNSUPPORTED;
-    if (hipDeviceSynchronize() != hipSuccess)
-        return RL_DA_ERR_HIP;
+    // Read the word behind the latest run on its stream, then clear it on the
+    // same stream; other streams of the device are not waited for.
+    const hipStream_t st = h->last_stream;
     int32_t v = 0;
-    if (hipMemcpy(&v, h->dev_error, sizeof v, hipMemcpyDeviceToHost) != hipSuccess)
+    if (hipMemcpyAsync(&v, h->dev_error, sizeof v, hipMemcpyDeviceToHost, st) != hipSuccess)
         return RL_DA_ERR_HIP;
-    if (hipMemset(h->dev_error, 0, sizeof v) != hipSuccess)
+    hipLaunchKernelGGL(clear_words, dim3(1), dim3(64), 0, st, h->dev_error, 1);
+    if (hipGetLastError() != hipSuccess)
+        return RL_DA_ERR_HIP;
+    if (hipStreamSynchronize(st) != hipSuccess)
         return RL_DA_ERR_HIP;
     *device_error = v;
     return RL_DA_OK;

@@ -82,22 +82,42 @@ def check_close(got, ref, what="", extra_abs=0.0):
         % (what, err[worst], ulp[worst], worst, ref[worst], got[worst]))
     with np.errstate(invalid="ignore", divide="ignore"):
         ulps = np.where(ulp > 0, err / ulp, 0.0)
+    ref_rms = float(np.sqrt(np.mean(ref * ref)))
     return dict(max_abs_err=float(err.max()), max_ulp=float(ulps.max()),
-                frac_rne_equal=float(np.mean(got == rne_bf16(ref))))
+                frac_rne_equal=float(np.mean(got == rne_bf16(ref))),
+                rel_rms_err=float(np.sqrt(np.mean(err * err))) / ref_rms if ref_rms > 0 else 0.0,
+                elements=int(err.size))
 
 
-def sample_rows(p, n, seed=0):
-    """(b, h) pairs: the longest and shortest sequences in full, plus random."""
-    rng = np.random.default_rng(seed)
-    L = p.lengths()
-    Hq = p.num_q_heads
-    rows = set()
-    for b in (int(np.argmax(L)), int(np.argmin(L))):
-        for h in range(0, Hq, max(1, Hq // 8)):
-            rows.add((b, h))
-    while len(rows) < n:
-        rows.add((int(rng.integers(p.batch)), int(rng.integers(Hq))))
-    return np.array(sorted(rows), dtype=np.int32)
+# Extend attention feeds the P.V product with each probability rounded to
+# bf16: w_t (1 + d_t), |d_t| <= 2^-9.  Writing o = sum w v / sum w:
+#   bf16 pools normalise by the sum of the same rounded weights, so the fp32
+#   result is sum w (1+d) v / sum w (1+d) = o + sum w d (v - o) / sum w (1+d),
+#   off by at most 2^-9 / (1 - 2^-9) * sum w |v - o| / sum w
+#   <= 2^-9 (1 + 2^-8) (M1 + |o|),  M1 = sum w |v| / sum w;
+#   e4m3 pools normalise by the unrounded weights: off by at most 2^-9 M1.
+# M1 is the attention output over the same weights with every value replaced
+# by its magnitude (one more oracle call on a pool with the sign bits cleared).
+P_ROUND = 2.0 ** -9 * (1.0 + 2.0 ** -8)
+
+
+def extend_extra(kv_dtype, ref, abs_ref):
+    """Per-element allowance of the rounded probabilities (above), given the
+    reference o and the weighted mean magnitude M1 of the values."""
+    ref = np.abs(np.asarray(ref, dtype=np.float64))
+    abs_ref = np.asarray(abs_ref, dtype=np.float64)
+    assert np.all(abs_ref >= ref * (1 - 1e-12)), "M1 must bound |o|"
+    if kv_dtype == "bf16":
+        return P_ROUND * (abs_ref + ref)
+    return P_ROUND * abs_ref
+
+
+def abs_value_host(p, h=None):
+    """Host copy of problem p's value pool with every sign bit cleared (bf16
+    bit 15, e4m3 bit 7): the pool of |V| under the same slab scales."""
+    h = h if h is not None else p.host_arrays()
+    v = h["v_pool"]
+    return v & (np.uint16(0x7FFF) if v.dtype == np.uint16 else np.uint8(0x7F))
 
 
 def max_pages_for(lengths, page=16):

@@ -9,7 +9,8 @@ import torch
 from paper_2512_22492_amd import binding as B
 from paper_2512_22492_amd import workloads
 
-from gpu_util import bf16_to_f64, bf16_ulp, check_close, device, run_gpu
+from gpu_util import (abs_value_host, bf16_to_f64, bf16_ulp, check_close, device, extend_extra,
+                      run_gpu)
 
 pytestmark = pytest.mark.gpu
 
@@ -127,14 +128,17 @@ def test_extend_with_zero_scale_gives_causal_prefix_means(layout):
     torch.cuda.synchronize()
     got = bf16_to_f64(out)
     want = np.zeros_like(got)
+    m1 = np.zeros_like(got)
     for b in range(len(new)):
         for i in range(new[b]):
             row = int(q_start[b]) + i
             for h in range(8):
-                want[row, h] = visible_values(p, b, h // 4, upto=prior[b] + i + 1).mean(axis=0)
-    # the P.V product takes P rounded to bf16: 2^-8 max|V| on top of one ulp
-    extra = 2.0 ** -8 * float(p.v_pool.float().abs().max())
-    print(check_close(got, want, "extend zero scale " + layout, extra_abs=extra))
+                vis = visible_values(p, b, h // 4, upto=prior[b] + i + 1)
+                want[row, h] = vis.mean(axis=0)
+                m1[row, h] = np.abs(vis).mean(axis=0)
+    # equal weights: the rounded-probability allowance with M1 = mean |v|
+    print(check_close(got, want, "extend zero scale " + layout,
+                      extra_abs=extend_extra("bf16", want, m1)))
 
 
 @pytest.mark.parametrize("layout", LAYOUTS)
@@ -158,9 +162,10 @@ def test_negative_and_zero_scales_match_the_oracle(layout):
         B.extend_attention(pe, q, q_start, max(new), out)
         torch.cuda.synchronize()
         h = pe.host_arrays()
-        ref = oracle.extend_attention(q.cpu().view(torch.int16).numpy().view(np.uint16),
-                                      q_start.cpu().numpy(), h["k_pool"], h["v_pool"],
-                                      h["block_table"], h["seq_lens"], num_kv_heads=2,
-                                      scale=scale, layout=layout)
-        extra = 2.0 ** -8 * float(pe.v_pool.float().abs().max())
-        print(check_close(bf16_to_f64(out), ref, "extend scale %g" % scale, extra_abs=extra))
+        refs = [oracle.extend_attention(q.cpu().view(torch.int16).numpy().view(np.uint16),
+                                        q_start.cpu().numpy(), h["k_pool"], v,
+                                        h["block_table"], h["seq_lens"], num_kv_heads=2,
+                                        scale=scale, layout=layout)
+                for v in (h["v_pool"], abs_value_host(pe, h))]
+        print(check_close(bf16_to_f64(out), refs[0], "extend scale %g" % scale,
+                          extra_abs=extend_extra("bf16", refs[0], refs[1])))

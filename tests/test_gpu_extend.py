@@ -9,7 +9,7 @@ import oracle
 from paper_2512_22492_amd import binding as B
 from paper_2512_22492_amd import workloads
 
-from gpu_util import bf16_to_f64, check_close, device
+from gpu_util import abs_value_host, bf16_to_f64, check_close, device, extend_extra
 
 pytestmark = pytest.mark.gpu
 
@@ -33,32 +33,47 @@ def run_extend(p, q, q_start, max_new):
     return out
 
 
-def p_split_bound(p):
-    """The PV MFMA takes each probability rounded to bf16 (relative error at
-    most 2^-9 per weight).  bf16 pools normalise by the sum of the rounded
-    weights (the weights of the convex combination then move by at most 2^-8
-    in total), e4m3 pools by the sum of the unrounded ones: either way the
-    output may move by 2^-8 * max|V| beyond the bf16 output rounding (V
-    decoded with its slab scales for e4m3 pools)."""
-    if p.kv_dtype == "bf16":
-        vmax = float(p.v_pool.float().abs().max())
-    else:
-        codes = p.v_pool.view(torch.float8_e4m3fn).float().abs()
-        dims = (2, 3) if p.layout == "hnd" else (1, 3)   # slot and dim axes
-        vmax = float((codes.amax(dim=dims) * p.v_scale).max())
-    return 2.0 ** -8 * vmax
-
-
-def oracle_extend(p, q, q_start):
+def oracle_extend(p, q, q_start, abs_values=False):
+    """The oracle's extend attention of problem p; with abs_values, over the
+    value pool of magnitudes |V| (same weights), which gives M1."""
     h = p.host_arrays()
     kw = {}
     if p.kv_dtype != "bf16":
         kw = dict(kv_dtype=oracle.KV_FP8_E4M3, k_scale=h["k_scale"], v_scale=h["v_scale"])
+    v_pool = abs_value_host(p, h) if abs_values else h["v_pool"]
     return oracle.extend_attention(q.cpu().view(torch.int16).numpy().view(np.uint16),
-                                   q_start.cpu().numpy(), h["k_pool"], h["v_pool"],
+                                   q_start.cpu().numpy(), h["k_pool"], v_pool,
                                    h["block_table"], h["seq_lens"],
                                    num_kv_heads=p.num_kv_heads, scale=p.scale,
                                    layout=p.layout, **kw)
+
+
+def check_extend(p, q, q_start, got, what):
+    """Official bound, and one bf16 ulp plus the rounded-probability
+    allowance derived from each row's own weights (extend_extra)."""
+    ref = oracle_extend(p, q, q_start)
+    extra = extend_extra(p.kv_dtype, ref, oracle_extend(p, q, q_start, abs_values=True))
+    stats = check_close(bf16_to_f64(got), ref, what, extra_abs=extra)
+    print(what, stats, flush=True)
+    return stats
+
+
+def check_rows_as_decode(p, got_row, q_bits_row, b, visible, what, kw=None):
+    """New token of sequence b that sees `visible` cached tokens: all its heads
+    against the oracle's decode attention over that prefix."""
+    h = p.host_arrays()
+    kw = kw or {}
+    lens = h["seq_lens"].copy()
+    lens[b] = visible
+    qrow = np.repeat(q_bits_row, p.batch, axis=0)
+    rows = [[b, hh] for hh in range(p.num_q_heads)]
+    args = (h["k_pool"], h["block_table"], lens)
+    ref = oracle.decode_attention(qrow, args[0], h["v_pool"], args[1], args[2],
+                                  num_kv_heads=p.num_kv_heads, scale=p.scale, rows=rows, **kw)
+    m1 = oracle.decode_attention(qrow, args[0], abs_value_host(p, h), args[1], args[2],
+                                 num_kv_heads=p.num_kv_heads, scale=p.scale, rows=rows, **kw)
+    return check_close(bf16_to_f64(got_row), ref, what,
+                       extra_abs=extend_extra(p.kv_dtype, ref, m1))
 
 
 CASES = [
@@ -73,9 +88,8 @@ CASES = [
 def test_extend_matches_oracle(hq, hkv, case):
     new, prior = CASES[case]
     p, q, q_start = extend_problem(new, prior, seed=31 + case, hq=hq, hkv=hkv)
-    got = bf16_to_f64(run_extend(p, q, q_start, max(new)))
-    print(check_close(got, oracle_extend(p, q, q_start), "extend G=%d case %d" % (hq // hkv, case),
-                      extra_abs=p_split_bound(p)))
+    got = run_extend(p, q, q_start, max(new))
+    check_extend(p, q, q_start, got, "extend G=%d case %d" % (hq // hkv, case))
 
 
 def test_extend_qwen3_8b_shapes_sampled():
@@ -84,22 +98,14 @@ def test_extend_qwen3_8b_shapes_sampled():
     got = run_extend(p, q, q_start, max(new))
     # oracle on a sample of rows: the oracle takes whole sequences, so restrict
     # each sequence's rows by passing a sub-problem of 4 chosen tokens each
-    h = p.host_arrays()
     qs = q_start.cpu().numpy()
-    pick = []
+    q_bits = q.cpu().view(torch.int16).numpy().view(np.uint16)
     for b in range(4):
         n = new[b]
         for i in sorted({0, n // 2, n - 1}):
-            pick.append((b, i))
-    for b, i in pick:
-        lens = h["seq_lens"].copy()
-        lens[b] = prior[b] + i + 1
-        qrow = q[qs[b] + i:qs[b] + i + 1].cpu().view(torch.int16).numpy().view(np.uint16)
-        ref = oracle.decode_attention(np.repeat(qrow, 4, axis=0), h["k_pool"], h["v_pool"],
-                                      h["block_table"], lens, num_kv_heads=8, scale=p.scale,
-                                      rows=[[b, hh] for hh in range(32)])
-        check_close(bf16_to_f64(got[qs[b] + i]), ref, "row b=%d i=%d" % (b, i),
-                    extra_abs=p_split_bound(p))
+            r = qs[b] + i
+            print(check_rows_as_decode(p, got[r], q_bits[r:r + 1], b, prior[b] + i + 1,
+                                       "row b=%d i=%d" % (b, i)))
 
 
 @pytest.mark.parametrize("config,n", [("qwen3_8b_step", 512), ("fp8_large_batch", 128)])
@@ -131,14 +137,9 @@ def test_extend_bench_workloads_sampled(config, n):
     q_bits = q.cpu().view(torch.int16).numpy().view(np.uint16)
     for b in seqs:
         for i in sorted({0, n // 2, n - 1}):
-            lens = h["seq_lens"].copy()
-            lens[b] = int(prior[b]) + i + 1
-            qrow = np.repeat(q_bits[b * n + i:b * n + i + 1], p.batch, axis=0)
-            ref = oracle.decode_attention(qrow, h["k_pool"], h["v_pool"], h["block_table"], lens,
-                                          num_kv_heads=p.num_kv_heads, scale=p.scale,
-                                          rows=[[b, hh] for hh in range(p.num_q_heads)], **kw)
-            check_close(bf16_to_f64(got[b * n + i]), ref, "%s b=%d i=%d" % (config, b, i),
-                        extra_abs=p_split_bound(p))
+            r = b * n + i
+            print(check_rows_as_decode(p, got[r], q_bits[r:r + 1], b, int(prior[b]) + i + 1,
+                                       "%s b=%d i=%d" % (config, b, i), kw))
 
 
 def test_extend_ignores_unread_memory_and_is_causal():
@@ -185,8 +186,7 @@ def test_extend_ignores_unstaged_memory_and_the_table_tail(kv, layout):
             row[row == 0] = spare
     p = workloads.DecodeProblem(**{**p.__dict__, "block_table": bt})
     base = run_extend(p, q, q_start, max(new))
-    print(check_close(bf16_to_f64(base), oracle_extend(p, q, q_start), "unstaged " + kv + layout,
-                      extra_abs=p_split_bound(p)))
+    check_extend(p, q, q_start, base, "unstaged " + kv + layout)
     nan_code = float("nan") if kv == "bf16" else 0x7F   # e4m3 NaN
     for pool in (p.k_pool, p.v_pool):
         pool[0] = nan_code
@@ -231,8 +231,7 @@ def test_extend_longest_first_order_on_a_large_batch():
     sub_q = torch.cat([q[qs[b]:qs[b + 1]] for b in rows])
     sub_start = torch.tensor(np.concatenate([[0], np.cumsum([new[b] for b in rows])]),
                              dtype=torch.int32, device=q.device)
-    print(check_close(bf16_to_f64(got), oracle_extend(sub, sub_q, sub_start),
-                      "longest-first, 37000 sequences", extra_abs=p_split_bound(p)))
+    check_extend(sub, sub_q, sub_start, got, "longest-first, 37000 sequences")
 
 
 def test_extend_argument_validation():
@@ -265,8 +264,7 @@ def test_extend_nhd_pools_match_oracle_and_the_hnd_result(hq, hkv):
     pn, q, q_start = extend_problem(new, prior, seed=40 + hq, hq=hq, hkv=hkv, layout="nhd")
     ph, _, _ = extend_problem(new, prior, seed=40 + hq, hq=hq, hkv=hkv)
     got = run_extend(pn, q, q_start, max(new))
-    print(check_close(bf16_to_f64(got), oracle_extend(pn, q, q_start),
-                      "extend nhd G=%d" % (hq // hkv), extra_abs=p_split_bound(pn)))
+    check_extend(pn, q, q_start, got, "extend nhd G=%d" % (hq // hkv))
     same = run_extend(ph, q, q_start, max(new))
     assert torch.equal(got.view(torch.int16), same.view(torch.int16))
 
@@ -280,7 +278,5 @@ def test_extend_fp8_pools_match_oracle(hq, hkv, case, layout):
     new, prior = CASES[case]
     p, q, q_start = extend_problem(new, prior, seed=50 + case, hq=hq, hkv=hkv, layout=layout,
                                    kv="fp8_e4m3")
-    got = bf16_to_f64(run_extend(p, q, q_start, max(new)))
-    print(check_close(got, oracle_extend(p, q, q_start),
-                      "extend fp8 %s G=%d case %d" % (layout, hq // hkv, case),
-                      extra_abs=p_split_bound(p)))
+    got = run_extend(p, q, q_start, max(new))
+    check_extend(p, q, q_start, got, "extend fp8 %s G=%d case %d" % (layout, hq // hkv, case))

@@ -10,7 +10,8 @@ from oracle import weight_sync as WS
 from paper_2512_22492_amd import binding as B
 from paper_2512_22492_amd import workloads
 
-from gpu_util import KV, bf16_to_f64, check_close, device, oracle_ref, run_gpu
+from gpu_util import (KV, abs_value_host, bf16_to_f64, check_close, device, extend_extra,
+                      oracle_ref, run_gpu)
 
 pytestmark = pytest.mark.gpu
 
@@ -71,13 +72,13 @@ def test_extend_and_append_beyond_4gib(layout):
     torch.cuda.synchronize()
     # oracle over the gathered sequences only (the full pool is too large to copy)
     h = p.host_arrays()
-    ref = oracle.extend_attention(q.cpu().view(torch.int16).numpy().view(np.uint16),
-                                  q_start.cpu().numpy(), h["k_pool"], h["v_pool"],
-                                  h["block_table"], h["seq_lens"], num_kv_heads=8,
-                                  scale=p.scale, layout=layout)
-    # the P.V product takes P rounded to bf16: 2^-8 max|V| on top of one ulp
-    extra = 2.0 ** -8 * float(p.v_pool.float().abs().max())
-    print(check_close(bf16_to_f64(out), ref, "extend > 4 GiB " + layout, extra_abs=extra))
+    ref, m1 = [oracle.extend_attention(q.cpu().view(torch.int16).numpy().view(np.uint16),
+                                       q_start.cpu().numpy(), h["k_pool"], v,
+                                       h["block_table"], h["seq_lens"], num_kv_heads=8,
+                                       scale=p.scale, layout=layout)
+               for v in (h["v_pool"], abs_value_host(p, h))]
+    print(check_close(bf16_to_f64(out), ref, "extend > 4 GiB " + layout,
+                      extra_abs=extend_extra("bf16", ref, m1)))
 
 
 def test_pack_a_tensor_larger_than_4gib():
