@@ -90,15 +90,16 @@ def check_close(got, ref, what="", extra_abs=0.0):
 
 
 # Extend attention feeds the P.V product with each probability rounded to
-# bf16: w_t (1 + d_t), |d_t| <= 2^-9.  Writing o = sum w v / sum w:
+# bf16 (8 significant bits, round to nearest even): w_t (1 + d_t) with
+# |d_t| <= 2^-8.  Writing o = sum w v / sum w:
 #   bf16 pools normalise by the sum of the same rounded weights, so the fp32
 #   result is sum w (1+d) v / sum w (1+d) = o + sum w d (v - o) / sum w (1+d),
-#   off by at most 2^-9 / (1 - 2^-9) * sum w |v - o| / sum w
-#   <= 2^-9 (1 + 2^-8) (M1 + |o|),  M1 = sum w |v| / sum w;
-#   e4m3 pools normalise by the unrounded weights: off by at most 2^-9 M1.
+#   off by at most 2^-8 / (1 - 2^-8) * sum w |v - o| / sum w
+#   <= 2^-8 (1 + 2^-7) (M1 + |o|),  M1 = sum w |v| / sum w;
+#   e4m3 pools normalise by the unrounded weights: off by at most 2^-8 M1.
 # M1 is the attention output over the same weights with every value replaced
 # by its magnitude (one more oracle call on a pool with the sign bits cleared).
-P_ROUND = 2.0 ** -9 * (1.0 + 2.0 ** -8)
+P_ROUND = 2.0 ** -8 * (1.0 + 2.0 ** -7)
 
 
 def extend_extra(kv_dtype, ref, abs_ref):
