@@ -83,7 +83,9 @@ typedef enum {
     RL_DA_ERR_INVALID_ARG = 1,   /* null/misaligned pointer, bad size         */
     RL_DA_ERR_UNSUPPORTED = 2,   /* valid request this build does not serve   */
     RL_DA_ERR_OUT_OF_MEMORY = 3, /* workspace allocation failed in create()   */
-    RL_DA_ERR_HIP = 4            /* a HIP runtime call or launch failed       */
+    RL_DA_ERR_HIP = 4,           /* a HIP runtime call or launch failed       */
+    RL_DA_ERR_SCRATCH_TOO_SMALL = 5 /* rl_decode_attn_run_noalloc: the step's  */
+                                 /* workspace exceeds its fixed scratch       */
 } rl_da_status;
 
 typedef enum { RL_DA_KV_BF16 = 0, RL_DA_KV_FP8_E4M3 = 1 } rl_da_kv_dtype;
@@ -264,6 +266,38 @@ rl_da_status rl_kv_append(const void* k_new, const void* v_new, void* k_pool, vo
  */
 rl_da_status rl_decode_attn_set_timing_events(rl_decode_attn* h, void* split_begin,
                                               void* split_end);
+
+/* Bytes of device scratch that rl_decode_attn_run_noalloc uses on each device. */
+#define RL_DA_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/*
+ * For callers that cannot allocate device memory -- code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc: one decode
+ * step exactly as rl_decode_attn_run computes it for a handle created with
+ * cfg (same kernels, same split size, bit-identical results), with the
+ * handle's workspace replaced by a fixed array of
+ * RL_DA_NOALLOC_SCRATCH_BYTES in device memory that the library holds on each
+ * device it runs on until the process ends.  Calls no hipMalloc or hipFree
+ * and allocates no host memory; the first call on a device looks up that
+ * device's copy of the array.  Arguments and preconditions as for create()
+ * plus run(); the caller still owns every input and output.
+ *   RL_DA_ERR_SCRATCH_TOO_SMALL  when rl_decode_attn_workspace_size(cfg)
+ *                                exceeds RL_DA_NOALLOC_SCRATCH_BYTES
+ *                                (nothing is enqueued)
+ *   RL_DA_ERR_UNSUPPORTED        with RL_DA_CHECKED (there is no handle whose
+ *                                error word could be read)
+ * Every call on one device shares that device's scratch, which keeps the
+ * last call's contents: calls that can overlap on one device (two streams,
+ * two host threads enqueueing concurrently) race on it and give wrong
+ * results.  Order them on one stream.  Before each launch that uses the unit
+ * queue, the queue is cleared by a kernel on the caller's stream.
+ */
+rl_da_status rl_decode_attn_run_noalloc(const rl_da_config* cfg, const void* q,
+                                        const void* k_pool, const void* v_pool,
+                                        const float* k_scale, const float* v_scale,
+                                        int64_t num_pages, const int32_t* block_table,
+                                        int32_t max_pages, const int32_t* seq_lens,
+                                        int32_t batch, float scale, void* out, void* stream);
 
 #ifdef __cplusplus
 }

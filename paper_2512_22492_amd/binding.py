@@ -18,9 +18,12 @@ RL_DA_ERR_INVALID_ARG = 1
 RL_DA_ERR_UNSUPPORTED = 2
 RL_DA_ERR_OUT_OF_MEMORY = 3
 RL_DA_ERR_HIP = 4
+RL_DA_ERR_SCRATCH_TOO_SMALL = 5
+RL_DA_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 RL_DA_KV_BF16 = 0
 RL_DA_KV_FP8_E4M3 = 1
+KV_DTYPES = {"bf16": RL_DA_KV_BF16, "fp8_e4m3": RL_DA_KV_FP8_E4M3}
 
 RL_DA_LAYOUT_HND = 0
 RL_DA_LAYOUT_NHD = 1
@@ -53,6 +56,7 @@ EXPORTED = [
     "rl_ws_pack",
     "rl_ws_unpack",
     "rl_ws_destroy",
+    "rl_decode_attn_run_noalloc",
 ]
 
 
@@ -119,6 +123,10 @@ def load_library():
     lib.rl_decode_attn_run.argtypes = [vp, vp, vp, vp, vp, vp, i64, vp, i32, vp, i32,
                                        ctypes.c_float, vp, vp]
     lib.rl_decode_attn_run.restype = ctypes.c_int
+    lib.rl_decode_attn_run_noalloc.argtypes = [ctypes.POINTER(rl_da_config), vp, vp, vp, vp,
+                                               vp, i64, vp, i32, vp, i32, ctypes.c_float, vp,
+                                               vp]
+    lib.rl_decode_attn_run_noalloc.restype = ctypes.c_int
     lib.rl_decode_attn_destroy.argtypes = [vp]
     lib.rl_decode_attn_destroy.restype = ctypes.c_int
     lib.rl_da_status_string.argtypes = [ctypes.c_int]
@@ -269,6 +277,15 @@ def rl_decode_attn_run(h, q, k_pool, v_pool, k_scale, v_scale, num_pages, block_
                        max_pages, seq_lens, batch, scale, out, stream=None) -> int:
     return load_library().rl_decode_attn_run(
         h, _ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(k_scale), _ptr(v_scale),
+        int(num_pages), _ptr(block_table), int(max_pages), _ptr(seq_lens), int(batch),
+        float(scale), _ptr(out), _stream(stream))
+
+
+def rl_decode_attn_run_noalloc(cfg, q, k_pool, v_pool, k_scale, v_scale, num_pages,
+                               block_table, max_pages, seq_lens, batch, scale, out,
+                               stream=None) -> int:
+    return load_library().rl_decode_attn_run_noalloc(
+        ctypes.byref(cfg), _ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(k_scale), _ptr(v_scale),
         int(num_pages), _ptr(block_table), int(max_pages), _ptr(seq_lens), int(batch),
         float(scale), _ptr(out), _stream(stream))
 
@@ -487,7 +504,7 @@ class DecodeAttention:
     def __init__(self, num_q_heads, num_kv_heads, max_batch, max_pages_per_seq, *,
                  kv_dtype="bf16", layout="hnd", split_tokens=0, flags=0, head_dim=128,
                  page_size=16):
-        dt = {"bf16": RL_DA_KV_BF16, "fp8_e4m3": RL_DA_KV_FP8_E4M3}[kv_dtype]
+        dt = KV_DTYPES[kv_dtype]
         self.kv_dtype = kv_dtype
         self.layout = layout
         self.cfg = make_config(num_q_heads, num_kv_heads, max_batch, max_pages_per_seq,

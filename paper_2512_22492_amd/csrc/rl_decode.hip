@@ -30,6 +30,9 @@
 // with log2(e)) so that every exponential is one v_exp_f32.
 
 #include <stdlib.h>
+#include <string.h>
+
+#include <mutex>
 
 #include "rl_common.h"
 
@@ -1618,6 +1621,8 @@ const char* rl_da_status_string(rl_da_status s)
     case RL_DA_ERR_UNSUPPORTED: return "unsupported configuration";
     case RL_DA_ERR_OUT_OF_MEMORY: return "out of device memory";
     case RL_DA_ERR_HIP: return "HIP runtime error";
+    case RL_DA_ERR_SCRATCH_TOO_SMALL:
+        return "workspace exceeds the allocation-free entry point's fixed scratch";
     }
     return "unknown status";
 }
@@ -1740,3 +1745,109 @@ rl_da_status rl_decode_attn_check_error(rl_decode_attn* h, int32_t* device_error
 }
 
 }  // extern "C"
+
+// ------------------------------------------ allocation-free entry point ---
+//
+// rl_decode_attn_run_noalloc runs the decode step with the kernels and split
+// size of a handle created with the same configuration, but takes its
+// workspace (per-split partials, error word, unit queue) from `scratch`, a
+// fixed device array, instead of allocating one.  Host code must never pass
+// the array's name to a kernel or a copy: it names a host-side stand-in.  The
+// device address comes from hipGetSymbolAddress, taken once per device (each
+// device holds its own copy of the array) with that device current, and only
+// that address is used afterwards.
+
+static __device__ __align__(256) uint8_t scratch[RL_DA_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+// Recently used configurations, so that repeated calls skip the occupancy
+// queries of init_handle.
+constexpr int kNoallocCacheEntries = 8;
+
+struct NoallocEntry {
+    bool used;
+    int device;
+    rl_da_config cfg;
+    rl_decode_attn h;  // workspace not bound
+};
+
+std::mutex g_noalloc_mu;
+void* g_scratch_ptr[kMaxDevices];  // device address of `scratch`, per device
+NoallocEntry g_noalloc_cache[kNoallocCacheEntries];
+int g_noalloc_next;
+
+// Fills *h for cfg on the current device `dev` (no workspace bound) and
+// returns the device address of that device's scratch in *ws.
+rl_da_status noalloc_setup(const rl_da_config* cfg, int dev, rl_decode_attn* h, void** ws)
+{
+    std::lock_guard<std::mutex> lock(g_noalloc_mu);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress((void**)&ptr, HIP_SYMBOL(scratch)) != hipSuccess ||
+            ptr == nullptr) {
+            (void)hipGetLastError();
+            return RL_DA_ERR_HIP;
+        }
+        g_scratch_ptr[dev] = ptr;
+    }
+    *ws = g_scratch_ptr[dev];
+    for (int i = 0; i < kNoallocCacheEntries; ++i) {
+        const NoallocEntry& e = g_noalloc_cache[i];
+        if (e.used && e.device == dev && memcmp(&e.cfg, cfg, sizeof *cfg) == 0) {
+            *h = e.h;
+            return RL_DA_OK;
+        }
+    }
+    memset(h, 0, sizeof *h);
+    const rl_da_status rc = init_handle(h, cfg);
+    if (rc != RL_DA_OK)
+        return rc;
+    if (h->workspace_bytes > (size_t)RL_DA_NOALLOC_SCRATCH_BYTES)
+        return RL_DA_ERR_SCRATCH_TOO_SMALL;
+    NoallocEntry& slot = g_noalloc_cache[g_noalloc_next];
+    g_noalloc_next = (g_noalloc_next + 1) % kNoallocCacheEntries;
+    slot.used = true;
+    slot.device = dev;
+    slot.cfg = *cfg;
+    slot.h = *h;
+    return RL_DA_OK;
+}
+
+}  // namespace
+
+extern "C" rl_da_status rl_decode_attn_run_noalloc(
+    const rl_da_config* cfg, const void* q, const void* k_pool, const void* v_pool,
+    const float* k_scale, const float* v_scale, int64_t num_pages, const int32_t* block_table,
+    int32_t max_pages, const int32_t* seq_lens, int32_t batch, float scale, void* out,
+    void* stream)
+{
+    if (cfg == nullptr)
+        return RL_DA_ERR_INVALID_ARG;
+    int st, sp, ms;
+    const rl_da_status rc = check_config(cfg, &st, &sp, &ms);
+    if (rc != RL_DA_OK)
+        return rc;
+    if ((cfg->flags & RL_DA_CHECKED) != 0)
+        return RL_DA_ERR_UNSUPPORTED;  // no handle to read the error word from
+    if (workspace_bytes_for(cfg, ms) > (size_t)RL_DA_NOALLOC_SCRATCH_BYTES)
+        return RL_DA_ERR_SCRATCH_TOO_SMALL;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess)
+        return RL_DA_ERR_HIP;
+    if (dev < 0 || dev >= kMaxDevices)
+        return RL_DA_ERR_UNSUPPORTED;
+    rl_decode_attn h;
+    void* ws = nullptr;
+    const rl_da_status rs = noalloc_setup(cfg, dev, &h, &ws);
+    if (rs != RL_DA_OK)
+        return rs;
+    bind_workspace(&h, ws);
+    h.ev_split_begin = nullptr;
+    h.ev_split_end = nullptr;
+    // The unit queue is cleared on the stream before each persistent launch:
+    // the scratch keeps whatever the device's previous call left in it.
+    return enqueue_run(&h, q, k_pool, v_pool, k_scale, v_scale, num_pages, block_table,
+                       max_pages, seq_lens, batch, scale, out, (hipStream_t)stream, true);
+}

@@ -62,7 +62,7 @@ def test_config_struct_matches_the_header(tmp_path):
 
 def test_status_strings():
     assert B.rl_da_status_string(B.RL_DA_OK) == "ok"
-    for s in (1, 2, 3, 4):
+    for s in (1, 2, 3, 4, 5):
         assert B.rl_da_status_string(s) not in ("ok", "unknown status")
     assert B.rl_da_status_string(99) == "unknown status"
 
@@ -146,3 +146,20 @@ def test_null_arguments():
     v = ctypes.c_int32()
     assert lib.rl_decode_attn_check_error(None, ctypes.byref(v)) == B.RL_DA_ERR_INVALID_ARG
     assert lib.rl_decode_attn_workspace_size(None, None) == B.RL_DA_ERR_INVALID_ARG
+
+
+def test_noalloc_entry_point_host_checks():
+    """The allocation-free entry point rejects, before touching the device:
+    no configuration, a configuration create() rejects, checked mode, and a
+    step whose workspace exceeds its fixed scratch."""
+    lib = B.load_library()
+    args = (1, 1, 1, None, None, 1, 1, 1, 1, 1, 1.0, 1, None)
+    assert lib.rl_decode_attn_run_noalloc(None, *args) == B.RL_DA_ERR_INVALID_ARG
+    assert B.rl_decode_attn_run_noalloc(cfg(head_dim=64), *args) == B.RL_DA_ERR_UNSUPPORTED
+    assert B.rl_decode_attn_run_noalloc(cfg(max_batch=0), *args) == B.RL_DA_ERR_INVALID_ARG
+    assert B.rl_decode_attn_run_noalloc(cfg(flags=B.RL_DA_CHECKED), *args) == \
+        B.RL_DA_ERR_UNSUPPORTED
+    big = cfg(max_batch=1024, max_pages_per_seq=4096, split_tokens=512)
+    rc, need = B.rl_decode_attn_workspace_size(big)
+    assert rc == B.RL_DA_OK and need > B.RL_DA_NOALLOC_SCRATCH_BYTES
+    assert B.rl_decode_attn_run_noalloc(big, *args) == B.RL_DA_ERR_SCRATCH_TOO_SMALL
