@@ -107,6 +107,9 @@ def parse_args():
                          "reads data a previous step left in the caches")
     ap.add_argument("--scores", choices=["mfma", "valu"], default="mfma",
                     help="score path of the split-K kernel")
+    ap.add_argument("--pv", choices=["mfma", "valu"], default="mfma",
+                    help="P.V product of the split-K kernel: the matrix cores (default), or "
+                         "vector-ALU FMAs (not for 16 query heads per kv head)")
     ap.add_argument("--split-tokens", type=int, default=0)
     ap.add_argument("--layout", choices=["hnd", "nhd"], default="hnd",
                     help="pool layout: [page][kv head][slot][dim] or [page][slot][kv head][dim]")
@@ -641,6 +644,8 @@ def main():
     flags = binding.RL_DA_SCORES_ON_VALU if args.scores == "valu" else 0
     if args.per_head_units:
         flags |= binding.RL_DA_PER_HEAD_UNITS
+    if args.pv == "valu":
+        flags |= binding.RL_DA_PV_ON_VALU
     attn = binding.DecodeAttention.for_problem(base, flags=flags,
                                                split_tokens=args.split_tokens)
     split_tokens, num_splits = attn.split_info(base.max_pages)
@@ -716,7 +721,10 @@ def main():
             "num_kv_heads": base.num_kv_heads, "head_dim": base.head_dim,
             "page_size": base.page_size, "seq_len_mean": float(base.lengths().mean()),
             "split_tokens": split_tokens, "num_splits": num_splits,
-            "scores": args.scores, "replicas": len(replicas), "layout": base.layout,
+            "scores": args.scores,
+            "pv": "valu" if args.scores == "valu" or args.pv == "valu" or unit_heads > 1
+                  else "mfma",
+            "replicas": len(replicas), "layout": base.layout,
             "units": "per-head" if unit_heads == 1
                      else "head-parallel (%d kv heads)" % unit_heads,
         },

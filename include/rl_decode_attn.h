@@ -113,6 +113,15 @@ typedef enum { RL_DA_LAYOUT_HND = 0, RL_DA_LAYOUT_NHD = 1 } rl_da_layout;
  * on head-major pools, with RL_DA_SCORES_ON_VALU, or with one kv head per
  * group (rl_decode_attn_unit_heads reports the choice). */
 #define RL_DA_PER_HEAD_UNITS 0x4u
+/* create() flag: accumulate the P.V product with vector-ALU FMAs on fp32
+ * probabilities instead of on the matrix cores.  By default the four-wavefront
+ * units form P.V with v_mfma_f32_16x16x16_bf16 over the page's values
+ * transposed through LDS, each probability entering as two bf16 terms (hi +
+ * lo, 2^-16 relative); kept to measure one path against the other.  Not
+ * available for Hq / Hkv = 16 (UNSUPPORTED), whose accumulators only the
+ * matrix-core pass holds; no effect on the head-parallel units, which keep
+ * the vector-ALU pass. */
+#define RL_DA_PV_ON_VALU 0x8u
 
 /* Device error word bits reported by rl_decode_attn_check_error(). */
 #define RL_DA_DEVERR_PAGE_OUT_OF_RANGE 0x1
@@ -120,7 +129,7 @@ typedef enum { RL_DA_LAYOUT_HND = 0, RL_DA_LAYOUT_NHD = 1 } rl_da_layout;
 
 typedef struct {
     int32_t num_q_heads;       /* Hq; a multiple of num_kv_heads               */
-    int32_t num_kv_heads;      /* Hkv; Hq / Hkv in {1, 2, 4, 8}                */
+    int32_t num_kv_heads;      /* Hkv; Hq / Hkv in {1, 2, 4, 8, 16}            */
     int32_t head_dim;          /* 128                                         */
     int32_t page_size;         /* tokens per page: 16                         */
     int32_t max_batch;         /* largest batch a run() may pass (>= 1)       */
@@ -133,7 +142,7 @@ typedef struct {
                                /* sequences of max_pages_per_seq pages into   */
                                /* >= 256 work-groups (a per-handle constant)  */
     uint32_t flags;            /* RL_DA_CHECKED, RL_DA_SCORES_ON_VALU,        */
-                               /* RL_DA_PER_HEAD_UNITS, or 0                  */
+                               /* RL_DA_PER_HEAD_UNITS, RL_DA_PV_ON_VALU, 0   */
 } rl_da_config;
 
 /*

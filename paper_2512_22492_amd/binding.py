@@ -32,6 +32,7 @@ LAYOUTS = {"hnd": RL_DA_LAYOUT_HND, "nhd": RL_DA_LAYOUT_NHD}
 RL_DA_CHECKED = 0x1
 RL_DA_SCORES_ON_VALU = 0x2
 RL_DA_PER_HEAD_UNITS = 0x4
+RL_DA_PV_ON_VALU = 0x8
 
 RL_DA_DEVERR_PAGE_OUT_OF_RANGE = 0x1
 RL_DA_DEVERR_LENGTH_TOO_LONG = 0x2

@@ -23,8 +23,9 @@
 // wavefront with four 16-byte-per-lane non-temporal loads each for K and V.  Scores are computed once per
 // kv head for all G query heads of the group (the GQA reuse), either with one
 // MFMA per 32 dims (the G query rows packed into a 16-row tile) or with bf16
-// dot2 ops and DPP row reductions; the value accumulation runs in fp32 on the
-// VALU.
+// dot2 ops and DPP row reductions.  The value accumulation runs on the matrix
+// cores by default (the page's values transposed through LDS, the weights as
+// two bf16 terms), or in fp32 on the vector ALUs.
 //
 // All arithmetic is fp32; scores are kept in the log2 domain (scale folded
 // with log2(e)) so that every exponential is one v_exp_f32.
@@ -570,6 +571,8 @@ struct KvBf16 {
     __device__ static uint4 k_block(const Buf& b, int i) { return b.k[i]; }
     __device__ static void values(const Buf& b, int k, float (&v)[8]) { unpack8(b.v[k], v); }
     __device__ static void clear_values(Buf& b, int k) { b.v[k] = make_uint4(0, 0, 0, 0); }
+    // dims 8c..8c+7 of token 4k + r as eight bf16
+    __device__ static uint4 values_bf16(const Buf& b, int k) { return b.v[k]; }
 };
 
 // OCP e4m3 slab: 2 KiB.  K: two 16-byte loads per lane (dims 16kg..16kg+15 and
@@ -618,6 +621,12 @@ struct KvFp8 {
         v[4] = a2.x; v[5] = a2.y; v[6] = a3.x; v[7] = a3.y;
     }
     __device__ static void clear_values(Buf& b, int k) { b.v[k] = make_uint2(0, 0); }
+    // the eight codes as exact bf16 (slab scale not applied)
+    __device__ static uint4 values_bf16(const Buf& b, int k)
+    {
+        return make_uint4(cvt2<false>(b.v[k].x), cvt2<true>(b.v[k].x), cvt2<false>(b.v[k].y),
+                          cvt2<true>(b.v[k].y));
+    }
 };
 
 // ------------------------------------------------ split kernel, MFMA QK ---
@@ -639,9 +648,9 @@ struct KvFp8 {
 // G = 8 (two scores per lane).
 template <int G>
 struct ScoreRows {
-    static constexpr int kStep = G > 4 ? 2 : 4;       // head g sits in row kStep * g
-    static constexpr int kPerLane = 4 / kStep;       // scores per lane
-    static constexpr int kLdsHeads = G > 4 ? 8 : 4;  // p/alpha entries per token in LDS
+    static constexpr int kStep = G > 8 ? 1 : G > 4 ? 2 : 4;  // head g sits in row kStep * g
+    static constexpr int kPerLane = 4 / kStep;              // scores per lane
+    static constexpr int kLdsHeads = G > 4 ? 8 : 4;         // p/alpha entries per token in LDS
 };
 
 // One wavefront's pass over its pages of one (sequence, kv head): the pages
@@ -1173,6 +1182,256 @@ __global__ __launch_bounds__(kWave * kUnitWaves) void split_valu_bf16(SplitArgs 
         unit(a, blockIdx.x / a.num_kv_heads, blockIdx.x % a.num_kv_heads, 0, true);
 }
 
+// ----------------------------------- split kernel, MFMA scores and MFMA PV ---
+//
+// Both contractions on the matrix cores.  Per page a wavefront forms the
+// scores of the query tile as split_mfma does (head g in row kStep * g; for
+// G = 16 every row is a head), then accumulates
+//     O^T[dim][row] += V^T[dim][token] P^T[token][row]
+// with v_mfma_f32_16x16x16_bf16, one product per 16-dim block.  V^T comes
+// from the page's values staged in wavefront-private LDS as [token][dim]
+// rows, read back with the LDS transpose read (lane 16q + j: tokens
+// 4q..4q+3 of dim 16i + j); P^T from the probabilities staged as [row][token]
+// rows (lane 16q + j: row j, tokens 4q..4q+3).  P enters the product as two
+// bf16 terms, hi = bf16(p) and lo = bf16(p - hi), so the weights carry p to
+// 2^-16 relative; the normaliser l sums the fp32 probabilities.  The
+// accumulators take 32 registers per lane whatever the group size (lane
+// 16q + j holds row j, dims 16i + 4q .. 16i + 4q + 3): what lets a group of 16
+// query heads run, whose value pass on the vector ALUs would need 16 x 8
+// accumulators per lane.  e4m3 values are widened exactly to bf16 as they are
+// staged; v_scale multiplies p before the split.
+
+constexpr int kPvVRow = kHeadDim + 16;  // bf16 per staged value row (288 bytes)
+constexpr int kPvPRow = 20;             // floats per staged probability row (80 bytes)
+
+struct PvWaveLds {
+    uint16_t v[kPageSize * kPvVRow];
+    float p[16 * kPvPRow];
+    float alpha[16];
+};
+
+// The per-wavefront tiles of the page loop and the unit merge's state share
+// the work-group's LDS: the merge runs after every wavefront has left its
+// loop.
+template <int G>
+union PvShared {
+    PvWaveLds wave[kUnitWaves];
+    UnitShared<G> unit;
+};
+
+typedef short short4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) short4_t lds_short4_t;
+
+// Four bf16 of one dim from four consecutive rows of a [row][dim] LDS tile
+// (ds_read_b64_tr_b16): within each 16-lane group, lane j receives element
+// j % 4 of the 8-byte chunks addressed by lanes j / 4 + 4e, e = 0..3, so when
+// lane s addresses row (base + s / 4), dims (d0 + 4 (s % 4)) .. +3, lane j
+// gets rows base .. base + 3 of dim d0 + j.
+__device__ __forceinline__ short4_t lds_read_tr16(const uint16_t* p)
+{
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_t*)p);
+}
+
+// Four fp32 weights as the two bf16 terms of the PV product.
+__device__ __forceinline__ void split_bf16(const float4& p, short4_t& hi, short4_t& lo)
+{
+    const uint32_t h0 = pack_bf16x2(p.x, p.y), h1 = pack_bf16x2(p.z, p.w);
+    const uint32_t l0 = pack_bf16x2(p.x - bf16_lo(h0), p.y - bf16_hi(h0));
+    const uint32_t l1 = pack_bf16x2(p.z - bf16_lo(h1), p.w - bf16_hi(h1));
+    hi = __builtin_bit_cast(short4_t, make_uint2(h0, h1));
+    lo = __builtin_bit_cast(short4_t, make_uint2(l0, l1));
+}
+
+// One wavefront's pass over its pages (p0 + wave + 4i) of one (sequence, kv
+// head).  On return o[i] holds, for lane 16q + j, tile row j's unnormalised
+// output at dims 16i + 4q .. +3, and the lanes of score group kg hold (m, l)
+// of tile rows 4kg + e kStep.
+template <int G, bool CHECKED, typename KV>
+__device__ __forceinline__ void attend_pages_pv(const SplitArgs& a, const WaveTask& t,
+                                                int32_t my_page, PvWaveLds& lds,
+                                                floatx4_t (&o)[kHeadDim / 16],
+                                                float (&m)[ScoreRows<G>::kPerLane],
+                                                float (&l_row)[ScoreRows<G>::kPerLane])
+{
+    using SR = ScoreRows<G>;
+    constexpr int kE = SR::kPerLane;
+    const int lane = t.lane;
+    const int n = lane & 15, kg = lane >> 4;  // score layout: token n, rows 4kg + e kStep
+    const int r = lane >> 4, c = lane & 15;   // value layout: token 4k + r, dims 8c..8c+7
+    const int h0 = t.kvh * G;
+    float my_kscale = 1.0f, my_vscale = 1.0f;
+
+    uint4 qa[4];
+    {
+        const int row = lane & 15;
+        const int g = row / SR::kStep;
+        const bool has = row % SR::kStep == 0 && g < G;
+        const uint16_t* qrow =
+            a.q + ((int64_t)t.b * a.num_q_heads + h0 + (has ? g : 0)) * kHeadDim;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            qa[i] = has ? *reinterpret_cast<const uint4*>(qrow + KV::q_dim(i, kg))
+                        : make_uint4(0, 0, 0, 0);
+    }
+    bool real[kE];  // the lane's e-th score row holds a query head
+#pragma unroll
+    for (int e = 0; e < kE; ++e)
+        real[e] = (4 * kg + e * SR::kStep) / SR::kStep < G;
+
+    // rows that hold no head keep zero weights; alpha starts at 1
+#pragma unroll
+    for (int x = lane; x < 16 * kPvPRow; x += kWave)
+        lds.p[x] = 0.0f;
+    if (lane < 16)
+        lds.alpha[lane] = 1.0f;
+
+    float lsum[kE];
+#pragma unroll
+    for (int e = 0; e < kE; ++e) {
+        m[e] = -INFINITY;
+        lsum[e] = 0.0f;
+    }
+#pragma unroll
+    for (int i = 0; i < kHeadDim / 16; ++i)
+        o[i] = floatx4_t{0.0f, 0.0f, 0.0f, 0.0f};
+
+    auto issue = [&](typename KV::Buf& buf, int i) {
+        const int64_t page = __builtin_amdgcn_readlane(my_page, i);
+        KV::load(buf, slab_base(a, a.k_pool, page, t.kvh), slab_base(a, a.v_pool, page, t.kvh),
+                 lane, a.row_bytes);
+    };
+
+    auto consume = [&](typename KV::Buf& buf, int i) {
+        floatx4_t sacc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8_t, qa[k]),
+                __builtin_bit_cast(bf16x8_t, KV::k_block(buf, k)), sacc, 0, 0, 0);
+
+        const int valid = t.seq_len - task_page(t, i) * kPageSize;  // >= 1 valid tokens
+        float sl = a.scale_log2;
+        if (KV::kScaled)
+            sl *= __int_as_float(__builtin_amdgcn_readlane(__float_as_int(my_kscale), i));
+        float s[kE], mx[kE];
+        bool grow = false;
+#pragma unroll
+        for (int e = 0; e < kE; ++e) {
+            s[e] = (n < valid) ? sacc[e * SR::kStep] * sl : -INFINITY;
+            mx[e] = row16_max(s[e]);  // finite: token 0 is valid
+            grow |= real[e] && mx[e] > m[e] + kMaxSlack;
+        }
+        wave_lds_sync();  // the previous page's tiles have been read
+        const bool rescale = __any(grow);
+        if (rescale) {
+#pragma unroll
+            for (int e = 0; e < kE; ++e) {
+                const float m_new = mx[e] > m[e] + kMaxSlack ? mx[e] : m[e];
+                const float alpha = exp2_fast(m[e] - m_new);  // 0 on the first page
+                lsum[e] *= alpha;
+                m[e] = m_new;
+                if (n == 0 && real[e])
+                    lds.alpha[4 * kg + e * SR::kStep] = alpha;
+            }
+        }
+        float vs = 1.0f;
+        if (KV::kScaled)
+            vs = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(my_vscale), i));
+#pragma unroll
+        for (int e = 0; e < kE; ++e) {
+            const float pexp = exp2_fast(s[e] - m[e]);
+            lsum[e] += pexp;
+            if (real[e])
+                lds.p[(4 * kg + e * SR::kStep) * kPvPRow + n] = pexp * vs;
+        }
+        // the page's values as [token][dim] rows; unread slots may hold NaN
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            uint4 v = KV::values_bf16(buf, k);
+            if (valid < kPageSize && 4 * k + r >= valid)
+                v = make_uint4(0, 0, 0, 0);
+            *reinterpret_cast<uint4*>(&lds.v[(4 * k + r) * kPvVRow + 8 * c]) = v;
+        }
+        wave_lds_sync();
+        if (rescale) {
+            const float al = lds.alpha[n];
+#pragma unroll
+            for (int i2 = 0; i2 < kHeadDim / 16; ++i2)
+                o[i2] *= al;
+        }
+        const float4 pp = *reinterpret_cast<const float4*>(&lds.p[n * kPvPRow + 4 * kg]);
+        short4_t p_hi, p_lo;
+        split_bf16(pp, p_hi, p_lo);
+        const uint16_t* vrow = &lds.v[(4 * kg + n / 4) * kPvVRow + 4 * (n % 4)];
+#pragma unroll
+        for (int i2 = 0; i2 < kHeadDim / 16; ++i2) {
+            const short4_t vt = lds_read_tr16(vrow + 16 * i2);
+            o[i2] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt, p_hi, o[i2], 0, 0, 0);
+            o[i2] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt, p_lo, o[i2], 0, 0, 0);
+        }
+    };
+
+    if (KV::kScaled && lane < t.count) {
+        const int64_t slab = (int64_t)my_page * a.num_kv_heads + t.kvh;
+        my_kscale = a.k_scale[slab];
+        my_vscale = a.v_scale[slab];
+    }
+    typename KV::Buf buf_a, buf_b;
+    stream_pages(t.count, buf_a, buf_b, issue, consume);
+#pragma unroll
+    for (int e = 0; e < kE; ++e)
+        l_row[e] = row16_sum(lsum[e]);
+}
+
+template <int G, bool CHECKED, typename KV, bool PERSISTENT>
+__global__ __launch_bounds__(kWave * kUnitWaves)
+__attribute__((amdgpu_waves_per_eu(G > 4 || PERSISTENT ? 2 : 3))) void split_pv(SplitArgs a)
+{
+    static_assert(G == 1 || G == 2 || G == 4 || G == 8 || G == 16, "query group of 1..16 heads");
+    using SR = ScoreRows<G>;
+    constexpr int kE = SR::kPerLane;
+    __shared__ __attribute__((aligned(16))) PvShared<G> sh;
+    extern __shared__ int plan[];
+
+    auto unit = [&](const SplitArgs& a, int b, int kvh, int s, bool owner) {
+        WaveTask t;
+        int32_t my_page;
+        if (!begin_unit<CHECKED>(a, t, my_page, b, kvh, s, owner)) {
+            write_zero_rows<G>(a, t);
+            return;
+        }
+        floatx4_t o[kHeadDim / 16];
+        float m[kE], l_row[kE];
+        attend_pages_pv<G, CHECKED, KV>(a, t, my_page, sh.wave[t.wave], o, m, l_row);
+        __syncthreads();  // every wavefront has left its page loop
+        // Lane 16q + j holds tile row j: the head (j / kStep) when it is one.
+        const int j = t.lane & 15, q = t.lane >> 4;
+        if (j % SR::kStep == 0 && j / SR::kStep < G) {
+            const int g = j / SR::kStep;
+#pragma unroll
+            for (int i = 0; i < kHeadDim / 16; ++i)
+                *reinterpret_cast<float4*>(&sh.unit.acc[t.wave][g][16 * i + 4 * q]) =
+                    make_float4(o[i][0], o[i][1], o[i][2], o[i][3]);
+        }
+        if ((t.lane & 15) == 0) {
+#pragma unroll
+            for (int e = 0; e < kE; ++e) {
+                const int row = 4 * q + e * SR::kStep;
+                if (row / SR::kStep < G) {
+                    sh.unit.m[t.wave][row / SR::kStep] = m[e];
+                    sh.unit.l[t.wave][row / SR::kStep] = l_row[e];
+                }
+            }
+        }
+        __syncthreads();
+        merge_unit<G>(a, t, sh.unit);
+    };
+    if (PERSISTENT)
+        run_persistent(a, a.num_kv_heads, plan, unit);
+    else  // one split per sequence: unit (b, kv head) = blockIdx.x
+        unit(a, blockIdx.x / a.num_kv_heads, blockIdx.x % a.num_kv_heads, 0, true);
+}
+
 // -------------------------------------------------------- merge kernel ---
 //
 // One work-group of four wavefronts per (b, h) of sequences with more than one
@@ -1244,10 +1503,14 @@ __global__ __launch_bounds__(kWave * kMergeWaves) void merge_splits(MergeArgs a)
 typedef void (*SplitKernel)(SplitArgs);
 
 // PERSISTENT: the kernel for runs with more than one split (persistent
-// work-groups taking units from the queue).
+// work-groups taking units from the queue).  pv: the P.V product on the
+// matrix cores.
 template <int G, bool CHECKED, bool PERSISTENT>
-SplitKernel pick(bool fp8, bool mfma, bool hp)
+SplitKernel pick(bool fp8, bool mfma, bool hp, bool pv)
 {
+    if (pv)
+        return fp8 ? split_pv<G, CHECKED, KvFp8, PERSISTENT>
+                   : split_pv<G, CHECKED, KvBf16, PERSISTENT>;
     if (hp)
         return fp8 ? split_mfma_hp<G, CHECKED, KvFp8, PERSISTENT>
                    : split_mfma_hp<G, CHECKED, KvBf16, PERSISTENT>;
@@ -1259,25 +1522,39 @@ SplitKernel pick(bool fp8, bool mfma, bool hp)
 }
 
 template <bool CHECKED, bool PERSISTENT>
-SplitKernel select_for_group(int G, bool fp8, bool mfma, bool hp)
+SplitKernel select_for_group(int G, bool fp8, bool mfma, bool hp, bool pv)
 {
     switch (G) {
-    case 1: return pick<1, CHECKED, PERSISTENT>(fp8, mfma, hp);
-    case 2: return pick<2, CHECKED, PERSISTENT>(fp8, mfma, hp);
-    case 4: return pick<4, CHECKED, PERSISTENT>(fp8, mfma, hp);
-    case 8: return pick<8, CHECKED, PERSISTENT>(fp8, mfma, hp);
+    case 1: return pick<1, CHECKED, PERSISTENT>(fp8, mfma, hp, pv);
+    case 2: return pick<2, CHECKED, PERSISTENT>(fp8, mfma, hp, pv);
+    case 4: return pick<4, CHECKED, PERSISTENT>(fp8, mfma, hp, pv);
+    case 8: return pick<8, CHECKED, PERSISTENT>(fp8, mfma, hp, pv);
+    case 16:  // only the matrix-core value pass holds 16 heads' accumulators
+        return fp8 ? split_pv<16, CHECKED, KvFp8, PERSISTENT>
+                   : split_pv<16, CHECKED, KvBf16, PERSISTENT>;
     default: return nullptr;
     }
 }
 
-SplitKernel select_split_kernel(int G, bool checked, bool fp8, bool mfma, bool hp,
+SplitKernel select_split_kernel(int G, bool checked, bool fp8, bool mfma, bool hp, bool pv,
                                bool persistent)
 {
     if (checked)
-        return persistent ? select_for_group<true, true>(G, fp8, mfma, hp)
-                          : select_for_group<true, false>(G, fp8, mfma, hp);
-    return persistent ? select_for_group<false, true>(G, fp8, mfma, hp)
-                      : select_for_group<false, false>(G, fp8, mfma, hp);
+        return persistent ? select_for_group<true, true>(G, fp8, mfma, hp, pv)
+                          : select_for_group<true, false>(G, fp8, mfma, hp, pv);
+    return persistent ? select_for_group<false, true>(G, fp8, mfma, hp, pv)
+                      : select_for_group<false, false>(G, fp8, mfma, hp, pv);
+}
+
+// Whether the four-wavefront units accumulate P.V on the matrix cores (the
+// default; measured against the vector-ALU value pass on one box: Qwen3-8B
+// step 166.9 -> 164.9 us, Qwen3-32B heads 179.1 -> 165.3 us, long tail 965 ->
+// 955 us, stragglers 473 -> 470 us, fp8 large batch and the TP = 8 share
+// within 1%), or with vector-ALU FMAs on request (RL_DA_PV_ON_VALU, and the
+// vector-ALU score path, which has its own value pass).
+bool uses_pv_mfma(const rl_da_config* cfg)
+{
+    return (cfg->flags & (RL_DA_PV_ON_VALU | RL_DA_SCORES_ON_VALU)) == 0;
 }
 
 // kv heads per head-parallel work-group: the largest divisor of Hkv up to 8
@@ -1318,7 +1595,7 @@ bool uses_head_parallel(const rl_da_config* cfg)
 {
     if (cfg->layout != RL_DA_LAYOUT_NHD ||
         (cfg->flags & (RL_DA_SCORES_ON_VALU | RL_DA_PER_HEAD_UNITS)) != 0 ||
-        heads_per_unit_for(cfg->num_kv_heads) < 2)
+        heads_per_unit_for(cfg->num_kv_heads) < 2 || cfg->num_q_heads > 8 * cfg->num_kv_heads)
         return false;
     const int st = cfg->split_tokens != 0 ? cfg->split_tokens
                                           : default_split_tokens(cfg, cfg->num_kv_heads);
@@ -1368,7 +1645,8 @@ rl_da_status check_config(const rl_da_config* cfg, int* split_tokens, int* split
         return RL_DA_ERR_INVALID_ARG;
     if (cfg->num_q_heads % cfg->num_kv_heads != 0)
         return RL_DA_ERR_INVALID_ARG;
-    if ((cfg->flags & ~(RL_DA_CHECKED | RL_DA_SCORES_ON_VALU | RL_DA_PER_HEAD_UNITS)) != 0)
+    if ((cfg->flags & ~(RL_DA_CHECKED | RL_DA_SCORES_ON_VALU | RL_DA_PER_HEAD_UNITS |
+                        RL_DA_PV_ON_VALU)) != 0)
         return RL_DA_ERR_INVALID_ARG;
     if (cfg->kv_dtype != RL_DA_KV_BF16 && cfg->kv_dtype != RL_DA_KV_FP8_E4M3)
         return RL_DA_ERR_INVALID_ARG;
@@ -1377,9 +1655,13 @@ rl_da_status check_config(const rl_da_config* cfg, int* split_tokens, int* split
         return RL_DA_ERR_INVALID_ARG;
     const int G = cfg->num_q_heads / cfg->num_kv_heads;
     if (cfg->head_dim != kHeadDim || cfg->page_size != kPageSize ||
-        (G != 1 && G != 2 && G != 4 && G != 8))
+        (G != 1 && G != 2 && G != 4 && G != 8 && G != 16))
         return RL_DA_ERR_UNSUPPORTED;
-    if (cfg->kv_dtype == RL_DA_KV_FP8_E4M3 && (cfg->flags & RL_DA_SCORES_ON_VALU) != 0)
+    // only the matrix-core value pass holds a 16-head group's accumulators; the
+    // vector-ALU score path serves bf16 pools only
+    if (G == 16 && !uses_pv_mfma(cfg))
+        return RL_DA_ERR_UNSUPPORTED;
+    if ((cfg->flags & RL_DA_SCORES_ON_VALU) != 0 && cfg->kv_dtype == RL_DA_KV_FP8_E4M3)
         return RL_DA_ERR_UNSUPPORTED;
     const bool hp = uses_head_parallel(cfg);
     // work units per (sequence, split)
@@ -1442,7 +1724,7 @@ rl_da_status init_handle(rl_decode_attn* h, const rl_da_config* cfg)
     for (int persistent = 0; persistent < 2; ++persistent)
         (persistent ? h->split_kernel_persistent : h->split_kernel) = select_split_kernel(
             G, (cfg->flags & RL_DA_CHECKED) != 0, cfg->kv_dtype == RL_DA_KV_FP8_E4M3, h->use_mfma,
-            h->head_parallel, persistent != 0);
+            h->head_parallel, !h->head_parallel && uses_pv_mfma(cfg), persistent != 0);
     if (hipGetDevice(&h->device) != hipSuccess)
         return RL_DA_ERR_HIP;
     // One persistent work-group per slot that can be resident with the

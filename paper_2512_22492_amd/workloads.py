@@ -65,6 +65,12 @@ CONFIGS.update({
     "qwen3_32b_step": dict(
         batch=64, num_q_heads=64, num_kv_heads=8, head_dim=128, page_size=16,
         lengths=("fixed", 4096), pool_factor=1.25, kv_dtype="bf16", seed=20251228),
+    # a group of 16 query heads per kv head: the Qwen3-235B-A22B attention
+    # layout (64 query heads, 4 kv heads), whose rollouts the paper also
+    # evaluates (Sec. 7.1) without stating head counts
+    "qwen3_235b_step": dict(
+        batch=64, num_q_heads=64, num_kv_heads=4, head_dim=128, page_size=16,
+        lengths=("fixed", 4096), pool_factor=1.25, kv_dtype="bf16", seed=20251229),
 })
 
 CONFIG_ORDER = ["tiny", "qwen3_8b_step", "long_tail", "straggler",

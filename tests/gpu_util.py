@@ -34,9 +34,37 @@ def run_gpu(p, *, flags=0, split_tokens=0, attn=None, stream=None):
     return out
 
 
-def oracle_ref(p, rows=None):
+def oracle_ref(p, rows=None, abs_values=False):
+    """The oracle's decode attention of problem p; with abs_values, over the
+    value pool of magnitudes |V| (same weights): M1 = sum w |v| / sum w."""
     h = p.host_arrays()
+    if abs_values:
+        h["v_pool"] = abs_value_host(p, h)
     return oracle.decode_attention(kv_dtype=KV[p.kv_dtype], rows=rows, **h)
+
+
+# The matrix-core value pass (the default of the four-wavefront units) feeds
+# each weight to the product as hi = bf16(p) plus lo = bf16(p - hi), which
+# carries p to 2^-16 relative, and normalises by the fp32 sum of the weights:
+# the result moves by at most 2^-16 M1 beyond fp32 rounding (the e4m3 case of
+# the analysis above with the residual term).
+PV_ROUND = 2.0 ** -16 * (1.0 + 2.0 ** -8)
+
+
+def uses_pv(p, flags):
+    """Whether a handle created with `flags` may take the matrix-core value
+    pass (token-major handles with head-parallel units do not; the allowance
+    applies to them too, as a bound)."""
+    return not flags & (binding.RL_DA_PV_ON_VALU | binding.RL_DA_SCORES_ON_VALU)
+
+
+def decode_extra(p, flags, rows=None):
+    """Allowance on top of one ulp for the decode path a handle with `flags`
+    takes: 0 for the vector-ALU value pass, PV_ROUND * M1 for the
+    matrix-core one."""
+    if not uses_pv(p, flags):
+        return 0.0
+    return PV_ROUND * oracle_ref(p, rows=rows, abs_values=True)
 
 
 def bf16_to_f64(t):

@@ -115,13 +115,17 @@ def test_token_major_pools_default_split():
     (dict(max_pages_per_seq=0), B.RL_DA_ERR_INVALID_ARG),
     (dict(split_tokens=-16), B.RL_DA_ERR_INVALID_ARG),
     (dict(flags=0x80), B.RL_DA_ERR_INVALID_ARG),
-    (dict(flags=0x8), B.RL_DA_ERR_INVALID_ARG),
+    (dict(flags=0x10), B.RL_DA_ERR_INVALID_ARG),
     (dict(kv_dtype=7), B.RL_DA_ERR_INVALID_ARG),
     (dict(layout=2), B.RL_DA_ERR_INVALID_ARG),
     (dict(head_dim=64), B.RL_DA_ERR_UNSUPPORTED),
     (dict(page_size=32), B.RL_DA_ERR_UNSUPPORTED),
     (dict(num_q_heads=24, num_kv_heads=8), B.RL_DA_ERR_UNSUPPORTED),   # G = 3
-    (dict(num_q_heads=128, num_kv_heads=8), B.RL_DA_ERR_UNSUPPORTED),  # G = 16
+    (dict(num_q_heads=256, num_kv_heads=8), B.RL_DA_ERR_UNSUPPORTED),  # G = 32
+    (dict(num_q_heads=128, num_kv_heads=8, flags=B.RL_DA_SCORES_ON_VALU),
+     B.RL_DA_ERR_UNSUPPORTED),                                          # G = 16, VALU scores
+    (dict(num_q_heads=128, num_kv_heads=8, flags=B.RL_DA_PV_ON_VALU),
+     B.RL_DA_ERR_UNSUPPORTED),                                          # G = 16, VALU values
     (dict(split_tokens=24), B.RL_DA_ERR_UNSUPPORTED),
     (dict(kv_dtype=B.RL_DA_KV_FP8_E4M3, flags=B.RL_DA_SCORES_ON_VALU), B.RL_DA_ERR_UNSUPPORTED),
     (dict(split_tokens=4112), B.RL_DA_ERR_UNSUPPORTED),

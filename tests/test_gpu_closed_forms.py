@@ -9,13 +9,16 @@ import torch
 from paper_2512_22492_amd import binding as B
 from paper_2512_22492_amd import workloads
 
-from gpu_util import (abs_value_host, bf16_to_f64, bf16_ulp, check_close, device, extend_extra,
-                      run_gpu)
+from gpu_util import (PV_ROUND, abs_value_host, bf16_to_f64, bf16_ulp, check_close, device,
+                      extend_extra, run_gpu, uses_pv)
 
 pytestmark = pytest.mark.gpu
 
 LAYOUTS = ["hnd", "nhd"]
 KVS = ["bf16", "fp8_e4m3"]
+# (Hq, Hkv, create flags): four heads per kv head on either value pass, and
+# sixteen (the matrix-core value pass only)
+HEADS = {"g4": (32, 8, 0), "g4valu": (32, 8, B.RL_DA_PV_ON_VALU), "g16": (64, 4, 0)}
 
 
 def problem(lengths, kv, layout, seed, hq=32, hkv=8, pool_factor=1.25):
@@ -59,11 +62,13 @@ def visible_values(p, b, kvh, upto=None):
     return v[bt[t // 16], kvh, t % 16, :]
 
 
+@pytest.mark.parametrize("heads", list(HEADS))
 @pytest.mark.parametrize("layout", LAYOUTS)
 @pytest.mark.parametrize("kv", KVS)
-def test_one_token_returns_its_value(kv, layout):
-    p = problem([1] * 16, kv, layout, seed=61)
-    got = bf16_to_f64(run_gpu(p))
+def test_one_token_returns_its_value(kv, layout, heads):
+    hq, hkv, flags = HEADS[heads]
+    p = problem([1] * 16, kv, layout, seed=61, hq=hq, hkv=hkv)
+    got = bf16_to_f64(run_gpu(p, flags=flags))
     G = p.num_q_heads // p.num_kv_heads
     for b in range(p.batch):
         for h in range(p.num_q_heads):
@@ -74,12 +79,14 @@ def test_one_token_returns_its_value(kv, layout):
                 assert np.all(np.abs(got[b, h] - want) <= bf16_ulp(want)), (b, h)
 
 
+@pytest.mark.parametrize("heads", list(HEADS))
 @pytest.mark.parametrize("layout", LAYOUTS)
 @pytest.mark.parametrize("kv", KVS)
 @pytest.mark.parametrize("how", ["equal_keys", "zero_scale"])
-def test_uniform_weights_give_the_mean(kv, layout, how):
+def test_uniform_weights_give_the_mean(kv, layout, how, heads):
+    hq, hkv, flags = HEADS[heads]
     lengths = [1, 16, 17, 300, 4096, 5000, 9000]
-    p = problem(lengths, kv, layout, seed=62)
+    p = problem(lengths, kv, layout, seed=62, hq=hq, hkv=hkv)
     if how == "equal_keys":
         # every key of every page the same row: all scores equal
         row = p.k_pool.reshape(-1, p.head_dim)[0].clone()
@@ -89,20 +96,28 @@ def test_uniform_weights_give_the_mean(kv, layout, how):
     else:
         p.scale = 0.0
     for split in (0, 1024):
-        got = bf16_to_f64(run_gpu(p, split_tokens=split))
+        got = bf16_to_f64(run_gpu(p, split_tokens=split, flags=flags))
         G = p.num_q_heads // p.num_kv_heads
         want = np.stack([[visible_values(p, b, h // G).mean(axis=0)
                           for h in range(p.num_q_heads)] for b in range(p.batch)])
-        print(check_close(got, want, "%s %s %s split %d" % (how, kv, layout, split)))
+        extra = 0.0
+        if uses_pv(p, flags):   # equal weights: M1 is the mean magnitude
+            extra = PV_ROUND * np.stack([[np.abs(visible_values(p, b, h // G)).mean(axis=0)
+                                          for h in range(p.num_q_heads)]
+                                         for b in range(p.batch)])
+        print(check_close(got, want, "%s %s %s split %d" % (how, kv, layout, split),
+                          extra_abs=extra))
 
 
+@pytest.mark.parametrize("heads", list(HEADS))
 @pytest.mark.parametrize("layout", LAYOUTS)
 @pytest.mark.parametrize("kv", KVS)
-def test_outputs_lie_in_the_convex_hull_of_the_values(kv, layout):
+def test_outputs_lie_in_the_convex_hull_of_the_values(kv, layout, heads):
+    hq, hkv, flags = HEADS[heads]
     lengths = [3, 100, 700, 2049]
-    p = problem(lengths, kv, layout, seed=63)
+    p = problem(lengths, kv, layout, seed=63, hq=hq, hkv=hkv)
     p.q.mul_(8.0)                        # peaked softmax: outputs near single values
-    got = bf16_to_f64(run_gpu(p))
+    got = bf16_to_f64(run_gpu(p, flags=flags))
     G = p.num_q_heads // p.num_kv_heads
     for b in range(p.batch):
         for h in range(p.num_q_heads):
@@ -146,11 +161,12 @@ def test_negative_and_zero_scales_match_the_oracle(layout):
     """The softmax scale is any finite number: a negative one turns the
     largest dot products into the smallest weights."""
     import oracle
-    from gpu_util import oracle_ref
+    from gpu_util import decode_extra, oracle_ref
     for scale in (-0.09, 0.0):
         p = problem([1, 17, 300, 4100], "bf16", layout, seed=66)
         p.scale = scale
-        print(check_close(bf16_to_f64(run_gpu(p)), oracle_ref(p), "decode scale %g" % scale))
+        print(check_close(bf16_to_f64(run_gpu(p)), oracle_ref(p), "decode scale %g" % scale,
+                          extra_abs=decode_extra(p, 0)))
         new, prior = [3, 70], [14, 200]
         pe = problem([a + b for a, b in zip(new, prior)], "bf16", layout, seed=67, hq=8, hkv=2)
         pe.scale = scale

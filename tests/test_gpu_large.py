@@ -10,8 +10,8 @@ from oracle import weight_sync as WS
 from paper_2512_22492_amd import binding as B
 from paper_2512_22492_amd import workloads
 
-from gpu_util import (KV, abs_value_host, bf16_to_f64, check_close, device, extend_extra,
-                      oracle_ref, run_gpu)
+from gpu_util import (KV, abs_value_host, bf16_to_f64, check_close, decode_extra, device,
+                      extend_extra, oracle_ref, run_gpu)
 
 pytestmark = pytest.mark.gpu
 
@@ -43,7 +43,8 @@ def test_decode_reads_pages_beyond_4gib(kv, layout):
     rows = np.array([(b, h) for b in range(len(lengths)) for h in (0, 5, 31)], dtype=np.int32)
     out = run_gpu(p)
     got = bf16_to_f64(out[torch.from_numpy(rows[:, 0]).long(), torch.from_numpy(rows[:, 1]).long()])
-    print(check_close(got, oracle_ref(p, rows=rows), "decode > 4 GiB %s %s" % (kv, layout)))
+    print(check_close(got, oracle_ref(p, rows=rows), "decode > 4 GiB %s %s" % (kv, layout),
+                      extra_abs=decode_extra(p, 0, rows=rows)))
 
 
 @pytest.mark.parametrize("layout", ["hnd", "nhd"])

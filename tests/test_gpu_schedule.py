@@ -12,7 +12,7 @@ import torch
 from paper_2512_22492_amd import binding as B
 from paper_2512_22492_amd import workloads
 
-from gpu_util import bf16_to_f64, check_close, device, oracle_ref, run_gpu
+from gpu_util import bf16_to_f64, check_close, decode_extra, device, oracle_ref, run_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -53,7 +53,8 @@ def test_large_batches_with_and_without_the_plan(batch, hq, hkv, flags):
     print("case batch", batch, "hq", hq, "hkv", hkv, "flags", flags, flush=True)
     p = problem(hq, hkv, short_lengths(batch, seed=batch + hq), seed=batch + hq)
     got = run_gpu(p, split_tokens=64, flags=flags)
-    print(check_close(bf16_to_f64(got), oracle_ref(p), "batch %d G=%d" % (batch, hq // hkv)))
+    print(check_close(bf16_to_f64(got), oracle_ref(p), "batch %d G=%d" % (batch, hq // hkv),
+                      extra_abs=decode_extra(p, flags)))
     rows = list(range(0, batch, 7))
     part = run_gpu(sub_problem(p, rows), split_tokens=64, flags=flags)
     assert torch.equal(part.view(torch.int16), got[rows].view(torch.int16))
@@ -71,7 +72,8 @@ def test_checked_mode_on_the_persistent_schedule(kv, layout):
         assert attn.unit_heads() == 1 and attn.split_info(p.max_pages)[1] > 1
         good = run_gpu(p, attn=attn)
         assert attn.check_error() == 0
-        print(check_close(bf16_to_f64(good), oracle_ref(p), "checked persistent " + kv + layout))
+        print(check_close(bf16_to_f64(good), oracle_ref(p), "checked persistent " + kv + layout,
+                          extra_abs=decode_extra(p, B.RL_DA_CHECKED)))
         others = [b for b in range(len(lengths)) if b not in (5, 123)]
         bad_table = p.block_table.clone()
         bad_table[123, 7] = p.num_pages + 5        # inside sequence 123
@@ -109,15 +111,19 @@ def test_degenerate_length_mixes(kv, layout, flags):
         padded = lengths + [0] * (500 - len(lengths))
         p = problem(8, 2, padded, seed=len(lengths), kv=kv, layout=layout, max_pages=width)
         assert p.max_pages > 16
-        got_padded = run_gpu(p, flags=flags, split_tokens=256)
-        got = run_gpu(sub_problem(p, list(range(len(lengths)))), flags=flags, split_tokens=256)
+        # one handle for both runs: the unit family (token-major pools) follows
+        # the handle's capacity, and results are batch-invariant for a handle
+        with B.DecodeAttention.for_problem(p, flags=flags, split_tokens=256) as attn:
+            got_padded = run_gpu(p, attn=attn)
+            got = run_gpu(sub_problem(p, list(range(len(lengths)))), attn=attn)
         assert torch.equal(got.view(torch.int16), got_padded[:len(lengths)].view(torch.int16))
         got = bf16_to_f64(got)
         assert np.all(bf16_to_f64(got_padded)[len(lengths):] == 0)
         if max(lengths) == 0:
             assert np.all(got == 0)
             continue
-        print(check_close(got, oracle_ref(sub_problem(p, list(range(len(lengths))))), name))
+        sub = sub_problem(p, list(range(len(lengths))))
+        print(check_close(got, oracle_ref(sub), name, extra_abs=decode_extra(sub, flags)))
         assert np.all(got[np.array(lengths) == 0] == 0)
 
 
@@ -131,7 +137,8 @@ def test_queue_is_reset_between_launches_of_any_shape():
     runs = [(long_tail, 256), (few, 256), (one_split, 256), (long_tail, 512), (few, 64)]
     fresh = [run_gpu(p, split_tokens=s) for p, s in runs]
     for p, s in runs:
-        print(check_close(bf16_to_f64(run_gpu(p, split_tokens=s)), oracle_ref(p), "queue"))
+        print(check_close(bf16_to_f64(run_gpu(p, split_tokens=s)), oracle_ref(p), "queue",
+                          extra_abs=decode_extra(p, 0)))
     handles = {s: B.DecodeAttention(8, 2, 64, max_pages, split_tokens=s) for s in (64, 256, 512)}
     try:
         for rep in range(3):
