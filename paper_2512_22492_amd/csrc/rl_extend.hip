@@ -28,13 +28,14 @@ namespace {
 // group g; the V^T operand in that order comes from the [key][dim] rows by
 // the LDS transpose read.  Row max, rescale and sum are therefore lane-local
 // but for two lane swaps per 64 keys.  P enters the PV product rounded to bf16
-// (relative error at most 2^-9 per weight, as in common flash-attention
-// kernels; an earlier two-term hi + lo split kept fp32-level accuracy at a
-// third more MFMAs and conversion work).  For bf16 pools l is the sum of the
-// same rounded weights, taken by the PV product against a block of ones, so
-// the output is a convex combination of the values with weights off by at
-// most 2^-8 relative in total; for e4m3 pools (whose packed weights carry the
-// page's v_scale) l sums the unrounded fp32 probabilities.
+// (relative error at most 2^-8 per weight: 8 significant bits, round to
+// nearest, as in common flash-attention kernels; an earlier two-term hi + lo
+// split kept fp32-level accuracy at a third more MFMAs and conversion work).
+// For bf16 pools l is the sum of the same rounded weights, taken by the PV
+// product against a block of ones, so the output is a convex combination of
+// the values with weights within 2^-7 relative of the exact ones; for e4m3
+// pools (whose packed weights carry the page's v_scale) l sums the unrounded
+// fp32 probabilities.
 //
 // Work-group order: consecutive work-groups go to the eight XCDs in turn,
 // and the tiles of one (sequence, kv head) read the same keys, so they are
