@@ -111,8 +111,9 @@ def parse_args():
                     help="P.V product of the split-K kernel: the matrix cores (default), or "
                          "vector-ALU FMAs (not for 16 query heads per kv head)")
     ap.add_argument("--split-tokens", type=int, default=0)
-    ap.add_argument("--layout", choices=["hnd", "nhd"], default="hnd",
-                    help="pool layout: [page][kv head][slot][dim] or [page][slot][kv head][dim]")
+    ap.add_argument("--layout", choices=["hnd", "nhd", "hnd_kv"], default="hnd",
+                    help="pool layout: [page][kv head][slot][dim], [page][slot][kv head][dim], "
+                         "or [page][kv head][K|V][slot][dim] in one allocation")
     ap.add_argument("--per-head-units", action="store_true",
                     help="token-major pools: four-wavefront units per kv head")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -633,10 +634,7 @@ def main():
     base = workloads.make_config(args.config, device=dev, layout=args.layout)
     replicas = [base]
     for _ in range(1, max(1, args.replicas)):
-        replicas.append(workloads.DecodeProblem(**{
-            **base.__dict__, "k_pool": base.k_pool.clone(), "v_pool": base.v_pool.clone(),
-            "k_scale": None if base.k_scale is None else base.k_scale.clone(),
-            "v_scale": None if base.v_scale is None else base.v_scale.clone()}))
+        replicas.append(base.clone_pools())
     if args.op == "append":
         print(json.dumps(bench_append(args, base, torch.cuda.current_stream())), flush=True)
         return

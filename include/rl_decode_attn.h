@@ -21,6 +21,11 @@
  *                (layout RL_DA_LAYOUT_HND), or
  *                [num_pages][page_size][Hkv][head_dim]         (RL_DA_LAYOUT_NHD)
  *   v_pool       same as k_pool
+ *                or, with RL_DA_LAYOUT_HND_KV, one allocation
+ *                [num_pages][Hkv][2][page_size][head_dim] holding a (page, kv
+ *                head)'s key slab and then its value slab: k_pool points at
+ *                its start and v_pool exactly one slab (page_size * head_dim
+ *                elements) further
  *   k_scale      [num_pages][Hkv] fp32, fp8 pools only: a stored code c of
  *   v_scale      slab (page, kvh) stands for e4m3(c) * scale[page][kvh]
  *   block_table  [batch][max_pages] int32 (row stride max_pages)
@@ -92,9 +97,18 @@ typedef enum { RL_DA_KV_BF16 = 0, RL_DA_KV_FP8_E4M3 = 1 } rl_da_kv_dtype;
 
 /* Order of a page's (kv head, token slot) rows in the pools.  HND keeps each
  * (page, kv head) slab contiguous; NHD keeps each token slot's kv heads
- * together (the page-major layout many serving engines allocate).  Same page
- * stride either way; the fp8 scales are [num_pages][Hkv] in both. */
-typedef enum { RL_DA_LAYOUT_HND = 0, RL_DA_LAYOUT_NHD = 1 } rl_da_layout;
+ * together (the page-major layout many serving engines allocate); HND_KV
+ * puts a (page, kv head)'s value slab right after its key slab in one
+ * allocation, so a decode step reads one contiguous block per (page, kv head)
+ * (twice the slab: 4 KiB for e4m3, 8 KiB for bf16) instead of two.  The fp8
+ * scales are [num_pages][Hkv] in every layout.  With HND_KV every entry point
+ * that takes k_pool and v_pool returns INVALID_ARG unless v_pool is k_pool
+ * plus one slab. */
+typedef enum {
+    RL_DA_LAYOUT_HND = 0,
+    RL_DA_LAYOUT_NHD = 1,
+    RL_DA_LAYOUT_HND_KV = 2
+} rl_da_layout;
 
 /* create() flag: kernels check block-table entries and lengths on device. */
 #define RL_DA_CHECKED 0x1u
@@ -216,7 +230,7 @@ rl_da_status rl_decode_attn_unit_heads(const rl_decode_attn* h, int32_t* kv_head
  * entries of pages 0 .. (L_b-1)/page_size in [0, num_pages).  Needs no
  * handle and no workspace; enqueues one kernel on `stream`.  bf16 or e4m3
  * pools (k_scale and v_scale non-NULL exactly for e4m3, as for decode),
- * either rl_da_layout, head_dim 128, page_size 16 and Hq/Hkv in
+ * any rl_da_layout, head_dim 128, page_size 16 and Hq/Hkv in
  * {1, 2, 4, 8, 16} only (else UNSUPPORTED); q, the pools and out 16-byte
  * aligned.
  */
@@ -253,7 +267,7 @@ rl_da_status rl_extend_attn(const void* q, const int32_t* q_start, int32_t max_q
  * skipped (nothing written) and, when device_error is non-NULL, reported in
  * that int32 device word with RL_DA_DEVERR_LENGTH_TOO_LONG /
  * RL_DA_DEVERR_PAGE_OUT_OF_RANGE (bits are only ever set).  Needs no handle;
- * enqueues one kernel on `stream`.  Pools in either rl_da_layout;
+ * enqueues one kernel on `stream`.  Pools in any rl_da_layout;
  * head_dim 128 and page_size 16 only (else UNSUPPORTED); k_new, v_new and the
  * pools 16-byte aligned; k_scale and v_scale non-NULL exactly for e4m3.
  */

@@ -27,7 +27,8 @@ KV_DTYPES = {"bf16": RL_DA_KV_BF16, "fp8_e4m3": RL_DA_KV_FP8_E4M3}
 
 RL_DA_LAYOUT_HND = 0
 RL_DA_LAYOUT_NHD = 1
-LAYOUTS = {"hnd": RL_DA_LAYOUT_HND, "nhd": RL_DA_LAYOUT_NHD}
+RL_DA_LAYOUT_HND_KV = 2
+LAYOUTS = {"hnd": RL_DA_LAYOUT_HND, "nhd": RL_DA_LAYOUT_NHD, "hnd_kv": RL_DA_LAYOUT_HND_KV}
 
 RL_DA_CHECKED = 0x1
 RL_DA_SCORES_ON_VALU = 0x2
@@ -199,14 +200,15 @@ def _pool_shape(layout, num_pages, num_kv_heads, page_size, head_dim):
     return (num_pages, num_kv_heads, page_size, head_dim)
 
 
-def _check_tensor(name, t, *, dtype=None, shape=None, ndim=None, device=None):
-    """Raises ValueError unless t is a contiguous torch tensor of the given
+def _check_tensor(name, t, *, dtype=None, shape=None, ndim=None, device=None,
+                  contiguous=True):
+    """Raises ValueError unless t is a (contiguous) torch tensor of the given
     dtype, shape (None entries match anything) and device."""
     if not hasattr(t, "data_ptr") or not hasattr(t, "is_contiguous"):
         raise ValueError("%s must be a torch tensor" % name)
     if dtype is not None and t.dtype not in (dtype if isinstance(dtype, tuple) else (dtype,)):
         raise ValueError("%s has dtype %s, expected %s" % (name, t.dtype, dtype))
-    if not t.is_contiguous():
+    if contiguous and not t.is_contiguous():
         raise ValueError("%s must be contiguous" % name)
     if ndim is not None and t.dim() != ndim:
         raise ValueError("%s must have %d dimensions, has shape %s" % (name, ndim, tuple(t.shape)))
@@ -226,12 +228,23 @@ def _check_pools(k_pool, v_pool, k_scale, v_scale, *, kv_dtype, layout, num_kv_h
     fp32 [num_pages, num_kv_heads] scales exactly for e4m3.  Returns num_pages."""
     import torch
     elt = torch.bfloat16 if kv_dtype == RL_DA_KV_BF16 else torch.uint8
-    _check_tensor("k_pool", k_pool, dtype=elt, ndim=4, device=device)
+    paired = layout == RL_DA_LAYOUT_HND_KV
+    _check_tensor("k_pool", k_pool, dtype=elt, ndim=4, device=device, contiguous=not paired)
     P = int(k_pool.shape[0])
     want = _pool_shape("nhd" if layout == RL_DA_LAYOUT_NHD else "hnd", P, num_kv_heads,
                        page_size, head_dim)
-    _check_tensor("k_pool", k_pool, shape=want)
-    _check_tensor("v_pool", v_pool, dtype=elt, shape=want, device=device)
+    _check_tensor("k_pool", k_pool, shape=want, contiguous=not paired)
+    _check_tensor("v_pool", v_pool, dtype=elt, shape=want, device=device,
+                  contiguous=not paired)
+    if paired:
+        # views of one [P, Hkv, 2, page, D] allocation: key slab, then value slab
+        slab = page_size * head_dim
+        strides = (num_kv_heads * 2 * slab, 2 * slab, head_dim, 1)
+        if tuple(k_pool.stride()) != strides or tuple(v_pool.stride()) != strides:
+            raise ValueError("hnd_kv pools must be the [:, :, 0] and [:, :, 1] views of one "
+                             "contiguous [P, Hkv, 2, page, D] tensor")
+        if v_pool.data_ptr() != k_pool.data_ptr() + slab * k_pool.element_size():
+            raise ValueError("hnd_kv: v_pool must start one slab after k_pool")
     if kv_dtype == RL_DA_KV_BF16:
         if k_scale is not None or v_scale is not None:
             raise ValueError("bf16 pools take no k_scale / v_scale")

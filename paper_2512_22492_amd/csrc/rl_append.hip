@@ -135,6 +135,8 @@ rl_da_status rl_kv_append(const void* k_new, const void* v_new, void* k_pool, vo
     const bool fp8 = kv_dtype == RL_DA_KV_FP8_E4M3;
     if (fp8 != (k_scale != nullptr) || fp8 != (v_scale != nullptr))
         return RL_DA_ERR_INVALID_ARG;
+    if (!pools_paired(layout, k_pool, v_pool, fp8 ? 1 : 2))
+        return RL_DA_ERR_INVALID_ARG;
     PoolStrides ps;
     if (!pool_strides(layout, num_kv_heads, fp8 ? 1 : 2, &ps))
         return RL_DA_ERR_INVALID_ARG;

@@ -30,8 +30,18 @@ typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
 inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
+// RL_DA_LAYOUT_HND_KV keeps both pools in one allocation: the value pool must
+// start one slab after the key pool (elt-byte elements).  Other layouts take
+// any two pools.
+inline bool pools_paired(int32_t layout, const void* k_pool, const void* v_pool, int32_t elt)
+{
+    return layout != RL_DA_LAYOUT_HND_KV ||
+           (const uint8_t*)v_pool == (const uint8_t*)k_pool + kPageSize * kHeadDim * elt;
+}
+
 // Byte strides of a pool of elt-byte elements: per page, per kv head within a
-// page, per token slot within a (page, kv head) slab.
+// page, per token slot within a (page, kv head) slab.  Both pools use the
+// same strides from their own base.
 struct PoolStrides {
     int64_t page;
     int32_t head;
@@ -45,6 +55,12 @@ inline bool pool_strides(int32_t layout, int32_t num_kv_heads, int32_t elt, Pool
     s->page = (int64_t)num_kv_heads * kPageSize * row;
     if (layout == RL_DA_LAYOUT_HND) {
         s->head = kPageSize * row;
+        s->row = row;
+        return true;
+    }
+    if (layout == RL_DA_LAYOUT_HND_KV) {  // K slab, then V slab, per (page, kv head)
+        s->page *= 2;
+        s->head = 2 * kPageSize * row;
         s->row = row;
         return true;
     }

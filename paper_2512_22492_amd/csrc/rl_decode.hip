@@ -1802,6 +1802,8 @@ rl_da_status enqueue_run(rl_decode_attn* h, const void* q, const void* k_pool,
     const bool fp8 = cfg.kv_dtype == RL_DA_KV_FP8_E4M3;
     if (fp8 != (k_scale != nullptr) || fp8 != (v_scale != nullptr))
         return RL_DA_ERR_INVALID_ARG;
+    if (!pools_paired(cfg.layout, k_pool, v_pool, fp8 ? 1 : 2))
+        return RL_DA_ERR_INVALID_ARG;
     if (batch == 0)
         return RL_DA_OK;
 

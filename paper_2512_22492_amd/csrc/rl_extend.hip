@@ -617,6 +617,8 @@ rl_da_status rl_extend_attn(const void* q, const int32_t* q_start, int32_t max_q
     if (!aligned16(q) || !aligned16(k_pool) || !aligned16(v_pool) || !aligned16(out))
         return RL_DA_ERR_INVALID_ARG;
     const bool fp8 = kv_dtype == RL_DA_KV_FP8_E4M3;
+    if (!pools_paired(layout, k_pool, v_pool, fp8 ? 1 : 2))
+        return RL_DA_ERR_INVALID_ARG;
     PoolStrides ps;
     if (!pool_strides(layout, num_kv_heads, fp8 ? 1 : 2, &ps))
         return RL_DA_ERR_INVALID_ARG;

@@ -11,9 +11,12 @@ The shapes follow the paper's rollout workload (Sec. 7.1: Qwen3-8B rollouts,
 beyond 4k tokens).  The paper's datasets are not used; attention cost depends
 only on shapes and lengths, and values are N(0, 1).
 
-Pool layout is [num_pages][num_kv_heads][page_size][head_dim] ("hnd"), or
-[num_pages][page_size][num_kv_heads][head_dim] ("nhd": the same values, only
-stored in that order); pages are drawn from one random permutation of the
+Pool layout is [num_pages][num_kv_heads][page_size][head_dim] ("hnd"),
+[num_pages][page_size][num_kv_heads][head_dim] ("nhd"), or one allocation
+[num_pages][num_kv_heads][2][page_size][head_dim] holding each (page, kv
+head)'s key slab and then its value slab ("hnd_kv"; k_pool and v_pool are
+views of it): the same values, only stored in that order.  Pages are drawn
+from one random permutation of the
 whole pool and sequence b takes the next ceil(L_b / page_size) entries for its
 logical pages 0, 1, ...
 """
@@ -98,6 +101,7 @@ class DecodeProblem:
     block_table: torch.Tensor   # int32 [B, max_pages]
     seq_lens: torch.Tensor      # int32 [B]
     pad_page: int               # page index written into unused table slots
+    kv_pool: Optional[torch.Tensor] = None  # "hnd_kv": [P, Hkv, 2, page, D]; k/v_pool view it
 
     @property
     def num_pages(self) -> int:
@@ -127,10 +131,27 @@ class DecodeProblem:
     def to(self, device) -> "DecodeProblem":
         def mv(t):
             return None if t is None else t.to(device)
+        if self.kv_pool is not None:   # keep each value slab next to its key slab
+            kv = self.kv_pool.to(device)
+            k_pool, v_pool = kv[:, :, 0], kv[:, :, 1]
+        else:
+            kv, k_pool, v_pool = None, mv(self.k_pool), mv(self.v_pool)
         return dataclasses.replace(
-            self, q=mv(self.q), k_pool=mv(self.k_pool), v_pool=mv(self.v_pool),
+            self, q=mv(self.q), k_pool=k_pool, v_pool=v_pool, kv_pool=kv,
             k_scale=mv(self.k_scale), v_scale=mv(self.v_scale),
             block_table=mv(self.block_table), seq_lens=mv(self.seq_lens))
+
+    def clone_pools(self) -> "DecodeProblem":
+        """The same problem over copies of the K/V pools and slab scales."""
+        if self.kv_pool is not None:
+            kv = self.kv_pool.clone()
+            k_pool, v_pool = kv[:, :, 0], kv[:, :, 1]
+        else:
+            kv, k_pool, v_pool = None, self.k_pool.clone(), self.v_pool.clone()
+        return dataclasses.replace(
+            self, k_pool=k_pool, v_pool=v_pool, kv_pool=kv,
+            k_scale=None if self.k_scale is None else self.k_scale.clone(),
+            v_scale=None if self.v_scale is None else self.v_scale.clone())
 
     def host_arrays(self) -> dict:
         """numpy views for the oracle: bf16 as uint16 bits, e4m3 as uint8."""
@@ -139,11 +160,13 @@ class DecodeProblem:
             if t.dtype == torch.bfloat16:
                 return t.view(torch.int16).numpy().view(np.uint16)
             return t.numpy()
+        # "hnd_kv" views copy out as head-major pools
+        layout = "hnd" if self.layout == "hnd_kv" else self.layout
         out = dict(q_bits=bits(self.q), k_pool=bits(self.k_pool),
                    v_pool=bits(self.v_pool),
                    block_table=self.block_table.cpu().numpy(),
                    seq_lens=self.seq_lens.cpu().numpy(),
-                   num_kv_heads=self.num_kv_heads, scale=self.scale, layout=self.layout)
+                   num_kv_heads=self.num_kv_heads, scale=self.scale, layout=layout)
         if self.kv_dtype != "bf16":
             out["k_scale"] = self.k_scale.cpu().numpy()
             out["v_scale"] = self.v_scale.cpu().numpy()
@@ -248,8 +271,8 @@ def make_problem(name: str = "custom", *, batch: int, num_q_heads: int,
                  layout: str = "hnd", device="cpu") -> DecodeProblem:
     """Build one seeded problem.  `lengths` is a distribution spec or an array.
     The values do not depend on `layout`."""
-    if layout not in ("hnd", "nhd"):
-        raise ValueError("layout must be 'hnd' or 'nhd'")
+    if layout not in ("hnd", "nhd", "hnd_kv"):
+        raise ValueError("layout must be 'hnd', 'nhd' or 'hnd_kv'")
     rng = np.random.default_rng(seed)
     if isinstance(lengths, (list, tuple)) and lengths and isinstance(lengths[0], str):
         L = draw_lengths(rng, batch, lengths)
@@ -275,9 +298,13 @@ def make_problem(name: str = "custom", *, batch: int, num_q_heads: int,
         v_scale = vs.view(P, num_kv_heads)
     else:
         raise ValueError("kv_dtype must be 'bf16' or 'fp8_e4m3'")
+    kv_pool = None
     if layout == "nhd":
         k_pool = k_pool.transpose(1, 2).contiguous()
         v_pool = v_pool.transpose(1, 2).contiguous()
+    elif layout == "hnd_kv":
+        kv_pool = torch.stack([k_pool, v_pool], dim=2)
+        k_pool, v_pool = kv_pool[:, :, 0], kv_pool[:, :, 1]
     if scale is None:
         scale = 1.0 / math.sqrt(head_dim)
     return DecodeProblem(
@@ -287,7 +314,7 @@ def make_problem(name: str = "custom", *, batch: int, num_q_heads: int,
         v_pool=v_pool, k_scale=k_scale, v_scale=v_scale,
         block_table=torch.from_numpy(table).to(device),
         seq_lens=torch.from_numpy(L.astype(np.int32)).to(device),
-        pad_page=pad)
+        pad_page=pad, kv_pool=kv_pool)
 
 
 def make_config(name: str, device="cpu", seed: Optional[int] = None,

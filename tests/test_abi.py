@@ -117,7 +117,7 @@ def test_token_major_pools_default_split():
     (dict(flags=0x80), B.RL_DA_ERR_INVALID_ARG),
     (dict(flags=0x10), B.RL_DA_ERR_INVALID_ARG),
     (dict(kv_dtype=7), B.RL_DA_ERR_INVALID_ARG),
-    (dict(layout=2), B.RL_DA_ERR_INVALID_ARG),
+    (dict(layout=3), B.RL_DA_ERR_INVALID_ARG),
     (dict(head_dim=64), B.RL_DA_ERR_UNSUPPORTED),
     (dict(page_size=32), B.RL_DA_ERR_UNSUPPORTED),
     (dict(num_q_heads=24, num_kv_heads=8), B.RL_DA_ERR_UNSUPPORTED),   # G = 3

@@ -40,7 +40,7 @@ def host_bits(t):
     return t.view(torch.int16).numpy().view(np.uint16)
 
 
-@pytest.mark.parametrize("layout", ["hnd", "nhd"])
+@pytest.mark.parametrize("layout", ["hnd", "nhd", "hnd_kv"])
 @pytest.mark.parametrize("kv", ["bf16", "fp8_e4m3"])
 def test_append_steps_match_oracle_byte_for_byte(kv, layout):
     lengths = [0, 1, 14, 15, 16, 31, 100, 4095, 4096, 5000]
@@ -57,7 +57,7 @@ def test_append_steps_match_oracle_byte_for_byte(kv, layout):
         B.kv_append(p, k.to(device()), v.to(device()))
         ok, ov, oks, ovs = oracle.kv_append(host_bits(k), host_bits(v), ok, ov,
                                             h["block_table"], lens, kv_dtype=KV[kv],
-                                            k_scale=oks, v_scale=ovs, layout=layout)
+                                            k_scale=oks, v_scale=ovs, layout=h["layout"])
         p.seq_lens += 1
         torch.cuda.synchronize()
         got = p.host_arrays()
@@ -70,7 +70,7 @@ def test_append_steps_match_oracle_byte_for_byte(kv, layout):
     ref, m1 = [oracle.decode_attention(
         got["q_bits"], ok, v, h["block_table"], p.seq_lens.cpu().numpy(),
         num_kv_heads=p.num_kv_heads, scale=p.scale, kv_dtype=KV[kv], k_scale=oks,
-        v_scale=ovs, layout=layout)
+        v_scale=ovs, layout=h["layout"])
         for v in (ov, ov & (np.uint16(0x7FFF) if ov.dtype == np.uint16 else np.uint8(0x7F)))]
     print(check_close(bf16_to_f64(run_gpu(p)), ref, "attention after appends " + kv,
                       extra_abs=PV_ROUND * m1))
@@ -118,6 +118,7 @@ def test_append_argument_validation():
     assert call(head_dim=64) == B.RL_DA_ERR_UNSUPPORTED
     assert call(page_size=32) == B.RL_DA_ERR_UNSUPPORTED
     assert call(kv_dtype=5) == B.RL_DA_ERR_INVALID_ARG
-    assert call(layout=2) == B.RL_DA_ERR_INVALID_ARG
+    assert call(layout=3) == B.RL_DA_ERR_INVALID_ARG
+    assert call(layout=2) == B.RL_DA_ERR_INVALID_ARG   # two pools, not one slab apart
     assert call(batch=0) == B.RL_DA_OK
     torch.cuda.synchronize()

@@ -45,7 +45,7 @@ def oracle_extend(p, q, q_start, abs_values=False):
                                    q_start.cpu().numpy(), h["k_pool"], v_pool,
                                    h["block_table"], h["seq_lens"],
                                    num_kv_heads=p.num_kv_heads, scale=p.scale,
-                                   layout=p.layout, **kw)
+                                   layout=h["layout"], **kw)
 
 
 def check_extend(p, q, q_start, got, what):
@@ -280,3 +280,18 @@ def test_extend_fp8_pools_match_oracle(hq, hkv, case, layout):
                                    kv="fp8_e4m3")
     got = run_extend(p, q, q_start, max(new))
     check_extend(p, q, q_start, got, "extend fp8 %s G=%d case %d" % (layout, hq // hkv, case))
+
+
+@pytest.mark.parametrize("kv", ["bf16", "fp8_e4m3"])
+@pytest.mark.parametrize("hq,hkv", [(8, 2), (32, 8), (64, 4)])
+def test_extend_hnd_kv_pools_match_oracle_and_the_hnd_result(kv, hq, hkv):
+    """Key and value slabs side by side in one allocation: the same bits as
+    head-major pools holding the same values."""
+    new, prior = CASES[0]
+    pk, q, q_start = extend_problem(new, prior, seed=60 + hq, hq=hq, hkv=hkv, layout="hnd_kv",
+                                    kv=kv)
+    ph, _, _ = extend_problem(new, prior, seed=60 + hq, hq=hq, hkv=hkv, kv=kv)
+    got = run_extend(pk, q, q_start, max(new))
+    check_extend(pk, q, q_start, got, "extend hnd_kv %s G=%d" % (kv, hq // hkv))
+    same = run_extend(ph, q, q_start, max(new))
+    assert torch.equal(got.view(torch.int16), same.view(torch.int16))

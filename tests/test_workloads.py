@@ -123,3 +123,22 @@ def test_kv_bytes_of_qwen3_8b_step():
     } | dict(batch=2, seed=0))
     assert p.kv_bytes() == 2 * 4096 * 8 * 128 * 2 * 2
     assert expected == 1073741824
+
+
+@pytest.mark.parametrize("kv", ["bf16", "fp8_e4m3"])
+def test_hnd_kv_layout_views_one_allocation(kv):
+    """'hnd_kv' problems hold the head-major values in one [P, Hkv, 2, 16, D]
+    allocation, value slab right after key slab, through copies and moves."""
+    kw = dict(batch=3, num_q_heads=8, num_kv_heads=2, lengths=[5, 40, 17], kv_dtype=kv, seed=3)
+    h = workloads.make_problem("x", layout="hnd", **kw)
+    p = workloads.make_problem("x", layout="hnd_kv", **kw)
+    for q in (p, p.to("cpu"), p.clone_pools()):
+        assert q.kv_pool.shape == (q.num_pages, 2, 2, 16, 128) and q.kv_pool.is_contiguous()
+        slab = 16 * 128 * q.k_pool.element_size()
+        assert q.k_pool.data_ptr() == q.kv_pool.data_ptr()
+        assert q.v_pool.data_ptr() == q.k_pool.data_ptr() + slab
+        assert torch.equal(q.k_pool, h.k_pool) and torch.equal(q.v_pool, h.v_pool)
+        arrays = q.host_arrays()
+        assert arrays["layout"] == "hnd" and arrays["k_pool"].shape == (q.num_pages, 2, 16, 128)
+    c = p.clone_pools()
+    assert c.kv_pool.data_ptr() != p.kv_pool.data_ptr()
