@@ -551,6 +551,7 @@ __device__ __forceinline__ void stream_pages(int n, Buf& a, Buf& b, Issue issue,
 // bf16 slab: 4 KiB, four 16-byte loads per lane for K and for V.
 struct KvBf16 {
     static constexpr bool kScaled = false;
+    static constexpr bool kStagedK = false;
     struct Buf {
         uint4 k[4];
         uint4 v[4];
@@ -621,11 +622,47 @@ struct KvFp8 {
         v[4] = a2.x; v[5] = a2.y; v[6] = a3.x; v[7] = a3.y;
     }
     __device__ static void clear_values(Buf& b, int k) { b.v[k] = make_uint2(0, 0); }
-    // the eight codes as exact bf16 (slab scale not applied)
-    __device__ static uint4 values_bf16(const Buf& b, int k)
+};
+
+// The same e4m3 slab read as whole rows, for the matrix-core value pass: lane
+// l loads codes 16(l%8)..16(l%8)+15 of tokens l/8 and 8 + l/8, for K and for
+// V, so each load instruction covers eight complete 128-byte rows.  K reaches
+// the score layout above (k[0], k[1]) through the wavefront's staging tile
+// (kStagedK) before its k-blocks are taken; V is widened to bf16 as it is
+// staged.  On gfx950 this reads the pool measurably faster than the
+// score-layout loads, which touch sixteen rows per instruction.
+struct KvFp8Rows {
+    static constexpr bool kScaled = true;
+    static constexpr bool kStagedK = true;
+    struct Buf {
+        uint4 k[2];
+        uint4 v[2];
+    };
+    __device__ static int q_dim(int i, int kg) { return KvFp8::q_dim(i, kg); }
+    __device__ static void load(Buf& b, const uint8_t* ks, const uint8_t* vs, int lane, int row)
     {
-        return make_uint4(cvt2<false>(b.v[k].x), cvt2<true>(b.v[k].x), cvt2<false>(b.v[k].y),
-                          cvt2<true>(b.v[k].y));
+        const int off = (lane >> 3) * row + 16 * (lane & 7);
+        b.k[0] = load_stream16(ks + off);
+        b.k[1] = load_stream16(ks + off + 8 * row);
+        b.v[0] = load_stream16(vs + off);
+        b.v[1] = load_stream16(vs + off + 8 * row);
+    }
+    // k-block i once k[] holds the score layout
+    __device__ static uint4 k_block(const Buf& b, int i)
+    {
+        const uint4& w = b.k[i >> 1];
+        const uint32_t lo = (i & 1) ? w.z : w.x;
+        const uint32_t hi = (i & 1) ? w.w : w.y;
+        return make_uint4(KvFp8::cvt2<false>(lo), KvFp8::cvt2<true>(lo),
+                          KvFp8::cvt2<false>(hi), KvFp8::cvt2<true>(hi));
+    }
+    // codes 16(l%8) + 8h .. +7 of token 8j + l/8 as exact bf16
+    __device__ static uint4 values_bf16(const Buf& b, int j, int h)
+    {
+        const uint32_t lo = h ? b.v[j].z : b.v[j].x;
+        const uint32_t hi = h ? b.v[j].w : b.v[j].y;
+        return make_uint4(KvFp8::cvt2<false>(lo), KvFp8::cvt2<true>(lo),
+                          KvFp8::cvt2<false>(hi), KvFp8::cvt2<true>(hi));
     }
 };
 
@@ -1202,6 +1239,7 @@ __global__ __launch_bounds__(kWave * kUnitWaves) void split_valu_bf16(SplitArgs 
 // staged; v_scale multiplies p before the split.
 
 constexpr int kPvVRow = kHeadDim + 16;  // bf16 per staged value row (288 bytes)
+constexpr int kPvKRowBytes = 144;        // staged e4m3 key row pitch (bytes)
 constexpr int kPvPRow = 20;             // floats per staged probability row (80 bytes)
 
 struct PvWaveLds {
@@ -1302,6 +1340,31 @@ __device__ __forceinline__ void attend_pages_pv(const SplitArgs& a, const WaveTa
     };
 
     auto consume = [&](typename KV::Buf& buf, int i) {
+        const int valid = t.seq_len - task_page(t, i) * kPageSize;  // >= 1 valid tokens
+        if constexpr (KV::kStagedK) {
+            // whole key rows pass through the value tile into the score
+            // layout; the values replace them there once they are read
+            wave_lds_sync();  // the previous page's tiles have been read
+            uint8_t* tile = reinterpret_cast<uint8_t*>(lds.v);
+            const int tr = lane >> 3, tc = 16 * (lane & 7);
+            *reinterpret_cast<uint4*>(tile + tr * kPvKRowBytes + tc) = buf.k[0];
+            *reinterpret_cast<uint4*>(tile + (8 + tr) * kPvKRowBytes + tc) = buf.k[1];
+            wave_lds_sync();
+            buf.k[0] = *reinterpret_cast<const uint4*>(tile + n * kPvKRowBytes + 16 * kg);
+            buf.k[1] = *reinterpret_cast<const uint4*>(tile + n * kPvKRowBytes + 64 + 16 * kg);
+            wave_lds_sync();
+            // the page's values as [token][dim] rows; unread slots may hold NaN
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                uint4 v0 = KV::values_bf16(buf, j, 0), v1 = KV::values_bf16(buf, j, 1);
+                if (valid < kPageSize && 8 * j + tr >= valid) {
+                    v0 = make_uint4(0, 0, 0, 0);
+                    v1 = v0;
+                }
+                *reinterpret_cast<uint4*>(&lds.v[(8 * j + tr) * kPvVRow + tc]) = v0;
+                *reinterpret_cast<uint4*>(&lds.v[(8 * j + tr) * kPvVRow + tc + 8]) = v1;
+            }
+        }
         floatx4_t sacc = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
         for (int k = 0; k < 4; ++k)
@@ -1309,7 +1372,6 @@ __device__ __forceinline__ void attend_pages_pv(const SplitArgs& a, const WaveTa
                 __builtin_bit_cast(bf16x8_t, qa[k]),
                 __builtin_bit_cast(bf16x8_t, KV::k_block(buf, k)), sacc, 0, 0, 0);
 
-        const int valid = t.seq_len - task_page(t, i) * kPageSize;  // >= 1 valid tokens
         float sl = a.scale_log2;
         if (KV::kScaled)
             sl *= __int_as_float(__builtin_amdgcn_readlane(__float_as_int(my_kscale), i));
@@ -1321,7 +1383,8 @@ __device__ __forceinline__ void attend_pages_pv(const SplitArgs& a, const WaveTa
             mx[e] = row16_max(s[e]);  // finite: token 0 is valid
             grow |= real[e] && mx[e] > m[e] + kMaxSlack;
         }
-        wave_lds_sync();  // the previous page's tiles have been read
+        if constexpr (!KV::kStagedK)
+            wave_lds_sync();  // the previous page's tiles have been read
         const bool rescale = __any(grow);
         if (rescale) {
 #pragma unroll
@@ -1345,12 +1408,14 @@ __device__ __forceinline__ void attend_pages_pv(const SplitArgs& a, const WaveTa
                 lds.p[(4 * kg + e * SR::kStep) * kPvPRow + n] = pexp * vs;
         }
         // the page's values as [token][dim] rows; unread slots may hold NaN
+        if constexpr (!KV::kStagedK) {
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            uint4 v = KV::values_bf16(buf, k);
-            if (valid < kPageSize && 4 * k + r >= valid)
-                v = make_uint4(0, 0, 0, 0);
-            *reinterpret_cast<uint4*>(&lds.v[(4 * k + r) * kPvVRow + 8 * c]) = v;
+            for (int k = 0; k < 4; ++k) {
+                uint4 v = KV::values_bf16(buf, k);
+                if (valid < kPageSize && 4 * k + r >= valid)
+                    v = make_uint4(0, 0, 0, 0);
+                *reinterpret_cast<uint4*>(&lds.v[(4 * k + r) * kPvVRow + 8 * c]) = v;
+            }
         }
         wave_lds_sync();
         if (rescale) {
@@ -1509,7 +1574,7 @@ template <int G, bool CHECKED, bool PERSISTENT>
 SplitKernel pick(bool fp8, bool mfma, bool hp, bool pv)
 {
     if (pv)
-        return fp8 ? split_pv<G, CHECKED, KvFp8, PERSISTENT>
+        return fp8 ? split_pv<G, CHECKED, KvFp8Rows, PERSISTENT>
                    : split_pv<G, CHECKED, KvBf16, PERSISTENT>;
     if (hp)
         return fp8 ? split_mfma_hp<G, CHECKED, KvFp8, PERSISTENT>
@@ -1530,7 +1595,7 @@ SplitKernel select_for_group(int G, bool fp8, bool mfma, bool hp, bool pv)
     case 4: return pick<4, CHECKED, PERSISTENT>(fp8, mfma, hp, pv);
     case 8: return pick<8, CHECKED, PERSISTENT>(fp8, mfma, hp, pv);
     case 16:  // only the matrix-core value pass holds 16 heads' accumulators
-        return fp8 ? split_pv<16, CHECKED, KvFp8, PERSISTENT>
+        return fp8 ? split_pv<16, CHECKED, KvFp8Rows, PERSISTENT>
                    : split_pv<16, CHECKED, KvBf16, PERSISTENT>;
     default: return nullptr;
     }
