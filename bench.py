@@ -6,9 +6,11 @@ batch.  Inputs are seeded synthetic tensors resident in HBM before timing
 starts.  Prints one JSON line:
   value      = KV bytes read per step / step time  (GB/s, the metric's unit)
   roofline   = the split-K kernel's achieved bytes/s against 8 TB/s: the
-               step's algorithmic bytes over the kernel's mean duration, from
-               HIP events attached to each of its launches in a second pass
-               of K steps (the first pass, which gives value, has none)
+               step's algorithmic bytes over the kernel's mean duration --
+               the timed pass's GPU time per step (an event pair around the K
+               back-to-back steps) when a step is that kernel alone, else HIP
+               events attached to each of its launches in a second pass of K
+               steps (the first pass, which gives value, has none)
   cpu_baseline = the fp64 oracle timed on the host on a sample of the step
   parity     = the GPU output of that sample against the oracle's
 """
