@@ -123,11 +123,12 @@ __global__ __launch_bounds__(64 * kUnitWaves) void page_read_kernel(PageReadArgs
             for (int r = 0; r < 4; ++r)
                 acc ^= k[r].x ^ k[r].y ^ k[r].z ^ k[r].w ^ v[r].x ^ v[r].y ^ v[r].z ^ v[r].w;
         } else {
-            const int koff8 = (lane & 15) * 128 + 16 * (lane >> 4);
+            // e4m3 slabs: K and V both as whole 128-byte rows, eight per
+            // instruction, as the decode kernel reads them
             uint4 k[2], v[2];
 #pragma unroll
             for (int r = 0; r < 2; ++r) {
-                k[r] = load_stream16(a.k_pool + slab + koff8 + 64 * r);
+                k[r] = load_stream16(a.k_pool + slab + voff + 1024 * r);
                 v[r] = load_stream16(a.v_pool + slab + voff + 1024 * r);
             }
 #pragma unroll

@@ -47,10 +47,14 @@ constexpr int kRowBlocks = 2;                      // 16-row blocks per wavefron
 constexpr int kTileRows = kUnitWaves * kRowBlocks * 16;
 constexpr int kStageKeys = 64;                     // keys per LDS stage (4 pages)
 constexpr int kStagePages = kStageKeys / kPageSize;
-// K and V [key][dim] rows padded to 288 bytes: the 16-byte K operand reads
-// and the transposed V reads of an instruction then meet no bank conflict
-// (measured: half the LDS cycles of 272-byte rows).
-constexpr int kKRow = kHeadDim + 16;
+// K and V stage tiles are [key][dim] rows of 256 bytes whose sixteen 16-byte
+// chunks are stored at position chunk ^ chunk_swizzle(row).  Sixteen
+// consecutive rows then put one chunk at sixteen different positions (the
+// K operand reads), and eight consecutive rows put two adjacent chunks at
+// sixteen (the transposed V reads), so neither meets a bank conflict, while
+// every four rows stay one contiguous kilobyte (what a wavefront's direct
+// global-to-LDS load fills).
+__device__ __forceinline__ int chunk_swizzle(int row) { return ((row & 7) << 1) | ((row >> 3) & 1); }
 
 typedef short short4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) short4_t lds_short4_t;
@@ -189,10 +193,42 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
 {
     static_assert(G >= 1 && G <= 16 && 16 % G == 0, "16-row blocks hold whole groups");
     constexpr int kTileTok = kTileRows / G;
-    __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][kStageKeys][kKRow];
-    __shared__ __attribute__((aligned(16))) uint16_t v_lds[2][kStageKeys][kKRow];
+    // Two stage buffers per operand, as separate arrays: the compiler then
+    // tells the buffer being read from the one a direct load is filling and
+    // waits only where a wait is needed.
+    __shared__ __attribute__((aligned(16))) uint16_t k_lds0[kStageKeys][kHeadDim];
+    __shared__ __attribute__((aligned(16))) uint16_t k_lds1[kStageKeys][kHeadDim];
+    __shared__ __attribute__((aligned(16))) uint16_t v_lds0[kStageKeys][kHeadDim];
+    __shared__ __attribute__((aligned(16))) uint16_t v_lds1[kStageKeys][kHeadDim];
     // e4m3 pools: (k_scale, v_scale) of the stage's four pages
     __shared__ __attribute__((aligned(16))) float2 scale_lds[2][kStagePages];
+    // A stage buffer is named by a type (bf16: the direct loads need it
+    // static) or by an int (e4m3: staged through registers).
+    typedef uint16_t Tile[kStageKeys][kHeadDim];
+    auto buf_index = [](auto sel) -> int {
+        if constexpr (std::is_integral<decltype(sel)>::value)
+            return sel;
+        else
+            return decltype(sel)::value;
+    };
+    auto k_tile = [&](auto sel) -> Tile& {
+        if constexpr (std::is_integral<decltype(sel)>::value)
+            return sel ? k_lds1 : k_lds0;
+        else if constexpr (decltype(sel)::value == 0)
+            return k_lds0;
+        else
+            return k_lds1;
+    };
+    auto v_tile = [&](auto sel) -> Tile& {
+        if constexpr (std::is_integral<decltype(sel)>::value)
+            return sel ? v_lds1 : v_lds0;
+        else if constexpr (decltype(sel)::value == 0)
+            return v_lds0;
+        else
+            return v_lds1;
+    };
+    using Buf0 = std::integral_constant<int, 0>;
+    using Buf1 = std::integral_constant<int, 1>;
 
     // Work-group g runs on XCD g % 8.  Pairs (sequence, kv head) are dealt
     // to the XCDs in turn, pair p to XCD p % 8 with all its tiles, so the
@@ -216,7 +252,7 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
     // (the K staging buffer is free until the first stage is staged)
     const int b = sequence_at_rank(a.seq_lens, a.max_pages * kPageSize,
                                    (int)(gridDim.x / T / a.num_kv_heads), bk / a.num_kv_heads,
-                                   reinterpret_cast<uint8_t*>(&k_lds[0][0][0]), (int)sizeof(k_lds));
+                                   reinterpret_cast<uint8_t*>(&k_lds0[0][0]), (int)sizeof(k_lds0));
     const int q0 = a.q_start[b];
     // lengths clamped to what the table row can hold, new tokens to the length
     const int L = min(a.seq_lens[b], a.max_pages * kPageSize);
@@ -272,19 +308,20 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
             o[rb][db] = floatx4_t{0.0f, 0.0f, 0.0f, 0.0f};
     }
 
-    // Staging.  bf16 pools: thread t moves dims 8(t%16) .. +7 of key rows
-    // t/16 + 16r, r = 0..3 (slot t/16 of page r of the stage): 16 threads per
-    // whole key row, so that each staging write instruction covers four whole
-    // rows (every LDS bank once per row).  e4m3 pools (128-byte rows): thread
-    // t moves the codes of dims 16(t%8) .. +15 of keys 2(t/8) and 2(t/8) + 1
-    // (16-byte loads; whole-row staging would take 8-byte ones), widened to
-    // bf16 as they are staged.
+    // Staging.  bf16 pools: direct global-to-LDS loads, no registers: lane l
+    // of wavefront w fills chunk position l%16 of key row 16r + 4w + l/16
+    // (slot 4w + l/16 of page r of the stage), r = 0..3, so that each load
+    // instruction fills four whole rows, one contiguous kilobyte; the lane
+    // reads the chunk the swizzle puts there.  A key past the sequence end
+    // reads the sequence's last key instead (finite; its weight is 0 and its
+    // score is masked to -inf).  e4m3 pools (128-byte rows): thread t loads
+    // the codes of dims 16(t%8) .. +15 of keys 2(t/8) and 2(t/8) + 1 into
+    // registers and widens them to bf16 as it stages them (16-byte loads;
+    // whole-row staging would take 8-byte ones); value rows past the end are
+    // zeroed.
     //
-    // Loads are unconditional, so that nothing between a load and the staging
-    // of its data waits for it: page indices past the sequence are clamped to
-    // its last page, so a key past the end reads a slot of a page the sequence
-    // owns and is discarded (its value row is overwritten with zeros, its
-    // scores are masked to -inf; the clamped page's scales are finite).
+    // Loads are unconditional: page indices past the sequence are clamped to
+    // its last page (whose scales are finite).
     constexpr int kRowsPerThread = FP8 ? 2 : kStagePages;
     const int st_row = FP8 ? 2 * (threadIdx.x / 8) : threadIdx.x / 16;  // first key row
     const int st_col = FP8 ? 16 * (threadIdx.x % 8) : 8 * (threadIdx.x % 16);  // first dim
@@ -315,20 +352,41 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
         }
     };
     bool live[kRowsPerThread];
-    auto fetch = [&](int stage, const int* pg) {
+    // The tiles of one (sequence, kv head) read the same keys from one L2, so
+    // K/V loads keep the default cache policy (2.5x fewer HBM bytes than
+    // non-temporal loads).
+    auto fetch = [&](int stage, const int* pg) {  // e4m3: into registers
 #pragma unroll
         for (int r = 0; r < kRowsPerThread; ++r) {
             const int row = slot_row(r);
             live[r] = stage * kStageKeys + row < L;
-            const int64_t off = (int64_t)(FP8 ? pg[0] : pg[r]) * a.page_bytes + st_off +
+            const int64_t off = (int64_t)pg[0] * a.page_bytes + st_off +
                                 (int64_t)(row % kPageSize) * a.row_bytes;
-            kr[r] = load_stream16(a.k_pool + off);
-            vr[r] = load_stream16(a.v_pool + off);
+            kr[r] = *reinterpret_cast<const uint4*>(a.k_pool + off);
+            vr[r] = *reinterpret_cast<const uint4*>(a.v_pool + off);
         }
-        if (FP8) {
-            const int64_t slab = (int64_t)pg[1] * a.num_kv_heads + kvh;
-            ksr = a.k_scale[slab];
-            vsr = a.v_scale[slab];
+        const int64_t slab = (int64_t)pg[1] * a.num_kv_heads + kvh;
+        ksr = a.k_scale[slab];
+        vsr = a.v_scale[slab];
+    };
+    typedef __attribute__((address_space(3))) void lds_void;
+    typedef __attribute__((address_space(1))) void global_void;
+    const int dma_slot = 4 * wave + lane / 16;  // key row within its page
+    const int dma_chunk = (lane % 16) ^ chunk_swizzle(dma_slot);
+    const int dead_slot = (L - 1) % kPageSize;
+    auto dma = [&](int stage, const int* pg, auto sel) {  // bf16: into the stage tiles
+#pragma unroll
+        for (int r = 0; r < kStagePages; ++r) {
+            const bool in = stage * kStageKeys + r * kPageSize + dma_slot < L;
+            const int64_t off = (int64_t)pg[r] * a.page_bytes + (int64_t)kvh * a.head_bytes +
+                                (int64_t)(in ? dma_slot : dead_slot) * a.row_bytes +
+                                16 * dma_chunk;
+            __builtin_amdgcn_global_load_lds((global_void*)(a.k_pool + off),
+                                             (lds_void*)&k_tile(sel)[r * kPageSize + 4 * wave][0],
+                                             16, 0, 0);
+            __builtin_amdgcn_global_load_lds((global_void*)(a.v_pool + off),
+                                             (lds_void*)&v_tile(sel)[r * kPageSize + 4 * wave][0],
+                                             16, 0, 0);
         }
     };
     // 16 e4m3 codes to 16 bf16 (exact), in order.
@@ -342,49 +400,59 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
         lo = make_uint4(cvt(c.x, F{}), cvt(c.x, T{}), cvt(c.y, F{}), cvt(c.y, T{}));
         hi = make_uint4(cvt(c.z, F{}), cvt(c.z, T{}), cvt(c.w, F{}), cvt(c.w, T{}));
     };
-    auto stash = [&](int buf) {
+    auto stash = [&](auto sel) {  // e4m3: widened codes at their swizzled chunks
 #pragma unroll
         for (int r = 0; r < kRowsPerThread; ++r) {
             const int row = slot_row(r);
-            uint4* krow = reinterpret_cast<uint4*>(&k_lds[buf][row][st_col]);
-            uint4* vrow = reinterpret_cast<uint4*>(&v_lds[buf][row][st_col]);
-            if (FP8) {
-                uint4 lo, hi;
-                widen(kr[r], lo, hi);
-                krow[0] = lo;
-                krow[1] = hi;
-                widen(vr[r], lo, hi);
-                vrow[0] = lo;
-                vrow[1] = hi;
-                if (!live[r]) {  // slots past the sequence end may hold NaN
-                    vrow[0] = make_uint4(0, 0, 0, 0);
-                    vrow[1] = make_uint4(0, 0, 0, 0);
-                }
-            } else {
-                krow[0] = kr[r];
-                vrow[0] = vr[r];
-                if (!live[r])  // slots past the sequence end may hold NaN
-                    vrow[0] = make_uint4(0, 0, 0, 0);
+            const int sw = chunk_swizzle(row), c0 = st_col / 8;
+            uint4* k0 = reinterpret_cast<uint4*>(&k_tile(sel)[row][8 * (c0 ^ sw)]);
+            uint4* k1 = reinterpret_cast<uint4*>(&k_tile(sel)[row][8 * ((c0 + 1) ^ sw)]);
+            uint4* v0 = reinterpret_cast<uint4*>(&v_tile(sel)[row][8 * (c0 ^ sw)]);
+            uint4* v1 = reinterpret_cast<uint4*>(&v_tile(sel)[row][8 * ((c0 + 1) ^ sw)]);
+            uint4 lo, hi;
+            widen(kr[r], lo, hi);
+            *k0 = lo;
+            *k1 = hi;
+            widen(vr[r], lo, hi);
+            if (!live[r]) {  // slots past the sequence end may hold NaN
+                lo = make_uint4(0, 0, 0, 0);
+                hi = lo;
             }
+            *v0 = lo;
+            *v1 = hi;
         }
-        if (FP8 && threadIdx.x < kStagePages)
-            scale_lds[buf][threadIdx.x] = make_float2(ksr, vsr);
+        if (threadIdx.x < kStagePages)
+            scale_lds[buf_index(sel)][threadIdx.x] = make_float2(ksr, vsr);
     };
 
     stage_pages(0, pages_next);
-    fetch(0, pages_next);
+    if constexpr (FP8)
+        fetch(0, pages_next);
+    else
+        dma(0, pages_next, Buf0{});
     stage_pages(1, pages_next);
     // One stage; stages that cannot cross a query position (all but the
-    // last one or two of a tile) are compiled without the causal mask.
-    auto stage = [&](const int j, auto masked_t) {
+    // last one or two of a tile) are compiled without the causal mask.  sel:
+    // the stage buffer (j % 2).
+    auto stage = [&](const int j, auto masked_t, auto sel) __attribute__((always_inline)) {
         constexpr bool masked = decltype(masked_t)::value;
-        const int buf = j & 1;
-        stash(buf);
-        if (j + 1 < nstages) {
-            fetch(j + 1, pages_next);
-            stage_pages(j + 2, pages_next);
+        const int buf = buf_index(sel);
+        if constexpr (FP8) {
+            stash(sel);
+            if (j + 1 < nstages) {
+                fetch(j + 1, pages_next);
+                stage_pages(j + 2, pages_next);
+            }
+            __syncthreads();
+        } else {
+            // this stage's direct loads have landed (the barrier waits for
+            // them) and every wavefront is done with the other buffer
+            __syncthreads();
+            if (j + 1 < nstages) {
+                dma(j + 1, pages_next, std::integral_constant<int, 1 - decltype(sel)::value>{});
+                stage_pages(j + 2, pages_next);
+            }
         }
-        __syncthreads();
 
         // Score multiplier (scale * log2 e, times k_scale) and value scale
         // of the stage's four pages; a page past the sequence carries the
@@ -401,6 +469,24 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
                 vsc[kb] = ps.y;
             }
         }
+
+        // The lane's byte offsets into the stage tiles, the same for both
+        // buffers (each buffer's base folds into the LDS instructions'
+        // offset field).  They are recomputed in every stage from an opaque
+        // copy of the lane index: kept live across the loop, one set per
+        // unrolled stage body, they pushed the kernel past the register
+        // budget.
+        int ln = lane;
+        asm volatile("" : "+v"(ln));
+        const int li = ln & 15, lg = ln >> 4;
+        // K operand: row 16kb + li, dims 32ks + 8lg .. +7, at chunk
+        // (4ks + lg) ^ chunk_swizzle(li)
+        int koff[4];
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks)
+            koff[ks] = li * 256 + 16 * ((4 * ks + lg) ^ chunk_swizzle(li));
+        const char* ktile = reinterpret_cast<const char*>(&k_tile(sel)[0][0]);
+        const char* vtile = reinterpret_cast<const char*>(&v_tile(sel)[0][0]);
 
         // S^T for the stage's four 16-key blocks: lane holds row i16, keys
         // 16kb + 4g4 + jj.
@@ -420,7 +506,7 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb) {
                 const uint4 kv =
-                    *reinterpret_cast<const uint4*>(&k_lds[buf][16 * kb + i16][32 * ks + 8 * g4]);
+                    *reinterpret_cast<const uint4*>(ktile + 16 * kb * 256 + koff[ks]);
 #pragma unroll
                 for (int rb = 0; rb < kRowBlocks; ++rb)
                     sacc[rb][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
@@ -529,11 +615,17 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
         }
         // O^T += V^T P^T: lane holds dims 16db + 4g4 + jj of row i16.  The V^T
         // operand of the next (db, kh) is read before this one's MFMAs.
+        // Lane i16 + 16g4 reads row 32kh + 4g4 + i16/4 (and the row 16
+        // below, same swizzle), dims 16db + 4(i16 % 4) .. +3: chunk
+        // 2db + (i16 % 4)/2, half i16 % 2.
+        const int vrow = 4 * lg + (li >> 2), vsw = chunk_swizzle(vrow);
         auto vt_operand = [&](int step) {
             const int db = step >> 1, kh = step & 1;
-            const uint16_t* vp = &v_lds[buf][32 * kh + 4 * g4 + (i16 >> 2)][16 * db + 4 * (i16 & 3)];
+            const int voff = vrow * 256 + 16 * ((2 * db + ((li & 3) >> 1)) ^ vsw) + 8 * (li & 1);
+            const uint16_t* vp =
+                reinterpret_cast<const uint16_t*>(vtile + 32 * kh * 256 + voff);
             const uint2 va = lds_read_transposed(vp);
-            const uint2 vb = lds_read_transposed(vp + 16 * kKRow);
+            const uint2 vb = lds_read_transposed(vp + 16 * kHeadDim);
             return make_uint4(va.x, va.y, vb.x, vb.y);
         };
         __builtin_amdgcn_s_setprio(1);
@@ -565,11 +657,26 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
         }
         __builtin_amdgcn_s_setprio(0);
     };
+    // Stage j uses buffer j % 2.  bf16: stages run in pairs, so that each
+    // body names its buffers statically.
     int j = 0;
-    for (; j < min(first_masked_stage, nstages); ++j)
-        stage(j, std::false_type{});
-    for (; j < nstages; ++j)
-        stage(j, std::true_type{});
+    auto run = [&](int end, auto masked_t) {
+        if constexpr (FP8) {
+            for (; j < end; ++j)
+                stage(j, masked_t, j & 1);
+        } else {
+            if (j < end && (j & 1) != 0)
+                stage(j++, masked_t, Buf1{});
+            for (; j + 1 < end; j += 2) {
+                stage(j, masked_t, Buf0{});
+                stage(j + 1, masked_t, Buf1{});
+            }
+            if (j < end)
+                stage(j++, masked_t, Buf0{});
+        }
+    };
+    run(min(first_masked_stage, nstages), std::false_type{});
+    run(nstages, std::true_type{});
 
     // out[row] = O[row] / l[row]; lane holds row i16, dims 16db + 4g4 + jj.
 #pragma unroll
