@@ -1522,22 +1522,40 @@ __global__ __launch_bounds__(kWave * kMergeWaves) void merge_splits(MergeArgs a)
     __shared__ float part[kMergeWaves][kHeadDim + 1];
     const int64_t row = blockIdx.x;  // b * Hq + h
     const int b = (int)(row / a.num_q_heads);
-    const int L = min(a.seq_lens[b], a.max_pages * kPageSize);
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const float* ml = a.ws_ml + row * a.num_splits * 2;
+    const float* acc = a.ws_acc + row * a.num_splits * kHeadDim + 2 * lane;
+    // The length and the first loads of both passes go out together (every
+    // split index below num_splits lies inside the row's partials), so the
+    // common case takes one round trip to memory; entries past the
+    // sequence's own splits are read but not used.
+    const int len = a.seq_lens[b];
+    const float m_first = lane < a.num_splits ? ml[2 * lane] : -INFINITY;
+    float2 ml_first = make_float2(0.0f, 0.0f), v_first = make_float2(0.0f, 0.0f);
+    if (wave < a.num_splits) {
+        ml_first = *reinterpret_cast<const float2*>(ml + 2 * wave);
+        v_first = *reinterpret_cast<const float2*>(acc + (int64_t)wave * kHeadDim);
+    }
+    const int L = min(len, a.max_pages * kPageSize);
     const int npages = L > 0 ? (L + kPageSize - 1) / kPageSize : 0;
     const int n = (npages + a.split_pages - 1) / a.split_pages;
     if (n < 2)
         return;  // finished by the split kernel
-    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-    const float* ml = a.ws_ml + row * a.num_splits * 2;
-    float M = -INFINITY;
-    for (int s = lane; s < n; s += kWave)
+    float M = lane < n ? m_first : -INFINITY;
+    for (int s = lane + kWave; s < n; s += kWave)
         M = fmaxf(M, ml[2 * s]);
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1)
         M = fmaxf(M, __shfl_xor(M, off));
+    // wavefront w: splits w, w+4, ... in order
     float den = 0.0f, num0 = 0.0f, num1 = 0.0f;
-    const float* acc = a.ws_acc + row * a.num_splits * kHeadDim + 2 * lane;
-    for (int s = wave; s < n; s += kMergeWaves) {
+    if (wave < n) {
+        const float w = exp2_fast(ml_first.x - M);
+        den = fmaf(w, ml_first.y, den);
+        num0 = fmaf(w, v_first.x, num0);
+        num1 = fmaf(w, v_first.y, num1);
+    }
+    for (int s = wave + kMergeWaves; s < n; s += kMergeWaves) {
         const float w = exp2_fast(ml[2 * s] - M);
         den = fmaf(w, ml[2 * s + 1], den);
         const float2 v = *reinterpret_cast<const float2*>(acc + (int64_t)s * kHeadDim);
