@@ -446,12 +446,9 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
             __syncthreads();
         } else {
             // this stage's direct loads have landed (the barrier waits for
-            // them) and every wavefront is done with the other buffer
+            // them) and every wavefront is done with the other buffer, which
+            // the next stage's loads fill once the score products are issued
             __syncthreads();
-            if (j + 1 < nstages) {
-                dma(j + 1, pages_next, std::integral_constant<int, 1 - decltype(sel)::value>{});
-                stage_pages(j + 2, pages_next);
-            }
         }
 
         // Score multiplier (scale * log2 e, times k_scale) and value scale
@@ -515,6 +512,14 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
             }
         }
         __builtin_amdgcn_s_setprio(0);
+        // bf16: the next stage's direct loads, issued after the K operand
+        // reads so that their LDS writes do not compete with them
+        if constexpr (!FP8) {
+            if (j + 1 < nstages) {
+                dma(j + 1, pages_next, std::integral_constant<int, 1 - decltype(sel)::value>{});
+                stage_pages(j + 2, pages_next);
+            }
+        }
         // Probabilities (masked only in stages that can cross a query
         // position; rows past the tile's tokens score 0 and stay finite) and
         // O^T += V^T P^T: lane holds dims 16db + 4g4 + jj of row i16.
