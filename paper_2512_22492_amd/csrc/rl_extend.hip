@@ -322,9 +322,11 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
     //
     // Loads are unconditional: page indices past the sequence are clamped to
     // its last page (whose scales are finite).
-    constexpr int kRowsPerThread = FP8 ? 2 : kStagePages;
-    const int st_row = FP8 ? 2 * (threadIdx.x / 8) : threadIdx.x / 16;  // first key row
-    const int st_col = FP8 ? 16 * (threadIdx.x % 8) : 8 * (threadIdx.x % 16);  // first dim
+    // e4m3 register staging: thread t holds key rows st_row, st_row + 1,
+    // codes of dims st_col .. st_col + 15
+    constexpr int kRowsPerThread = 2;
+    const int st_row = 2 * (threadIdx.x / 8);
+    const int st_col = 16 * (threadIdx.x % 8);
     const int npages = (L + kPageSize - 1) / kPageSize;  // >= 1 here
     // The table row's address is uniform; held in vector registers, its
     // loads are vector loads, counted with the K/V loads and waited for at
@@ -333,12 +335,11 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
     typedef __attribute__((address_space(1))) const int32_t global_i32;
     global_i32* bt = (global_i32*)(a.block_table + (int64_t)b * a.max_pages);
     asm volatile("" : "+v"(bt));
-    constexpr int kElt = FP8 ? 1 : 2;
-    const int64_t st_off = (int64_t)kvh * a.head_bytes + kElt * st_col;
-    uint4 kr[kRowsPerThread], vr[kRowsPerThread];  // bf16 dims or e4m3 codes
+    const int64_t st_off = (int64_t)kvh * a.head_bytes + st_col;
+    uint4 kr[kRowsPerThread], vr[kRowsPerThread];  // e4m3 codes
     float ksr = 1.0f, vsr = 1.0f;                  // e4m3: scales of page t % 4
     // Key row (within the stage) of the thread's staging slot r.
-    auto slot_row = [&](int r) { return FP8 ? st_row + r : r * kPageSize + st_row; };
+    auto slot_row = [&](int r) { return st_row + r; };
     // The table entries of a stage are read one stage ahead, so that its K/V
     // loads do not wait on a table load: bf16, page r of the stage for slot
     // r; e4m3, the page of the thread's key pair (and page t % 4 for the
