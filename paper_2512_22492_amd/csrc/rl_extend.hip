@@ -181,7 +181,8 @@ struct ExtendArgs {
     int32_t num_kv_heads;
     int32_t max_pages;
     int32_t num_tiles;          // ceil(max_q_per_seq / tile tokens)
-    float scale_log2;
+    float scale_log2;           // |scale| * log2(e)
+    uint32_t q_sign;            // 0x80008000 for a negative scale: Q enters negated
 };
 
 // FP8: e4m3 pools.  Codes are staged as exact bf16 (scale 1); a page's
@@ -280,9 +281,14 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
             a.q + ((int64_t)(q0 + (row_real[rb] ? qi : 0)) * a.num_q_heads + h0 + r % G) *
                       kHeadDim;
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks)
-            qb[rb][ks] = row_real[rb] ? *reinterpret_cast<const uint4*>(qrow + 32 * ks + 8 * g4)
-                                      : make_uint4(0, 0, 0, 0);
+        for (int ks = 0; ks < 4; ++ks) {
+            uint4 v = *reinterpret_cast<const uint4*>(qrow + 32 * ks + 8 * g4);
+            v.x ^= a.q_sign;
+            v.y ^= a.q_sign;
+            v.z ^= a.q_sign;
+            v.w ^= a.q_sign;
+            qb[rb][ks] = row_real[rb] ? v : make_uint4(0, 0, 0, 0);
+        }
     }
     const int tile_last = min(tok0 + kTileTok, n_new) - 1;
     const int nkeys = base_pos + tile_last + 1;           // keys the tile sees
@@ -526,20 +532,18 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
         // O^T += V^T P^T: lane holds dims 16db + 4g4 + jj of row i16.
         // Row max of the scaled scores (log2 units) over the stage for both
         // row blocks (lane-local over 16 keys, then the two other lane groups
-        // of the row).  With every page's multiplier positive (the usual
-        // case) the multiply folds into the exponent, p = 2^(raw * mult - m),
-        // and the max is each page's multiplier times its raw max; a zero or
-        // negative multiplier takes the general path -- scale, then mask, so
-        // that masked keys stay at -inf for any scale -- with mult 1.
-        bool positive = true;
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
-            positive &= sl[kb] > 0.0f;
-        float mult[4];
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
-            mult[kb] = positive ? sl[kb] : 1.0f;
-        float sc[kRowBlocks][4][4], mx[kRowBlocks];
+        // of the row).  The multiply folds into the exponent,
+        // p = 2^(raw * mult - m).  Stages below the diagonal see every key:
+        // their max is each page's multiplier times its raw max (bf16 pools
+        // have one multiplier, |scale| log2 e >= 0, Q carrying the scale's
+        // sign), or times its raw min for a negative e4m3 multiplier, taken
+        // with the IEEE maximum instructions, which need no canonicalising
+        // copies of their operands.  Stages on the diagonal mask first: with
+        // every page's multiplier positive the max is again multiplier times
+        // raw max; a zero or negative one takes the general path -- scale,
+        // then mask, so that masked keys stay at -inf for any scale -- with
+        // mult 1.
+        float sc[kRowBlocks][4][4], mx[kRowBlocks], mult[4];
         auto stage_max = [&](auto pre_scaled) {
 #pragma unroll
             for (int rb = 0; rb < kRowBlocks; ++rb) {
@@ -563,10 +567,51 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
                 }
             }
         };
-        if (positive)
-            stage_max(std::false_type{});
-        else
-            stage_max(std::true_type{});
+        if constexpr (!masked) {
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb)
+                mult[kb] = sl[kb];
+#pragma unroll
+            for (int rb = 0; rb < kRowBlocks; ++rb) {
+                const floatx4_t(&x)[4] = sacc[rb];
+                float pm[4];
+#pragma unroll
+                for (int kb = 0; kb < 4; ++kb) {
+                    const float hi = __builtin_elementwise_maximum(
+                        __builtin_elementwise_maximum(x[kb][0], x[kb][1]),
+                        __builtin_elementwise_maximum(x[kb][2], x[kb][3]));
+                    if constexpr (FP8) {
+                        const float lo = __builtin_elementwise_minimum(
+                            __builtin_elementwise_minimum(x[kb][0], x[kb][1]),
+                            __builtin_elementwise_minimum(x[kb][2], x[kb][3]));
+                        pm[kb] = (sl[kb] >= 0.0f ? hi : lo) * sl[kb];
+                    } else {
+                        pm[kb] = hi;  // one multiplier >= 0 for the stage
+                    }
+                }
+                mx[rb] = __builtin_elementwise_maximum(__builtin_elementwise_maximum(pm[0], pm[1]),
+                                                       __builtin_elementwise_maximum(pm[2], pm[3]));
+                if constexpr (!FP8)
+                    mx[rb] *= sl[0];
+#pragma unroll
+                for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                    for (int jj = 0; jj < 4; ++jj)
+                        sc[rb][kb][jj] = x[kb][jj];
+            }
+        } else {
+            bool positive = true;
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb)
+                positive &= sl[kb] > 0.0f;
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb)
+                mult[kb] = positive ? sl[kb] : 1.0f;
+            if (positive)
+                stage_max(std::false_type{});
+            else
+                stage_max(std::true_type{});
+        }
 #pragma unroll
         for (int rb = 0; rb < kRowBlocks; ++rb)
             mx[rb] = max_lanes_xor16(mx[rb]);
@@ -577,7 +622,7 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
 #pragma unroll
         for (int rb = 0; rb < kRowBlocks; ++rb)
             grow |= mx[rb] > m_run[rb] + kMaxSlack;
-        if (__any(grow)) {
+        if (__builtin_expect(__any(grow), 0)) {  // rare: kept out of line
 #pragma unroll
             for (int rb = 0; rb < kRowBlocks; ++rb) {
                 const float m_new = mx[rb] > m_run[rb] + kMaxSlack ? mx[rb] : m_run[rb];
@@ -759,7 +804,8 @@ rl_da_status rl_extend_attn(const void* q, const int32_t* q_start, int32_t max_q
     ea.num_kv_heads = num_kv_heads;
     ea.max_pages = max_pages;
     ea.num_tiles = (max_q_per_seq + tile_tok - 1) / tile_tok;
-    ea.scale_log2 = scale * kLog2e;
+    ea.scale_log2 = fabsf(scale) * kLog2e;
+    ea.q_sign = scale < 0.0f ? 0x80008000u : 0u;
     const int64_t blocks = (int64_t)batch * num_kv_heads * ea.num_tiles;
     if (blocks > INT32_MAX)
         return RL_DA_ERR_UNSUPPORTED;
