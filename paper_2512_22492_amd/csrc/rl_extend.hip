@@ -17,7 +17,9 @@ namespace {
 // two blocks of 16.  The keys the tile can see pass through LDS 64 at a time
 // (four pages, K and V both as [key][dim] rows), double-buffered with one
 // barrier per stage; the next stage's loads are in flight during the current
-// stage's products.  bf16 pages are staged 16 threads per whole key row.
+// stage's products.  bf16 pages go from global memory straight into LDS
+// (direct loads, four whole key rows per instruction); e4m3 pages are
+// widened to bf16 through registers.
 //
 // Both products run transposed so that every lane keeps one query row from
 // the scores to the output.  S^T = K Q^T (v_mfma_f32_16x16x32_bf16, A = 16
