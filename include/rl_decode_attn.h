@@ -230,9 +230,9 @@ rl_da_status rl_decode_attn_unit_heads(const rl_decode_attn* h, int32_t* kv_head
  * entries of pages 0 .. (L_b-1)/page_size in [0, num_pages).  Needs no
  * handle and no workspace; enqueues one kernel on `stream`.  bf16 or e4m3
  * pools (k_scale and v_scale non-NULL exactly for e4m3, as for decode),
- * any rl_da_layout, head_dim 128, page_size 16 and Hq/Hkv in
- * {1, 2, 4, 8, 16} only (else UNSUPPORTED); q, the pools and out 16-byte
- * aligned.
+ * any rl_da_layout, head_dim 128, page_size 16, Hq/Hkv in {1, 2, 4, 8, 16}
+ * and pages (all kv heads) under 2 GiB only (else UNSUPPORTED); q, the pools
+ * and out 16-byte aligned.
  */
 rl_da_status rl_extend_attn(const void* q, const int32_t* q_start, int32_t max_q_per_seq,
                             const void* k_pool, const void* v_pool, const float* k_scale,

@@ -383,19 +383,29 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
     const int dma_slot = 4 * wave + lane / 16;  // key row within its page
     const int dma_chunk = (lane % 16) ^ chunk_swizzle(dma_slot);
     const int dead_slot = (L - 1) % kPageSize;
+    // the lane's byte offset within a page (its key row's slot; under 2^31
+    // like every in-page offset)
+    const int32_t lane_off = kvh * a.head_bytes + dma_slot * a.row_bytes + 16 * dma_chunk;
+    const uint32_t page_bytes32 = (uint32_t)a.page_bytes;  // < 2^31, checked by the host
     auto dma = [&](int stage, const int* pg, auto sel) {  // bf16: into the stage tiles
-#pragma unroll
-        for (int r = 0; r < kStagePages; ++r) {
-            const bool in = stage * kStageKeys + r * kPageSize + dma_slot < L;
-            const int64_t off = (int64_t)pg[r] * a.page_bytes + (int64_t)kvh * a.head_bytes +
-                                (int64_t)(in ? dma_slot : dead_slot) * a.row_bytes +
-                                16 * dma_chunk;
+        auto issue = [&](int r, int64_t off) {
+            off += (int64_t)((uint64_t)(uint32_t)pg[r] * page_bytes32);
             __builtin_amdgcn_global_load_lds((global_void*)(a.k_pool + off),
                                              (lds_void*)&k_tile(sel)[r * kPageSize + 4 * wave][0],
                                              16, 0, 0);
             __builtin_amdgcn_global_load_lds((global_void*)(a.v_pool + off),
                                              (lds_void*)&v_tile(sel)[r * kPageSize + 4 * wave][0],
                                              16, 0, 0);
+        };
+        if ((stage + 1) * kStageKeys <= L) {  // every key of the stage exists
+#pragma unroll
+            for (int r = 0; r < kStagePages; ++r)
+                issue(r, lane_off);
+        } else {  // a key past the end reads the sequence's last key
+            const int32_t dead_off = lane_off + (dead_slot - dma_slot) * a.row_bytes;
+#pragma unroll
+            for (int r = 0; r < kStagePages; ++r)
+                issue(r, stage * kStageKeys + r * kPageSize + dma_slot < L ? lane_off : dead_off);
         }
     };
     // 16 e4m3 codes to 16 bf16 (exact), in order.
@@ -782,6 +792,8 @@ rl_da_status rl_extend_attn(const void* q, const int32_t* q_start, int32_t max_q
     PoolStrides ps;
     if (!pool_strides(layout, num_kv_heads, fp8 ? 1 : 2, &ps))
         return RL_DA_ERR_INVALID_ARG;
+    if (ps.page >= ((int64_t)1 << 31))  // in-page offsets are 32-bit in the kernel
+        return RL_DA_ERR_UNSUPPORTED;
     const int G = num_q_heads / num_kv_heads;
     if (head_dim != kHeadDim || page_size != kPageSize ||
         (G != 1 && G != 2 && G != 4 && G != 8 && G != 16))
