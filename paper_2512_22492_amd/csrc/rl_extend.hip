@@ -652,38 +652,47 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
             }
         }
         // Probabilities as P^T operands: [rb][key half] bf16 x 8 (round to
-        // nearest even; the normaliser sums the unrounded values).
+        // nearest even; the normaliser sums the unrounded values).  Piece
+        // (rb, kb, jp): keys 16kb + 4g4 + 2jp, +1 of row block rb.
+        uint32_t pk[kRowBlocks][4][2];
+        auto make_p = [&](int rb, int kb, int jp) {
+            float p0 = exp2_fast(fmaf(sc[rb][kb][2 * jp], mult[kb], -m_run[rb]));
+            float p1 = exp2_fast(fmaf(sc[rb][kb][2 * jp + 1], mult[kb], -m_run[rb]));
+            if (FP8)
+                lsum[rb] += p0 + p1;
+            if (FP8) {
+                p0 *= vsc[kb];
+                p1 *= vsc[kb];
+            }
+            pk[rb][kb][jp] = pack_bf16x2(p0, p1);
+        };
         uint4 pt[kRowBlocks][2];
+        auto pack_half = [&](int kh) {
 #pragma unroll
-        for (int rb = 0; rb < kRowBlocks; ++rb) {
-            uint32_t pk[4][2];
+            for (int rb = 0; rb < kRowBlocks; ++rb)
+                pt[rb][kh] = make_uint4(pk[rb][2 * kh][0], pk[rb][2 * kh][1],
+                                        pk[rb][2 * kh + 1][0], pk[rb][2 * kh + 1][1]);
+        };
+        // keys 0..31 first
 #pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
+        for (int rb = 0; rb < kRowBlocks; ++rb)
 #pragma unroll
-                for (int jp = 0; jp < 2; ++jp) {
-                    float p0 = exp2_fast(fmaf(sc[rb][kb][2 * jp], mult[kb], -m_run[rb]));
-                    float p1 = exp2_fast(fmaf(sc[rb][kb][2 * jp + 1], mult[kb], -m_run[rb]));
-                    if (FP8)
-                        lsum[rb] += p0 + p1;
-                    if (FP8) {
-                        p0 *= vsc[kb];
-                        p1 *= vsc[kb];
-                    }
-                    pk[kb][jp] = pack_bf16x2(p0, p1);
-                }
+            for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-            for (int kh = 0; kh < 2; ++kh)
-                pt[rb][kh] = make_uint4(pk[2 * kh][0], pk[2 * kh][1], pk[2 * kh + 1][0],
-                                        pk[2 * kh + 1][1]);
-        }
-        // O^T += V^T P^T: lane holds dims 16db + 4g4 + jj of row i16.  The V^T
-        // operand of the next (db, kh) is read before this one's MFMAs.
-        // Lane i16 + 16g4 reads row 32kh + 4g4 + i16/4 (and the row 16
-        // below, same swizzle), dims 16db + 4(i16 % 4) .. +3: chunk
-        // 2db + (i16 % 4)/2, half i16 % 2.
+                for (int jp = 0; jp < 2; ++jp)
+                    make_p(rb, kb, jp);
+        pack_half(0);
+        // O^T += V^T P^T: lane holds dims 16db + 4g4 + jj of row i16.  Steps
+        // run over the first key half's eight dim blocks, then the second's,
+        // so the two products into one accumulator are eight steps apart;
+        // the second half's probabilities are made one piece per step of the
+        // first half.  The V^T operand of the next step is read before this
+        // one's MFMAs.  Lane i16 + 16g4 reads row 32kh + 4g4 + i16/4 (and
+        // the row 16 below, same swizzle), dims 16db + 4(i16 % 4) .. +3:
+        // chunk 2db + (i16 % 4)/2, half i16 % 2.
         const int vrow = 4 * lg + (li >> 2), vsw = chunk_swizzle(vrow);
         auto vt_operand = [&](int step) {
-            const int db = step >> 1, kh = step & 1;
+            const int kh = step >> 3, db = step & 7;
             const int voff = vrow * 256 + 16 * ((2 * db + ((li & 3) >> 1)) ^ vsw) + 8 * (li & 1);
             const uint16_t* vp =
                 reinterpret_cast<const uint16_t*>(vtile + 32 * kh * 256 + voff);
@@ -701,12 +710,17 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
             // keep the read ahead of this step's MFMAs (the scheduler would
             // otherwise sink it next to its own use)
             __builtin_amdgcn_sched_barrier(0);
-            const int db = step >> 1, kh = step & 1;
+            const int kh = step >> 3, db = step & 7;
 #pragma unroll
             for (int rb = 0; rb < kRowBlocks; ++rb) {
                 o[rb][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
                     __builtin_bit_cast(bf16x8_t, vt), __builtin_bit_cast(bf16x8_t, pt[rb][kh]),
                     o[rb][db], 0, 0, 0);
+            }
+            if (step < 8) {
+                make_p(step >> 2, 2 + ((step >> 1) & 1), step & 1);
+                if (step == 7)
+                    pack_half(1);
             }
         }
         if (!FP8) {
