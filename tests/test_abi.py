@@ -167,3 +167,30 @@ def test_noalloc_entry_point_host_checks():
     rc, need = B.rl_decode_attn_workspace_size(big)
     assert rc == B.RL_DA_OK and need > B.RL_DA_NOALLOC_SCRATCH_BYTES
     assert B.rl_decode_attn_run_noalloc(big, *args) == B.RL_DA_ERR_SCRATCH_TOO_SMALL
+
+
+def test_extend_host_checks_without_gpu():
+    """rl_extend_attn refuses bad requests before touching the device: null
+    or misaligned pointers, e4m3 scales given for bf16 pools, shapes it has
+    no kernel for, and pages of 2 GiB or more (its kernels address within a
+    page with 32-bit offsets).  The pointers are never dereferenced."""
+    fake = 1 << 20
+
+    def call(**kw):
+        args = dict(q=fake, q_start=fake, max_q_per_seq=4, k_pool=fake, v_pool=fake,
+                    k_scale=None, v_scale=None, num_pages=16, block_table=fake, max_pages=4,
+                    seq_lens=fake, batch=2, num_q_heads=32, num_kv_heads=8, out=fake)
+        args.update(kw)
+        return B.rl_extend_attn(**args)
+
+    assert call(q=None) == B.RL_DA_ERR_INVALID_ARG
+    assert call(out=fake + 8) == B.RL_DA_ERR_INVALID_ARG             # misaligned
+    assert call(k_scale=fake, v_scale=fake) == B.RL_DA_ERR_INVALID_ARG
+    assert call(layout=3) == B.RL_DA_ERR_INVALID_ARG
+    assert call(head_dim=64) == B.RL_DA_ERR_UNSUPPORTED
+    assert call(num_q_heads=24, num_kv_heads=8) == B.RL_DA_ERR_UNSUPPORTED   # G = 3
+    assert call(num_q_heads=256, num_kv_heads=8) == B.RL_DA_ERR_UNSUPPORTED  # G = 32
+    # 2^19 kv heads: 2 GiB per bf16 page in every layout
+    for layout in (B.RL_DA_LAYOUT_HND, B.RL_DA_LAYOUT_NHD):
+        assert call(num_q_heads=1 << 19, num_kv_heads=1 << 19,
+                    layout=layout) == B.RL_DA_ERR_UNSUPPORTED
