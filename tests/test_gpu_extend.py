@@ -295,3 +295,30 @@ def test_extend_hnd_kv_pools_match_oracle_and_the_hnd_result(kv, hq, hkv):
     check_extend(pk, q, q_start, got, "extend hnd_kv %s G=%d" % (kv, hq // hkv))
     same = run_extend(ph, q, q_start, max(new))
     assert torch.equal(got.view(torch.int16), same.view(torch.int16))
+
+
+@pytest.mark.parametrize("kv", ["bf16", "fp8_e4m3"])
+def test_extend_rows_do_not_depend_on_the_rest_of_the_batch(kv):
+    """A sequence's tiles, their key stages and the order of every sum depend
+    only on its own cached length and new-token count, so its output rows are
+    the same bits extended alone, in a batch, or at another batch position
+    (the work-group order does change with the batch: longest first)."""
+    new, prior = [7, 70, 1, 33, 100], [4000, 17, 900, 2500, 64]
+    p, q, q_start = extend_problem(new, prior, seed=51, hq=32, hkv=8, kv=kv)
+    full = run_extend(p, q, q_start, max(new))
+    starts = q_start.cpu().numpy()
+    for rows in ([1], [3, 0], [4, 2, 1]):
+        idx = torch.as_tensor(rows, device=p.q.device)
+        sub = workloads.DecodeProblem(**{**p.__dict__, "batch": len(rows),
+                                         "block_table": p.block_table[idx].contiguous(),
+                                         "seq_lens": p.seq_lens[idx].contiguous()})
+        sub_new = [new[b] for b in rows]
+        sub_q = torch.cat([q[starts[b]:starts[b + 1]] for b in rows]).contiguous()
+        sub_start = torch.tensor(np.concatenate([[0], np.cumsum(sub_new)]), dtype=torch.int32,
+                                 device=device())
+        got = run_extend(sub, sub_q, sub_start, max(sub_new))
+        at = 0
+        for b, n in zip(rows, sub_new):
+            assert torch.equal(got[at:at + n].view(torch.int16),
+                               full[starts[b]:starts[b] + n].view(torch.int16)), (rows, b)
+            at += n
