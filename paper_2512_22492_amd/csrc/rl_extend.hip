@@ -76,18 +76,19 @@ __device__ __forceinline__ uint2 lds_read_transposed(const uint16_t* p)
 // rows 1 <-> 0 and 3 <-> 2 between its two operands: with both equal to v,
 // lane l receives v of lanes l & ~16 and l | 16), or of lane l ^ 32
 // (permlane32_swap, the two halves).  Vector-ALU operations, no LDS round
-// trip.
+// trip.  The maxima are IEEE `maximum` (no canonicalising copies of the
+// operands); the row maxima they combine are finite or -inf.
 __device__ __forceinline__ float max_lanes_xor16(float v)
 {
     const auto s = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v),
                                                     false, false);
-    return fmaxf(__uint_as_float(s[0]), __uint_as_float(s[1]));
+    return __builtin_elementwise_maximum(__uint_as_float(s[0]), __uint_as_float(s[1]));
 }
 __device__ __forceinline__ float max_lanes_xor32(float v)
 {
     const auto s = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v),
                                                     false, false);
-    return fmaxf(__uint_as_float(s[0]), __uint_as_float(s[1]));
+    return __builtin_elementwise_maximum(__uint_as_float(s[0]), __uint_as_float(s[1]));
 }
 __device__ __forceinline__ float sum_lanes_xor16(float v)
 {
@@ -449,9 +450,9 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
     // (4ks + lg) ^ s, s = chunk_swizzle(li), is 4 (ks ^ (s >> 2)) + (lg ^
     // (s & 3)), so the offset of dims 32ks.. is k_lane + (k_xor ^ 64ks), the
     // two parts in disjoint bits; likewise the V^T operand's chunk (2db + c)
-    // ^ s is 2 (db ^ (s >> 1)) + (c ^ (s & 1)).  Four registers held for the
-    // whole tile replace the per-stage address arithmetic (7% fewer
-    // vector-ALU instructions, 3-4% faster).
+    // ^ s is 2 (db ^ (s >> 1)) + (c ^ (s & 1)).  The twelve offsets (four K
+    // dim blocks, eight V dim blocks) are made once per tile and held in
+    // registers, so a stage spends no vector-ALU instruction on addresses.
     int k_lane, k_xor, v_lane, v_xor;
     {
         const int li = lane & 15, lg = lane >> 4;
@@ -461,7 +462,17 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
         const int vrow = 4 * lg + (li >> 2), vsw = chunk_swizzle(vrow);
         v_lane = vrow * 256 + 16 * (((li & 3) >> 1) ^ (vsw & 1)) + 8 * (li & 1);
         v_xor = 32 * (vsw >> 1);
-        asm volatile("" : "+v"(k_lane), "+v"(k_xor), "+v"(v_lane), "+v"(v_xor));
+    }
+    int koff_t[4], voff_t[8];
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+        koff_t[ks] = (k_xor ^ (64 * ks)) + k_lane;
+        asm volatile("" : "+v"(koff_t[ks]));
+    }
+#pragma unroll
+    for (int db = 0; db < 8; ++db) {
+        voff_t[db] = (v_xor ^ (32 * db)) + v_lane;
+        asm volatile("" : "+v"(voff_t[db]));
     }
     stage_pages(0, pages_next);
     if constexpr (FP8)
@@ -507,11 +518,8 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
 
         // The lane's byte offsets into the stage tiles, the same for both
         // buffers (each buffer's base folds into the LDS instructions'
-        // offset field): one XOR-add each from the four lane values above.
-        int koff[4];
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks)
-            koff[ks] = (k_xor ^ (64 * ks)) + k_lane;
+        // offset field).
+        const int (&koff)[4] = koff_t;
         const char* ktile = reinterpret_cast<const char*>(&k_tile(sel)[0][0]);
         const char* vtile = reinterpret_cast<const char*>(&v_tile(sel)[0][0]);
 
@@ -597,25 +605,35 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
 #pragma unroll
             for (int rb = 0; rb < kRowBlocks; ++rb) {
                 const floatx4_t(&x)[4] = sacc[rb];
-                float pm[4];
+                if constexpr (FP8) {
+                    float pm[4];
 #pragma unroll
-                for (int kb = 0; kb < 4; ++kb) {
-                    const float hi = __builtin_elementwise_maximum(
-                        __builtin_elementwise_maximum(x[kb][0], x[kb][1]),
-                        __builtin_elementwise_maximum(x[kb][2], x[kb][3]));
-                    if constexpr (FP8) {
+                    for (int kb = 0; kb < 4; ++kb) {
+                        const float hi = __builtin_elementwise_maximum(
+                            __builtin_elementwise_maximum(x[kb][0], x[kb][1]),
+                            __builtin_elementwise_maximum(x[kb][2], x[kb][3]));
                         const float lo = __builtin_elementwise_minimum(
                             __builtin_elementwise_minimum(x[kb][0], x[kb][1]),
                             __builtin_elementwise_minimum(x[kb][2], x[kb][3]));
                         pm[kb] = (sl[kb] >= 0.0f ? hi : lo) * sl[kb];
-                    } else {
-                        pm[kb] = hi;  // one multiplier >= 0 for the stage
                     }
+                    mx[rb] = __builtin_elementwise_maximum(
+                        __builtin_elementwise_maximum(pm[0], pm[1]),
+                        __builtin_elementwise_maximum(pm[2], pm[3]));
+                } else {
+                    // one multiplier >= 0 for the stage: the max of the
+                    // sixteen raw scores as a tree of three-input maxima
+                    auto max3 = [](float a, float b, float c) {
+                        return __builtin_elementwise_maximum(__builtin_elementwise_maximum(a, b), c);
+                    };
+                    const float m0 = max3(x[0][0], x[0][1], x[0][2]);
+                    const float m1 = max3(x[0][3], x[1][0], x[1][1]);
+                    const float m2 = max3(x[1][2], x[1][3], x[2][0]);
+                    const float m3 = max3(x[2][1], x[2][2], x[2][3]);
+                    const float m4 = max3(x[3][0], x[3][1], x[3][2]);
+                    mx[rb] = __builtin_elementwise_maximum(max3(m0, m1, m2), max3(m3, m4, x[3][3])) *
+                             sl[0];
                 }
-                mx[rb] = __builtin_elementwise_maximum(__builtin_elementwise_maximum(pm[0], pm[1]),
-                                                       __builtin_elementwise_maximum(pm[2], pm[3]));
-                if constexpr (!FP8)
-                    mx[rb] *= sl[0];
 #pragma unroll
                 for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
@@ -703,7 +721,7 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
         // chunk 2db + (i16 % 4)/2, half i16 % 2.
         auto vt_operand = [&](int step) {
             const int kh = step >> 3, db = step & 7;
-            const int voff = (v_xor ^ (32 * db)) + v_lane;
+            const int voff = voff_t[db];
             const uint16_t* vp =
                 reinterpret_cast<const uint16_t*>(vtile + 32 * kh * 256 + voff);
             const uint2 va = lds_read_transposed(vp);
