@@ -494,9 +494,13 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
             }
             __syncthreads();
         } else {
-            // this stage's direct loads have landed (the barrier waits for
-            // them) and every wavefront is done with the other buffer, which
-            // the next stage's loads fill once the score products are issued
+            // this stage's direct loads have landed and every wavefront is
+            // done with the other buffer, which the next stage's loads fill
+            // once the score products are issued.  The wait for this
+            // wavefront's direct loads is explicit: the fence of the barrier
+            // waits for them only while the compiler tracks them as LDS
+            // writes (a source address built from an integer loses that).
+            __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
             __syncthreads();
         }
 
