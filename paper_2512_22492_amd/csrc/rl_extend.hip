@@ -167,6 +167,21 @@ __device__ int sequence_at_rank(const int32_t* seq_lens, int cap, int batch, int
     return pick;
 }
 
+// A direct global-to-LDS load of 16 bytes per lane, from a per-lane global
+// address to LDS address lds + 16 * lane (lds uniform, in M0), written as
+// inline assembly so that the compiler neither tracks these loads nor waits
+// for them: the kernel waits for its own loads before each stage barrier,
+// and the compiler, not knowing which LDS buffer a load fills, would
+// otherwise wait for it before every read of the other buffer.  (The nop is
+// the wait state between the M0 write and the load that reads it.)
+__device__ __forceinline__ void dma16(const uint8_t* gaddr, uint32_t lds)
+{
+    asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                 :
+                 : "v"(gaddr), "{m0}"(lds)
+                 : "memory");
+}
+
 struct ExtendArgs {
     const uint16_t* q;          // bf16 [T][Hq][D]
     const int32_t* q_start;     // [B+1]
@@ -197,42 +212,16 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
 {
     static_assert(G >= 1 && G <= 16 && 16 % G == 0, "16-row blocks hold whole groups");
     constexpr int kTileTok = kTileRows / G;
-    // Two stage buffers per operand, as separate arrays: the compiler then
-    // tells the buffer being read from the one a direct load is filling and
-    // waits only where a wait is needed.
+    // Two stage buffers per operand: stage j in buffer j % 2.
     __shared__ __attribute__((aligned(16))) uint16_t k_lds0[kStageKeys][kHeadDim];
     __shared__ __attribute__((aligned(16))) uint16_t k_lds1[kStageKeys][kHeadDim];
     __shared__ __attribute__((aligned(16))) uint16_t v_lds0[kStageKeys][kHeadDim];
     __shared__ __attribute__((aligned(16))) uint16_t v_lds1[kStageKeys][kHeadDim];
     // e4m3 pools: (k_scale, v_scale) of the stage's four pages
     __shared__ __attribute__((aligned(16))) float2 scale_lds[2][kStagePages];
-    // A stage buffer is named by a type (bf16: the direct loads need it
-    // static) or by an int (e4m3: staged through registers).
     typedef uint16_t Tile[kStageKeys][kHeadDim];
-    auto buf_index = [](auto sel) -> int {
-        if constexpr (std::is_integral<decltype(sel)>::value)
-            return sel;
-        else
-            return decltype(sel)::value;
-    };
-    auto k_tile = [&](auto sel) -> Tile& {
-        if constexpr (std::is_integral<decltype(sel)>::value)
-            return sel ? k_lds1 : k_lds0;
-        else if constexpr (decltype(sel)::value == 0)
-            return k_lds0;
-        else
-            return k_lds1;
-    };
-    auto v_tile = [&](auto sel) -> Tile& {
-        if constexpr (std::is_integral<decltype(sel)>::value)
-            return sel ? v_lds1 : v_lds0;
-        else if constexpr (decltype(sel)::value == 0)
-            return v_lds0;
-        else
-            return v_lds1;
-    };
-    using Buf0 = std::integral_constant<int, 0>;
-    using Buf1 = std::integral_constant<int, 1>;
+    auto k_tile = [&](int sel) -> Tile& { return sel ? k_lds1 : k_lds0; };
+    auto v_tile = [&](int sel) -> Tile& { return sel ? v_lds1 : v_lds0; };
 
     // Work-group g runs on XCD g % 8.  Pairs (sequence, kv head) are dealt
     // to the XCDs in turn, pair p to XCD p % 8 with all its tiles, so the
@@ -380,7 +369,6 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
         vsr = a.v_scale[slab];
     };
     typedef __attribute__((address_space(3))) void lds_void;
-    typedef __attribute__((address_space(1))) void global_void;
     const int dma_slot = 4 * wave + lane / 16;  // key row within its page
     const int dma_chunk = (lane % 16) ^ chunk_swizzle(dma_slot);
     const int dead_slot = (L - 1) % kPageSize;
@@ -388,15 +376,12 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
     // like every in-page offset)
     const int32_t lane_off = kvh * a.head_bytes + dma_slot * a.row_bytes + 16 * dma_chunk;
     const uint32_t page_bytes32 = (uint32_t)a.page_bytes;  // < 2^31, checked by the host
-    auto dma = [&](int stage, const int* pg, auto sel) {  // bf16: into the stage tiles
+    auto lds_addr = [](const void* p) { return (uint32_t)(uintptr_t)(lds_void*)p; };
+    auto dma = [&](int stage, const int* pg, int sel) {  // bf16: into the stage tiles
         auto issue = [&](int r, int64_t off) {
             off += (int64_t)((uint64_t)(uint32_t)pg[r] * page_bytes32);
-            __builtin_amdgcn_global_load_lds((global_void*)(a.k_pool + off),
-                                             (lds_void*)&k_tile(sel)[r * kPageSize + 4 * wave][0],
-                                             16, 0, 0);
-            __builtin_amdgcn_global_load_lds((global_void*)(a.v_pool + off),
-                                             (lds_void*)&v_tile(sel)[r * kPageSize + 4 * wave][0],
-                                             16, 0, 0);
+            dma16(a.k_pool + off, lds_addr(&k_tile(sel)[r * kPageSize + 4 * wave][0]));
+            dma16(a.v_pool + off, lds_addr(&v_tile(sel)[r * kPageSize + 4 * wave][0]));
         };
         if ((stage + 1) * kStageKeys <= L) {  // every key of the stage exists
 #pragma unroll
@@ -420,7 +405,7 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
         lo = make_uint4(cvt(c.x, F{}), cvt(c.x, T{}), cvt(c.y, F{}), cvt(c.y, T{}));
         hi = make_uint4(cvt(c.z, F{}), cvt(c.z, T{}), cvt(c.w, F{}), cvt(c.w, T{}));
     };
-    auto stash = [&](auto sel) {  // e4m3: widened codes at their swizzled chunks
+    auto stash = [&](int sel) {  // e4m3: widened codes at their swizzled chunks
 #pragma unroll
         for (int r = 0; r < kRowsPerThread; ++r) {
             const int row = slot_row(r);
@@ -442,7 +427,7 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
             *v1 = hi;
         }
         if (threadIdx.x < kStagePages)
-            scale_lds[buf_index(sel)][threadIdx.x] = make_float2(ksr, vsr);
+            scale_lds[sel][threadIdx.x] = make_float2(ksr, vsr);
     };
 
     // LDS operand offsets as a fixed lane part plus an XOR of the block
@@ -478,14 +463,14 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
     if constexpr (FP8)
         fetch(0, pages_next);
     else
-        dma(0, pages_next, Buf0{});
+        dma(0, pages_next, 0);
     stage_pages(1, pages_next);
     // One stage; stages that cannot cross a query position (all but the
     // last one or two of a tile) are compiled without the causal mask.  sel:
     // the stage buffer (j % 2).
-    auto stage = [&](const int j, auto masked_t, auto sel) __attribute__((always_inline)) {
+    auto stage = [&](const int j, auto masked_t, const int sel) __attribute__((always_inline)) {
         constexpr bool masked = decltype(masked_t)::value;
-        const int buf = buf_index(sel);
+        const int buf = sel;
         if constexpr (FP8) {
             stash(sel);
             if (j + 1 < nstages) {
@@ -496,10 +481,9 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
         } else {
             // this stage's direct loads have landed and every wavefront is
             // done with the other buffer, which the next stage's loads fill
-            // once the score products are issued.  The wait for this
-            // wavefront's direct loads is explicit: the fence of the barrier
-            // waits for them only while the compiler tracks them as LDS
-            // writes (a source address built from an integer loses that).
+            // once the score products are issued.  The compiler does not
+            // track the direct loads, so this wavefront waits for its own
+            // here, before the barrier.
             __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
             __syncthreads();
         }
@@ -558,7 +542,7 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
         // reads so that their LDS writes do not compete with them
         if constexpr (!FP8) {
             if (j + 1 < nstages) {
-                dma(j + 1, pages_next, std::integral_constant<int, 1 - decltype(sel)::value>{});
+                dma(j + 1, pages_next, 1 - sel);
                 stage_pages(j + 2, pages_next);
             }
         }
@@ -766,23 +750,10 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
         }
         __builtin_amdgcn_s_setprio(0);
     };
-    // Stage j uses buffer j % 2.  bf16: stages run in pairs, so that each
-    // body names its buffers statically.
     int j = 0;
     auto run = [&](int end, auto masked_t) {
-        if constexpr (FP8) {
-            for (; j < end; ++j)
-                stage(j, masked_t, j & 1);
-        } else {
-            if (j < end && (j & 1) != 0)
-                stage(j++, masked_t, Buf1{});
-            for (; j + 1 < end; j += 2) {
-                stage(j, masked_t, Buf0{});
-                stage(j + 1, masked_t, Buf1{});
-            }
-            if (j < end)
-                stage(j++, masked_t, Buf0{});
-        }
+        for (; j < end; ++j)
+            stage(j, masked_t, j & 1);
     };
     run(min(first_masked_stage, nstages), std::false_type{});
     run(nstages, std::true_type{});
