@@ -50,13 +50,22 @@ constexpr int kTileRows = kUnitWaves * kRowBlocks * 16;
 constexpr int kStageKeys = 64;                     // keys per LDS stage (4 pages)
 constexpr int kStagePages = kStageKeys / kPageSize;
 // K and V stage tiles are [key][dim] rows of 256 bytes whose sixteen 16-byte
-// chunks are stored at position chunk ^ chunk_swizzle(row).  Sixteen
-// consecutive rows then put one chunk at sixteen different positions (the
-// K operand reads), and eight consecutive rows put two adjacent chunks at
-// sixteen (the transposed V reads), so neither meets a bank conflict, while
-// every four rows stay one contiguous kilobyte (what a wavefront's direct
-// global-to-LDS load fills).
-__device__ __forceinline__ int chunk_swizzle(int row) { return ((row & 7) << 1) | ((row >> 3) & 1); }
+// chunks are stored at position chunk ^ chunk_swizzle(row); every four rows
+// stay one contiguous kilobyte (what a wavefront's direct global-to-LDS load
+// fills).  The swizzle keeps both operand reads free of bank conflicts, as
+// measured with the LDS counters on gfx950 (64 banks of 4 bytes):
+// ds_read_b128 serves its 64 lanes sixteen at a time, lanes l and l ^ 1,
+// l ^ 2, l ^ 20, l ^ 24 (and their combinations) together, so the K operand
+// reads (lane 16g + i: row i, chunk (4ks + g) ^ swizzle(i)) need swizzle(r ^
+// d) != swizzle(r) ^ (the g difference) for those lane pairs -- rows r and
+// r ^ 8 in particular, which the XOR with (row & 8) separates (without it
+// the reads were 2-way conflicted); ds_read_b64_tr_b16 serves 32 lanes at a
+// time, so the transposed V reads (eight consecutive rows, two adjacent
+// chunks each) need swizzle(row) >> 1 distinct over eight consecutive rows.
+__device__ __forceinline__ int chunk_swizzle(int row)
+{
+    return (((row & 7) << 1) | ((row >> 3) & 1)) ^ (row & 8);
+}
 
 typedef short short4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) short4_t lds_short4_t;
