@@ -596,6 +596,10 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
             }
         };
         if constexpr (!masked) {
+            // the stage's page multipliers are the same in every lane
+            const bool all_pos =
+                !FP8 || __builtin_amdgcn_readfirstlane((sl[0] >= 0.0f) & (sl[1] >= 0.0f) &
+                                                       (sl[2] >= 0.0f) & (sl[3] >= 0.0f));
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb)
                 mult[kb] = sl[kb];
@@ -604,15 +608,24 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
                 const floatx4_t(&x)[4] = sacc[rb];
                 if constexpr (FP8) {
                     float pm[4];
+                    if (all_pos) {  // every page's multiplier >= 0: raw max times it
 #pragma unroll
-                    for (int kb = 0; kb < 4; ++kb) {
-                        const float hi = __builtin_elementwise_maximum(
-                            __builtin_elementwise_maximum(x[kb][0], x[kb][1]),
-                            __builtin_elementwise_maximum(x[kb][2], x[kb][3]));
-                        const float lo = __builtin_elementwise_minimum(
-                            __builtin_elementwise_minimum(x[kb][0], x[kb][1]),
-                            __builtin_elementwise_minimum(x[kb][2], x[kb][3]));
-                        pm[kb] = (sl[kb] >= 0.0f ? hi : lo) * sl[kb];
+                        for (int kb = 0; kb < 4; ++kb)
+                            pm[kb] = __builtin_elementwise_maximum(
+                                         __builtin_elementwise_maximum(x[kb][0], x[kb][1]),
+                                         __builtin_elementwise_maximum(x[kb][2], x[kb][3])) *
+                                     sl[kb];
+                    } else {
+#pragma unroll
+                        for (int kb = 0; kb < 4; ++kb) {
+                            const float hi = __builtin_elementwise_maximum(
+                                __builtin_elementwise_maximum(x[kb][0], x[kb][1]),
+                                __builtin_elementwise_maximum(x[kb][2], x[kb][3]));
+                            const float lo = __builtin_elementwise_minimum(
+                                __builtin_elementwise_minimum(x[kb][0], x[kb][1]),
+                                __builtin_elementwise_minimum(x[kb][2], x[kb][3]));
+                            pm[kb] = (sl[kb] >= 0.0f ? hi : lo) * sl[kb];
+                        }
                     }
                     mx[rb] = __builtin_elementwise_maximum(
                         __builtin_elementwise_maximum(pm[0], pm[1]),

@@ -92,6 +92,25 @@ def test_extend_matches_oracle(hq, hkv, case):
     check_extend(p, q, q_start, got, "extend G=%d case %d" % (hq // hkv, case))
 
 
+@pytest.mark.parametrize("pattern", ["every_other_negative", "all_negative", "zero_and_negative"])
+def test_extend_fp8_slab_scales_of_either_sign(pattern):
+    """e4m3 slab scales of either sign, or zero: a page whose k_scale is
+    negative turns its largest codes into its smallest scores (below the
+    diagonal its row max comes from the raw minimum), and a zero scale makes
+    all its scores 0."""
+    new, prior = [5, 70, 33, 1, 130], [300, 1000, 17, 4000, 64]
+    p, q, q_start = extend_problem(new, prior, seed=90, kv="fp8_e4m3")
+    if pattern == "every_other_negative":
+        p.k_scale[::2] *= -1.0
+    elif pattern == "all_negative":
+        p.k_scale *= -1.0
+    else:
+        p.k_scale[::3] = 0.0
+        p.k_scale[1::3] *= -1.0
+    got = run_extend(p, q, q_start, max(new))
+    check_extend(p, q, q_start, got, "extend fp8 k_scale " + pattern)
+
+
 def test_extend_qwen3_8b_shapes_sampled():
     new, prior = [512, 300, 77, 1], [4096, 8000, 20, 12000]
     p, q, q_start = extend_problem(new, prior, seed=40, hq=32, hkv=8)
