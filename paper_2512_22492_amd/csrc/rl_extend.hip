@@ -236,17 +236,18 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
     // to the XCDs in turn, pair p to XCD p % 8 with all its tiles, so the
     // tiles that read the same keys share an L2 and every XCD takes every
     // eighth pair of the batch; pairs past the last whole eight follow in
-    // grid order.
+    // grid order.  A pair's last tile (the one that sees the most keys) is
+    // dealt first, so the shortest tiles fill the end of the launch.
     const int T = a.num_tiles;
     const int g = blockIdx.x;
     const int main_units = (int)(gridDim.x / T / 8) * 8 * T;
     int bk, tile;
     if (g < main_units) {
         bk = (g / 8 / T) * 8 + g % 8;
-        tile = (g / 8) % T;
+        tile = T - 1 - (g / 8) % T;
     } else {
         bk = g / T;
-        tile = g % T;
+        tile = T - 1 - g % T;
     }
     // Pairs are taken longest sequence first, so that the longest tiles do
     // not start last and set the end of the launch.
