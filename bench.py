@@ -26,6 +26,8 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+# default warm-up of --op extend, in milliseconds of back-to-back launches
+EXTEND_WARMUP_MS = 60.0
 # PCIe 5.0 x16, one direction: 32 GT/s x 16 lanes x 128/130 / 8
 PCIE5_X16_GBS = 63.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
@@ -101,7 +103,11 @@ def parse_args():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=None,
+                    help="untimed steps before the timed ones (default 5; for --op extend, "
+                         "as many launches as fill %d ms, since a stream of matrix work "
+                         "raises the clock over its first tens of milliseconds)"
+                         % EXTEND_WARMUP_MS)
     ap.add_argument("--config", default="qwen3_8b_step",
                     help="workload name (see paper_2512_22492_amd.workloads.CONFIGS)")
     ap.add_argument("--replicas", type=int, default=2,
@@ -441,8 +447,21 @@ def bench_extend(args, dev):
     q = torch.randn((T, p.num_q_heads, p.head_dim), generator=gen, device=dev).to(torch.bfloat16)
     q_start = torch.arange(0, T + 1, n, dtype=torch.int32, device=dev)
     out = torch.empty_like(q)
-    for _ in range(args.warmup):
-        binding.extend_attention(p, q, q_start, n, out)
+    if args.warmup is None:
+        # launch until EXTEND_WARMUP_MS of back-to-back launches have passed:
+        # under matrix load the clock settles only after tens of milliseconds
+        # (per XCD from about 1.5 to 2.0 GHz over the first ~30 ms, with the
+        # cycle count per launch unchanged)
+        args.warmup = 0
+        t_end = time.perf_counter() + EXTEND_WARMUP_MS / 1e3
+        while args.warmup < 5 or time.perf_counter() < t_end:
+            for _ in range(5):
+                binding.extend_attention(p, q, q_start, n, out)
+            args.warmup += 5
+            torch.cuda.synchronize()
+    else:
+        for _ in range(args.warmup):
+            binding.extend_attention(p, q, q_start, n, out)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
@@ -627,6 +646,8 @@ def main():
     if args.op == "extend":
         print(json.dumps(bench_extend(args, dev)), flush=True)
         return
+    if args.warmup is None:
+        args.warmup = 5
     if args.op == "pack":
         print(json.dumps(bench_pack(args, dev)), flush=True)
         return
