@@ -42,8 +42,9 @@ namespace {
 // Work-group order: consecutive work-groups go to the eight XCDs in turn,
 // and the tiles of one (sequence, kv head) read the same keys, so they are
 // placed on one XCD (one L2) -- see the unit mapping in the kernel.  The
-// sequences are taken longest first (by length class), so that the longest
-// tiles do not start last and set the end of the launch.
+// sequences are taken longest first (by length class), and each pair's
+// tiles last tile first, so that the longest tiles do not start last and
+// set the end of the launch.
 
 constexpr int kRowBlocks = 2;                      // 16-row blocks per wavefront
 constexpr int kTileRows = kUnitWaves * kRowBlocks * 16;
