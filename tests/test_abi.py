@@ -185,6 +185,12 @@ def test_extend_host_checks_without_gpu():
 
     assert call(q=None) == B.RL_DA_ERR_INVALID_ARG
     assert call(out=fake + 8) == B.RL_DA_ERR_INVALID_ARG             # misaligned
+    # nothing to do: success without touching the device
+    assert call(batch=0) == B.RL_DA_OK
+    assert call(max_q_per_seq=0) == B.RL_DA_OK
+    assert call(batch=-1) == B.RL_DA_ERR_INVALID_ARG
+    assert call(max_q_per_seq=-1) == B.RL_DA_ERR_INVALID_ARG
+    assert call(scale=float("nan")) == B.RL_DA_ERR_INVALID_ARG
     assert call(k_scale=fake, v_scale=fake) == B.RL_DA_ERR_INVALID_ARG
     assert call(layout=3) == B.RL_DA_ERR_INVALID_ARG
     assert call(head_dim=64) == B.RL_DA_ERR_UNSUPPORTED
@@ -194,3 +200,32 @@ def test_extend_host_checks_without_gpu():
     for layout in (B.RL_DA_LAYOUT_HND, B.RL_DA_LAYOUT_NHD):
         assert call(num_q_heads=1 << 19, num_kv_heads=1 << 19,
                     layout=layout) == B.RL_DA_ERR_UNSUPPORTED
+
+
+def test_kv_append_host_checks_without_gpu():
+    """rl_kv_append refuses bad requests before touching the device (null or
+    misaligned pointers, scales given exactly for e4m3 pools, shapes it has no
+    kernel for) and succeeds on an empty batch without launching anything.
+    The pointers are never dereferenced."""
+    fake = 1 << 20
+
+    def call(**kw):
+        args = dict(k_new=fake, v_new=fake, k_pool=fake, v_pool=fake, k_scale=None,
+                    v_scale=None, num_pages=16, block_table=fake, max_pages=4, seq_lens=fake,
+                    batch=2, num_kv_heads=8)
+        args.update(kw)
+        return B.rl_kv_append(**args)
+
+    assert call(batch=0) == B.RL_DA_OK
+    assert call(batch=-1) == B.RL_DA_ERR_INVALID_ARG
+    assert call(k_new=None) == B.RL_DA_ERR_INVALID_ARG
+    assert call(seq_lens=None) == B.RL_DA_ERR_INVALID_ARG
+    assert call(v_pool=fake + 8) == B.RL_DA_ERR_INVALID_ARG            # misaligned
+    assert call(num_kv_heads=0) == B.RL_DA_ERR_INVALID_ARG
+    assert call(max_pages=0) == B.RL_DA_ERR_INVALID_ARG
+    assert call(k_scale=fake, v_scale=fake) == B.RL_DA_ERR_INVALID_ARG   # scales on bf16
+    assert call(kv_dtype=B.RL_DA_KV_FP8_E4M3) == B.RL_DA_ERR_INVALID_ARG  # e4m3 without
+    assert call(kv_dtype=7) == B.RL_DA_ERR_INVALID_ARG
+    assert call(layout=3) == B.RL_DA_ERR_INVALID_ARG
+    assert call(head_dim=64) == B.RL_DA_ERR_UNSUPPORTED
+    assert call(page_size=32) == B.RL_DA_ERR_UNSUPPORTED
