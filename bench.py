@@ -13,6 +13,9 @@ starts.  Prints one JSON line:
                steps (the first pass, which gives value, has none)
   cpu_baseline = the fp64 oracle timed on the host on a sample of the step
   parity     = the GPU output of that sample against the oracle's
+--op extend reports TFLOP/s against the bf16 MFMA peak, with the oracle's
+extend attention timed on the launch's first sequences as its cpu_baseline
+and the GPU output's error statistics on them as its parity.
 """
 import argparse
 import json
@@ -278,15 +281,41 @@ def parity_stats(got, ref):
     }
 
 
+class _host_oracle:
+    """Builds the oracle for this host (-O3 -march=native, no FMA contraction:
+    the same results as the test build) in a temporary directory and makes it
+    the library the oracle module calls; yields a description of the build."""
+
+    def __enter__(self):
+        import tempfile
+
+        import oracle
+        self._tmp = tempfile.mkdtemp(prefix="oracle_native_")
+        try:
+            lib, build = oracle.build_native(self._tmp), \
+                "gcc -O3 -march=native -ffp-contract=off -fopenmp"
+        except Exception as e:  # no compiler on this host: the portable build
+            print("bench: native oracle build failed (%s); timing the portable build" % e,
+                  file=sys.stderr, flush=True)
+            lib, build = oracle.LIB_PATH, "gcc -O2 -ffp-contract=off -fopenmp (portable)"
+        self._using = oracle.using_library(lib)
+        self._using.__enter__()
+        return build
+
+    def __exit__(self, *exc):
+        import shutil
+        try:
+            return self._using.__exit__(*exc)
+        finally:
+            shutil.rmtree(self._tmp, ignore_errors=True)
+
+
 def cpu_baseline(p, gpu_out, min_seconds=10.0):
     """Times the oracle on the host, built for this host (-O3 -march=native,
     no FMA contraction: the same results as the test build).  The sample is
     the whole step (every (sequence, head) row) when that is bounded, else
     the first sequences.  The oracle's output of the sample also gives the
     GPU output's error statistics."""
-    import shutil
-    import tempfile
-
     import numpy as np
     import oracle
     kv_code = oracle.KV_BF16 if p.kv_dtype == "bf16" else oracle.KV_FP8_E4M3
@@ -298,34 +327,24 @@ def cpu_baseline(p, gpu_out, min_seconds=10.0):
     nseq = max(1, min(p.batch, nseq))
     rows = np.array([(b, hh) for b in range(nseq) for hh in range(p.num_q_heads)],
                     dtype=np.int32)
-    tmp = tempfile.mkdtemp(prefix="oracle_native_")
-    try:
+    with _host_oracle() as build:
+        # repeat the sample until about min_seconds of CPU work have been timed
+        reps, dt, ref = 0, 0.0, None
+        while reps == 0 or dt < min_seconds:
+            t0 = time.perf_counter()
+            ref = oracle.decode_attention(kv_dtype=kv_code, rows=rows, **h)
+            dt += time.perf_counter() - t0
+            reps += 1
+        cores = oracle.max_threads()
+        # one thread, on the first sequence's rows (a few seconds)
+        rows1 = rows[:p.num_q_heads]
+        oracle.set_threads(1)
         try:
-            lib, build = oracle.build_native(tmp), "gcc -O3 -march=native -ffp-contract=off -fopenmp"
-        except Exception as e:  # no compiler on this host: the portable build
-            print("bench: native oracle build failed (%s); timing the portable build" % e,
-                  file=sys.stderr, flush=True)
-            lib, build = oracle.LIB_PATH, "gcc -O2 -ffp-contract=off -fopenmp (portable)"
-        with oracle.using_library(lib):
-            # repeat the sample until about min_seconds of CPU work have been timed
-            reps, dt, ref = 0, 0.0, None
-            while reps == 0 or dt < min_seconds:
-                t0 = time.perf_counter()
-                ref = oracle.decode_attention(kv_dtype=kv_code, rows=rows, **h)
-                dt += time.perf_counter() - t0
-                reps += 1
-            cores = oracle.max_threads()
-            # one thread, on the first sequence's rows (a few seconds)
-            rows1 = rows[:p.num_q_heads]
-            oracle.set_threads(1)
-            try:
-                t0 = time.perf_counter()
-                oracle.decode_attention(kv_dtype=kv_code, rows=rows1, **h)
-                dt1 = time.perf_counter() - t0
-            finally:
-                oracle.set_threads(cores)
-    finally:
-        shutil.rmtree(tmp, ignore_errors=True)
+            t0 = time.perf_counter()
+            oracle.decode_attention(kv_dtype=kv_code, rows=rows1, **h)
+            dt1 = time.perf_counter() - t0
+        finally:
+            oracle.set_threads(cores)
     elt = 2 if p.kv_dtype == "bf16" else 1
     kv = int(L[:nseq].sum()) * p.num_kv_heads * p.head_dim * 2 * elt * reps
     kv1 = int(L[0]) * p.num_kv_heads * p.head_dim * 2 * elt
@@ -471,7 +490,7 @@ def bench_extend(args, dev):
     visible = sum(int(L) * n + n * (n + 1) // 2 for L in prior)
     flops = 4.0 * p.head_dim * p.num_q_heads * visible
     tf = flops / s / 1e12
-    return {
+    record = {
         "metric": "extend (prefill) attention TFLOP/s, causal, 1 GPU",
         "value": round(tf, 2), "unit": "TFLOP/s", "higher_is_better": True,
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(s * 1e3, 4),
@@ -483,6 +502,70 @@ def bench_extend(args, dev):
         "roofline": {"bound": "mfma", "achieved": round(tf, 2), "peak": 2500.0,
                      "unit": "TFLOP/s", "frac": round(tf / 2500.0, 4)},
     }
+    if not args.no_cpu_baseline:
+        print("bench: timing the CPU oracle", file=sys.stderr, flush=True)
+        record["cpu_baseline"], record["parity"] = extend_cpu_baseline(p, q, n, prior, out)
+    return record
+
+
+def extend_cpu_baseline(p, q, n, prior, gpu_out, min_seconds=10.0):
+    """The oracle's extend attention timed on the host on the launch's first
+    sequences (about 2e10 fp64 multiply-adds for bf16 pools, 2e9 for e4m3
+    ones, whose elements the oracle decodes one by one; one sequence at least),
+    repeated until about min_seconds of CPU work have been timed; its output
+    also gives the GPU output's error statistics on those sequences."""
+    import numpy as np
+    import oracle
+    import torch
+    kv_code = oracle.KV_BF16 if p.kv_dtype == "bf16" else oracle.KV_FP8_E4M3
+    h = p.host_arrays()
+    visible = np.array([int(L) * n + n * (n + 1) // 2 for L in prior], dtype=np.float64)
+    macs = visible * p.num_q_heads * p.head_dim * 2          # both products
+    budget = 2e10 if p.kv_dtype == "bf16" else 2e9
+    nseq = max(1, min(p.batch, int(np.searchsorted(np.cumsum(macs), budget, side="right"))))
+    q_bits = q[:nseq * n].cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+    q_start = np.arange(0, nseq * n + 1, n, dtype=np.int32)
+    kw = dict(num_kv_heads=p.num_kv_heads, scale=p.scale, kv_dtype=kv_code,
+              layout=h["layout"], k_scale=h.get("k_scale"), v_scale=h.get("v_scale"))
+    with _host_oracle() as build:
+        reps, dt, ref = 0, 0.0, None
+        while reps == 0 or dt < min_seconds:
+            t0 = time.perf_counter()
+            ref = oracle.extend_attention(q_bits, q_start, h["k_pool"], h["v_pool"],
+                                          h["block_table"][:nseq], h["seq_lens"][:nseq], **kw)
+            dt += time.perf_counter() - t0
+            reps += 1
+        cores = oracle.max_threads()
+        # M1, the weighted mean of |v| per output: the same attention over
+        # the value pool with every sign bit cleared (bf16 bit 15, e4m3 bit 7)
+        v_abs = h["v_pool"] & (np.uint16(0x7FFF) if h["v_pool"].dtype == np.uint16
+                               else np.uint8(0x7F))
+        m1 = oracle.extend_attention(q_bits, q_start, h["k_pool"], v_abs,
+                                     h["block_table"][:nseq], h["seq_lens"][:nseq], **kw)
+    got = gpu_out[:nseq * n].float().cpu().numpy().astype(np.float64).reshape(ref.shape)
+    flops = 4.0 * p.head_dim * p.num_q_heads * float(visible[:nseq].sum()) * reps
+    parity = parity_stats(got, ref)
+    # The kernel rounds each weight to bf16 before the value product (8
+    # significant bits, relative error <= 2^-8); with the normaliser summing
+    # the same rounded weights (bf16 pools) an output moves by at most
+    # 2^-8 (1 + 2^-7) (M1 + |o|), with the unrounded ones (e4m3 pools) by
+    # 2^-8 (1 + 2^-7) M1, on top of one bf16 ulp of the output plus 1e-6.
+    # The decode kernels' one-ulp gate does not apply here.
+    del parity["max_err_over_ulp_gate"]
+    p_round = 2.0 ** -8 * (1.0 + 2.0 ** -7)
+    extra = p_round * (np.abs(m1) + (np.abs(ref) if p.kv_dtype == "bf16" else 0.0))
+    parity["max_err_over_weight_bound"] = round(float(
+        (np.abs(got - ref) / (_bf16_ulp(ref) + 1e-6 + extra)).max()), 4)
+    return {
+        "value": flops / dt / 1e12,
+        "unit": "TFLOP/s",
+        "cores": cores,
+        "kind": "oracle",
+        "sample": "%d of %d sequences (%d new tokens each, every query head), fp64, %d passes "
+                  "in %.2f s" % (nseq, p.batch, n, reps, dt),
+        "build": build,
+        "cpu_model": _cpu_model(),
+    }, parity
 
 
 # Qwen3-8B weight tensors of one decoder layer, [out, in] (bf16): q, k, v, o
