@@ -625,6 +625,12 @@ def bench_pack(args, dev):
                 ws.pack(c, stream)
         s = _time_launches(step, args.steps, args.warmup)
         chunks = ws.num_chunks
+        torch.cuda.synchronize()
+        baseline = None
+        if not args.no_cpu_baseline:
+            # the buffer holds the last chunk of the last step
+            print("bench: timing the CPU oracle", file=sys.stderr, flush=True)
+            baseline = weight_sync_cpu_baseline(tensors, buf.cpu().numpy(), chunks - 1, cap, 256)
     # plain device copy of one buffer's worth, for the achievable copy rate
     copy_s = None
     if not args.no_ceilings:
@@ -634,7 +640,7 @@ def bench_pack(args, dev):
                                                           stream.cuda_stream), 10, 2)
     gbs = total / s / 1e9
     hbm = 2 * total / s / 1e9
-    return {
+    record = {
         "metric": "weight-sync pack GB/s of weights (layer by layer into a transfer buffer), 1 GPU",
         "value": round(gbs, 1), "unit": "GB/s", "higher_is_better": True,
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(s * 1e3, 4),
@@ -647,6 +653,41 @@ def bench_pack(args, dev):
                      "bytes_per_launch": 2 * total // chunks},
         "plain_copy_GBs_rw": None if copy_s is None else round(2 * cap / copy_s / 1e9, 1),
     }
+    if baseline is not None:
+        record["cpu_baseline"], record["parity"] = baseline
+    return record
+
+
+def weight_sync_cpu_baseline(tensors, gpu_buffer, chunk, capacity, align, min_seconds=5.0):
+    """The oracle's pack of one chunk (numpy, one thread) timed on the host,
+    repeated until about min_seconds, and the GPU's buffer for that chunk
+    compared with it byte for byte over every byte the chunk's pieces write."""
+    import numpy as np
+    import torch
+    from oracle import weight_sync as ows
+    sizes = [t.numel() * t.element_size() for t in tensors]
+    pieces = ows.plan(sizes, capacity, align)
+    used = sorted({t for t, c, _, _, _ in pieces if c == chunk})
+    host = [np.empty(0, dtype=np.uint8)] * len(tensors)
+    for i in used:
+        host[i] = tensors[i].detach().contiguous().view(torch.uint8).reshape(-1).cpu().numpy()
+    reps, dt = 0, 0.0
+    while reps == 0 or dt < min_seconds:
+        t0 = time.perf_counter()
+        ref, written = ows.pack(host, pieces, chunk, capacity)
+        dt += time.perf_counter() - t0
+        reps += 1
+    nbytes = int(written.sum())
+    mismatches = int(np.count_nonzero(gpu_buffer[:capacity][written] != ref[written]))
+    return {
+        "value": nbytes * reps / dt / 1e9,
+        "unit": "GB/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": "chunk %d (%d bytes of %d tensors), numpy, %d passes in %.2f s"
+                  % (chunk, nbytes, len(used), reps, dt),
+        "cpu_model": _cpu_model(),
+    }, {"bytes_compared": nbytes, "mismatched_bytes": mismatches, "bit_exact": mismatches == 0}
 
 
 def bench_d2h(args, dev):
@@ -663,10 +704,16 @@ def bench_d2h(args, dev):
     with binding.WeightSync(tensors, host, align=256) as ws:
         assert ws.num_chunks == 1
         s = _time_launches(lambda: ws.pack(0, stream), args.steps, args.warmup)
+        torch.cuda.synchronize()
+        baseline = None
+        if not args.no_cpu_baseline:
+            # before the runtime copy below overwrites the host buffer
+            print("bench: timing the CPU oracle", file=sys.stderr, flush=True)
+            baseline = weight_sync_cpu_baseline(tensors, host.numpy(), 0, cap, 256)
     flat = torch.empty(total, dtype=torch.uint8, device=dev)
     dma_s = _time_launches(lambda: host[:total].copy_(flat, non_blocking=True), 5, 1)
     gbs = total / s / 1e9
-    return {
+    record = {
         "metric": "checkpoint GPU-to-host copy GB/s (pinned host memory), 1 GPU",
         "value": round(gbs, 2), "unit": "GB/s", "higher_is_better": True,
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(s * 1e3, 3),
@@ -677,6 +724,9 @@ def bench_d2h(args, dev):
                      "unit": "GB/s", "frac": round(gbs / PCIE5_X16_GBS, 4)},
         "dma_copy_GBs": round(total / dma_s / 1e9, 2),
     }
+    if baseline is not None:
+        record["cpu_baseline"], record["parity"] = baseline
+    return record
 
 
 def traffic_key(args):
