@@ -420,22 +420,44 @@ def bench_append(args, base, stream):
         # append at the last slot of the last page instead of past the table
         base.seq_lens.copy_(torch.from_numpy(np.minimum(L, base.max_pages * base.page_size - 1)
                                              .astype(np.int32)).to(base.seq_lens.device))
+    # A token that opens a page goes to a page of its own, taken from the
+    # pool's unused pages, as a serving engine would allocate it (the table's
+    # padding slots all name one shared page, which several sequences would
+    # otherwise write at once).
+    L = base.lengths()
+    table = base.block_table.cpu().numpy().copy()
+    opens = (L % base.page_size == 0) & (L // base.page_size < base.max_pages)
+    if opens.any():
+        in_use = np.zeros(base.num_pages, dtype=bool)
+        in_use[table.reshape(-1)] = True
+        free = np.flatnonzero(~in_use)
+        if free.size < int(opens.sum()):
+            raise SystemExit("the pool has too few unused pages for the new tokens")
+        rows = np.flatnonzero(opens)
+        table[rows, L[rows] // base.page_size] = free[:rows.size]
+        base.block_table.copy_(torch.from_numpy(table).to(base.block_table.device))
     gen = torch.Generator(device=base.q.device).manual_seed(1)
     shape = (base.batch, base.num_kv_heads, base.head_dim)
     k = torch.randn(shape, generator=gen, device=base.q.device).to(torch.bfloat16)
     v = torch.randn(shape, generator=gen, device=base.q.device).to(torch.bfloat16)
+    # the cache before the first append, for the oracle leg (appending the
+    # same tokens at the same lengths again changes nothing: an e4m3 page's
+    # scale only grows, to the largest token's absmax / 448)
+    before = None if args.no_cpu_baseline else base.host_arrays()
+    # the cache is checked once; each call checks only the new tokens
+    append = binding.KvAppender(base)
     for _ in range(args.warmup):
-        binding.kv_append(base, k, v, stream=stream)
+        append(k, v, stream=stream)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        binding.kv_append(base, k, v, stream=stream)
+        append(k, v, stream=stream)
     torch.cuda.synchronize()
     us = (time.perf_counter() - t0) * 1e6 / args.steps
     elt = 2 if base.kv_dtype == "bf16" else 1
     tok = base.batch * base.num_kv_heads * base.head_dim
     moved = 2 * (tok * 2 + tok * elt) + base.batch * 8   # read new K/V, write slots, table
-    return {
+    record = {
         "metric": "KV-cache append (one token per sequence) us per call, 1 GPU",
         "value": round(us, 3), "unit": "us", "higher_is_better": False,
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
@@ -445,6 +467,49 @@ def bench_append(args, base, stream):
                    "layout": base.layout},
         "bytes_per_call": moved, "GBs": round(moved / us / 1e3, 2),
     }
+    if before is not None:
+        print("bench: timing the CPU oracle", file=sys.stderr, flush=True)
+        record["cpu_baseline"], record["parity"] = append_cpu_baseline(base, before, k, v)
+    return record
+
+
+def append_cpu_baseline(p, before, k, v, min_seconds=5.0):
+    """The oracle's append of the same tokens to the cache as it was before
+    the first call, timed on the host (whole step; the oracle returns updated
+    copies of the pools, so copying them is part of its time), and the GPU's
+    pools and scales after the timed calls compared with it byte for byte."""
+    import numpy as np
+    import oracle
+    import torch
+    kv_code = oracle.KV_BF16 if p.kv_dtype == "bf16" else oracle.KV_FP8_E4M3
+    bits = lambda t: t.cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+    kw = dict(kv_dtype=kv_code, layout=before["layout"], k_scale=before.get("k_scale"),
+              v_scale=before.get("v_scale"))
+    reps, dt = 0, 0.0
+    while reps == 0 or dt < min_seconds:
+        t0 = time.perf_counter()
+        ref = oracle.kv_append(bits(k), bits(v), before["k_pool"], before["v_pool"],
+                               before["block_table"], before["seq_lens"], **kw)
+        dt += time.perf_counter() - t0
+        reps += 1
+    after = p.host_arrays()
+    names = ["k_pool", "v_pool"] + (["k_scale", "v_scale"] if p.kv_dtype != "bf16" else [])
+    compared = mismatched = 0
+    for name, want in zip(names, ref):
+        got = np.ascontiguousarray(after[name]).view(np.uint8).reshape(-1)
+        want = np.ascontiguousarray(want).view(np.uint8).reshape(-1)
+        compared += want.size
+        mismatched += int(np.count_nonzero(got != want))
+    return {
+        "value": dt / reps * 1e6,
+        "unit": "us",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": "the whole step (%d sequences x %d kv heads), %d calls in %.2f s"
+                  % (p.batch, p.num_kv_heads, reps, dt),
+        "cpu_model": _cpu_model(),
+    }, {"bytes_compared": compared, "mismatched_bytes": mismatched,
+        "bit_exact": mismatched == 0}
 
 
 def bench_extend(args, dev):

@@ -204,20 +204,23 @@ def _check_tensor(name, t, *, dtype=None, shape=None, ndim=None, device=None,
                   contiguous=True):
     """Raises ValueError unless t is a (contiguous) torch tensor of the given
     dtype, shape (None entries match anything) and device."""
+    # called on every entry point's every tensor: the common case (exact
+    # dtype, exact shape) takes the cheap comparisons first
     if not hasattr(t, "data_ptr") or not hasattr(t, "is_contiguous"):
         raise ValueError("%s must be a torch tensor" % name)
-    if dtype is not None and t.dtype not in (dtype if isinstance(dtype, tuple) else (dtype,)):
+    if dtype is not None and t.dtype != dtype and (not isinstance(dtype, tuple)
+                                                   or t.dtype not in dtype):
         raise ValueError("%s has dtype %s, expected %s" % (name, t.dtype, dtype))
     if contiguous and not t.is_contiguous():
         raise ValueError("%s must be contiguous" % name)
     if ndim is not None and t.dim() != ndim:
         raise ValueError("%s must have %d dimensions, has shape %s" % (name, ndim, tuple(t.shape)))
     if shape is not None:
-        if t.dim() != len(shape) or any(w is not None and int(d) != int(w)
-                                        for d, w in zip(t.shape, shape)):
+        ts = tuple(t.shape)
+        if ts != tuple(shape) and (len(ts) != len(shape) or any(
+                w is not None and d != w for d, w in zip(ts, shape))):
             raise ValueError("%s has shape %s, expected %s"
-                             % (name, tuple(t.shape), tuple("*" if w is None else w
-                                                            for w in shape)))
+                             % (name, ts, tuple("*" if w is None else w for w in shape)))
     if device is not None and t.device != device:
         raise ValueError("%s is on %s, expected %s" % (name, t.device, device))
 
@@ -377,26 +380,46 @@ def rl_kv_append(k_new, v_new, k_pool, v_pool, k_scale, v_scale, num_pages, bloc
         _ptr(device_error), _stream(stream))
 
 
+class KvAppender:
+    """rl_kv_append for a loop that appends to one cache step after step:
+    checks problem p's pools, scales, block table and lengths once, here, and
+    only the new tokens on each call.  Those cache tensors must keep their
+    storage, dtype and shape while the appender is used (their contents may
+    change: the table and lengths are read by the kernel on every call)."""
+
+    def __init__(self, p, device_error=None):
+        import torch
+        self.kv_dtype = RL_DA_KV_BF16 if p.kv_dtype == "bf16" else RL_DA_KV_FP8_E4M3
+        self.device = p.k_pool.device
+        self.want = (p.batch, p.num_kv_heads, p.head_dim)
+        _check_pools(p.k_pool, p.v_pool, p.k_scale, p.v_scale, kv_dtype=self.kv_dtype,
+                     layout=LAYOUTS[p.layout], num_kv_heads=p.num_kv_heads,
+                     head_dim=p.head_dim, page_size=p.page_size, device=self.device)
+        _check_table(p.block_table, p.seq_lens, p.batch, self.device)
+        if device_error is not None:
+            _check_tensor("device_error", device_error, dtype=torch.int32, device=self.device)
+        self._fn = load_library().rl_kv_append
+        self._cache_args = (
+            _ptr(p.k_pool), _ptr(p.v_pool), _ptr(p.k_scale), _ptr(p.v_scale),
+            int(p.num_pages), _ptr(p.block_table), int(p.max_pages), _ptr(p.seq_lens),
+            int(p.batch), int(p.num_kv_heads), int(p.head_dim), int(p.page_size),
+            int(self.kv_dtype), int(LAYOUTS[p.layout]), _ptr(device_error))
+
+    def __call__(self, k_new, v_new, stream=None):
+        """Appends k_new/v_new [B, Hkv, D] (bf16) at positions seq_lens;
+        raises on a bad status."""
+        import torch
+        _check_tensor("k_new", k_new, dtype=torch.bfloat16, shape=self.want, device=self.device)
+        _check_tensor("v_new", v_new, dtype=torch.bfloat16, shape=self.want, device=self.device)
+        rc = self._fn(k_new.data_ptr(), v_new.data_ptr(), *self._cache_args, _stream(stream))
+        if rc != RL_DA_OK:
+            raise RLDecodeAttnError(rc, "rl_kv_append")
+
+
 def kv_append(p, k_new, v_new, device_error=None, stream=None):
     """Appends k_new/v_new [B, Hkv, D] (bf16 tensors) to problem p's pools at
     positions p.seq_lens; raises on a bad status."""
-    import torch
-    dt = RL_DA_KV_BF16 if p.kv_dtype == "bf16" else RL_DA_KV_FP8_E4M3
-    dev = p.k_pool.device
-    want = (p.batch, p.num_kv_heads, p.head_dim)
-    _check_tensor("k_new", k_new, dtype=torch.bfloat16, shape=want, device=dev)
-    _check_tensor("v_new", v_new, dtype=torch.bfloat16, shape=want, device=dev)
-    _check_pools(p.k_pool, p.v_pool, p.k_scale, p.v_scale, kv_dtype=dt,
-                 layout=LAYOUTS[p.layout], num_kv_heads=p.num_kv_heads, head_dim=p.head_dim,
-                 page_size=p.page_size, device=dev)
-    _check_table(p.block_table, p.seq_lens, p.batch, dev)
-    if device_error is not None:
-        _check_tensor("device_error", device_error, dtype=torch.int32, device=dev)
-    rc = rl_kv_append(k_new, v_new, p.k_pool, p.v_pool, p.k_scale, p.v_scale, p.num_pages,
-                      p.block_table, p.max_pages, p.seq_lens, p.batch, p.num_kv_heads,
-                      p.head_dim, p.page_size, dt, LAYOUTS[p.layout], device_error, stream)
-    if rc != RL_DA_OK:
-        raise RLDecodeAttnError(rc, "rl_kv_append")
+    KvAppender(p, device_error)(k_new, v_new, stream)
 
 
 def rl_decode_attn_set_timing_events(h, split_begin, split_end) -> int:
