@@ -270,29 +270,6 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
     const int h0 = kvh * G;
     const int base_pos = L - n_new;  // position of new token 0
 
-    // Q^T operand and the causal limit of this lane's row in each block.
-    uint4 qb[kRowBlocks][4];
-    int row_pos[kRowBlocks];
-    bool row_real[kRowBlocks];
-#pragma unroll
-    for (int rb = 0; rb < kRowBlocks; ++rb) {
-        const int r = wave * (kRowBlocks * 16) + rb * 16 + i16;
-        const int qi = tok0 + r / G;
-        row_real[rb] = qi < n_new;
-        row_pos[rb] = base_pos + qi;
-        const uint16_t* qrow =
-            a.q + ((int64_t)(q0 + (row_real[rb] ? qi : 0)) * a.num_q_heads + h0 + r % G) *
-                      kHeadDim;
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-            uint4 v = *reinterpret_cast<const uint4*>(qrow + 32 * ks + 8 * g4);
-            v.x ^= a.q_sign;
-            v.y ^= a.q_sign;
-            v.z ^= a.q_sign;
-            v.w ^= a.q_sign;
-            qb[rb][ks] = row_real[rb] ? v : make_uint4(0, 0, 0, 0);
-        }
-    }
     const int tile_last = min(tok0 + kTileTok, n_new) - 1;
     const int nkeys = base_pos + tile_last + 1;           // keys the tile sees
     const int nstages = (nkeys + kStageKeys - 1) / kStageKeys;
@@ -476,6 +453,41 @@ __attribute__((amdgpu_waves_per_eu(2))) void extend_attn(ExtendArgs a)
     else
         dma(0, pages_next, 0);
     stage_pages(1, pages_next);
+    // Q^T operand and the causal limit of this lane's row in each block,
+    // read after the first stage's loads are issued (loads complete in order,
+    // so the table reads those loads need wait for nothing else).  The eight
+    // loads go first and unconditionally (a row past the tile's tokens reads
+    // the sequence's first query), then the sign flip and a mask: a select on
+    // each loaded value became a branch around its load, and every branch
+    // waited for its load before the next one was issued.
+    uint4 qb[kRowBlocks][4];
+    int row_pos[kRowBlocks];
+    bool row_real[kRowBlocks];
+#pragma unroll
+    for (int rb = 0; rb < kRowBlocks; ++rb) {
+        const int r = wave * (kRowBlocks * 16) + rb * 16 + i16;
+        const int qi = tok0 + r / G;
+        row_real[rb] = qi < n_new;
+        row_pos[rb] = base_pos + qi;
+        const uint16_t* qrow =
+            a.q + ((int64_t)(q0 + (row_real[rb] ? qi : 0)) * a.num_q_heads + h0 + r % G) *
+                      kHeadDim;
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks)
+            qb[rb][ks] = *reinterpret_cast<const uint4*>(qrow + 32 * ks + 8 * g4);
+    }
+#pragma unroll
+    for (int rb = 0; rb < kRowBlocks; ++rb) {
+        const uint32_t keep = row_real[rb] ? 0xFFFFFFFFu : 0u;
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+            uint4& v = qb[rb][ks];
+            v.x = (v.x ^ a.q_sign) & keep;
+            v.y = (v.y ^ a.q_sign) & keep;
+            v.z = (v.z ^ a.q_sign) & keep;
+            v.w = (v.w ^ a.q_sign) & keep;
+        }
+    }
     // One stage; stages that cannot cross a query position (all but the
     // last one or two of a tile) are compiled without the causal mask.  sel:
     // the stage buffer (j % 2).
